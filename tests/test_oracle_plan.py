@@ -1,0 +1,118 @@
+"""Pins for the planner oracle (CPU only).
+
+- hand-worked costs, Eq. 3 values, greedy assignments and optima
+  (tests/golden/plan_worked_example.txt);
+- brute force on tiny inputs: the greedy never beats the optimum, and when
+  the capacity does not bind it stays within Graham's LPT bound
+  (4/3 - 1/(3M)) * OPT;
+- special cases with known answers (n <= M, equal costs, one microbatch);
+- I8: each sample at most once, capacity respected.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle.plan import brute_force, cost_scaled, eq3_cost, greedy_partition, imbalance, members
+from conftest import read_golden
+
+
+def _kv_lists(fields):
+    """'K 10 C 15 M 2 lengths 5 9 ...' -> dict of name -> list of ints."""
+    out, key = {}, None
+    for f in fields:
+        if f.lstrip("-").isdigit():
+            out[key].append(int(f))
+        else:
+            key = f
+            out[key] = []
+    return out
+
+
+def test_worked_examples():
+    seen = set()
+    for ln in read_golden("plan_worked_example.txt"):
+        f = ln.split()
+        seen.add(f[0])
+        if f[0] == "cost":
+            assert cost_scaled(int(f[1]), int(f[2])) == int(f[3])
+        elif f[0] == "eq3":
+            L = int(f[1])
+            eq = f.index("=")
+            lens = [int(x) for x in f[2:eq]]
+            assert math.isclose(eq3_cost(lens, L), float(f[eq + 1]), rel_tol=1e-15)
+        elif f[0] == "greedy":
+            arrow = f.index("->")
+            a = _kv_lists(f[1:arrow])
+            b = _kv_lists(f[arrow + 1:])
+            assign, tok, cst = greedy_partition(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
+            assert assign == b["assign"] and tok == b["tokens"] and cst == b["cost"]
+        elif f[0] == "opt":
+            eq = f.index("=")
+            a = _kv_lists(f[1:eq])
+            opt, _ = brute_force(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
+            assert opt == int(f[eq + 1])
+    assert seen == {"cost", "eq3", "greedy", "opt"}
+
+
+def _check_plan(lengths, capacity, n_mb, assign, tok, cst, k):
+    assert len(assign) == len(lengths)
+    for j in range(n_mb):
+        mem = [i for i, a in enumerate(assign) if a == j]
+        assert sum(lengths[i] for i in mem) == tok[j] <= capacity
+        assert sum(cost_scaled(lengths[i], k) for i in mem) == cst[j]
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_brute_force_bounds(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 8))
+    M = int(rng.integers(1, 4))
+    K = int(rng.integers(1, 50))
+    lengths = [int(x) for x in rng.integers(1, 40, size=n)]
+    binding = bool(rng.integers(0, 2))
+    C = int(rng.integers(max(lengths), 2 * max(lengths) + 1)) if binding else sum(lengths)
+    assign, tok, cst = greedy_partition(lengths, K, C, M)
+    _check_plan(lengths, C, M, assign, tok, cst, K)
+    opt, lex = brute_force(lengths, K, C, M)
+    if -1 not in assign:
+        assert opt is not None and max(cst) >= opt
+    assert sum(tok) <= lex[0]
+    if not binding:
+        assert -1 not in assign
+        assert max(cst) <= (4 / 3 - 1 / (3 * M)) * opt + 1e-9
+
+
+def test_greedy_strictly_worse_than_opt_within_bound():
+    # Classic LPT example; the ratio approaches Graham's 7/6 for M = 2.
+    for K in (10, 1000, 10 ** 6):
+        lengths = [3, 3, 2, 2, 2]
+        _, _, cst = greedy_partition(lengths, K, 100, 2)
+        opt, _ = brute_force(lengths, K, 100, 2)
+        assert max(cst) == 7 * K + 17 and opt == 6 * K + 18
+        assert opt < max(cst) <= (4 / 3 - 1 / 6) * opt
+
+
+def test_special_cases():
+    # n <= M: one sample per microbatch, max cost = the largest sample's cost.
+    lengths = [5, 17, 3]
+    a, tok, cst = greedy_partition(lengths, 8, 100, 4)
+    assert sorted(a) == [0, 1, 2] and max(cst) == cost_scaled(17, 8) == brute_force(lengths, 8, 100, 4)[0]
+    # n = q*M equal lengths: q per microbatch, optimal.
+    a, tok, cst = greedy_partition([7] * 12, 5, 1000, 4)
+    assert tok == [21] * 4 and cst == [3 * cost_scaled(7, 5)] * 4
+    # M = 1: longest first, everything that still fits.
+    a, tok, cst = greedy_partition([4, 9, 2, 6], 3, 12, 1)
+    assert a == [-1, 0, 0, -1] and tok == [11]
+    # Nothing fits.
+    a, tok, cst = greedy_partition([13, 20], 3, 12, 2)
+    assert a == [-1, -1] and tok == [0, 0]
+    # Empty input.
+    assert greedy_partition([], 3, 12, 2) == ([], [0, 0], [0, 0])
+
+
+def test_members_keep_input_order_and_imbalance():
+    assign = [1, 0, 1, -1, 0]
+    assert members(assign, 3) == [[1, 4], [0, 2], []]
+    assert imbalance([2, 4, 6]) == 1.5

@@ -1,0 +1,195 @@
+"""Pins for the pool oracle's addressing and allocation (CPU only).
+
+- hand-worked allocation and GVA sequences (tests/golden/allocator_worked_example.txt)
+  from the segment arithmetic of Sec. 3.2;
+- allocator invariants: pages conserved, no page in two samples, freed pages
+  reused, contiguous runs under "contig", all-or-nothing failure;
+- every page GVA lies in its tier's region and in this rank's segment, and
+  translation finds the frame that holds the row (Sec. 3.2);
+- a tier-masked pack split into the HBM part and the DRAM part equals one
+  full pack.
+"""
+
+import numpy as np
+import pytest
+
+from oracle.pool import MASK_HBM, MASK_HOST, OraclePool, PoolError
+from paper_2606_23087_amd.workloads import CONFIGS, churn_ops, gen_samples, scaled
+from tagging import tagged_table, tagged_vis
+from conftest import read_golden
+
+
+def _golden_blocks():
+    blocks, cur = [], None
+    for ln in read_golden("allocator_worked_example.txt"):
+        f = ln.split()
+        if f[0] == "pool":
+            kv = dict(zip(f[2::2], f[3::2]))
+            cur = {"alloc": f[1], "kv": kv, "ops": []}
+        elif f[0] == "end":
+            blocks.append(cur)
+        else:
+            cur["ops"].append(f)
+    return blocks
+
+
+@pytest.mark.parametrize("block", range(4))
+def test_allocator_worked_example(block):
+    b = _golden_blocks()[block]
+    kv = b["kv"]
+    pool = OraclePool(hidden=int(kv["hidden"]), page_tokens=int(kv["page_tokens"]),
+                      hbm_pages=int(kv["hbm"]), host_pages=int(kv["host"]), alloc=b["alloc"],
+                      gva_start=int(kv["start"], 16), world_size=int(kv["world"]), rank=int(kv["rank"]))
+    names = {}
+    for op in b["ops"]:
+        if op[0] == "free":
+            pool.free(names.pop(op[1]))
+            continue
+        arrow = op.index("->")
+        nvis = int(op[3])
+        wish = [int(x) for x in op[5:arrow]] if "wish" in op else None
+        expect = op[arrow + 1:]
+        before = (pool.free_pages(), [list(s) for s in pool.stack])
+        if expect == ["ENOMEM"]:
+            with pytest.raises(PoolError) as e:
+                pool.write([1], [0], [nvis], tier_wish=wish)
+            assert e.value.code == "ENOMEM"
+            assert (pool.free_pages(), [list(s) for s in pool.stack]) == before
+            continue
+        sid = pool.write([1], [0], [nvis], tier_wish=wish)
+        names[op[1]] = sid
+        assert pool.sample_pages(sid) == [int(x, 16) for x in expect]
+
+
+def test_gva_segments_and_translation():
+    """I9: page GVAs lie in [region start, start + ws*max) and in this rank's
+    [start + r*max, start + (r+1)*max); translating any row address gives the
+    frame and offset that hold the row."""
+    H, P = 8, 4
+    for ws, rank in [(1, 0), (4, 2), (3, 2)]:
+        pool = OraclePool(hidden=H, page_tokens=P, hbm_pages=10, host_pages=6, alloc="scatter",
+                          world_size=ws, rank=rank, frame_order=[list(range(9, -1, -1)), [3, 1, 4, 0, 5, 2]])
+        mx = [10 * P * 2 * H, 6 * P * 2 * H]
+        assert pool.region_start[1] == pool.region_start[0] + ws * mx[0]
+        rng = np.random.default_rng(ws)
+        for i in range(5):
+            n = int(rng.integers(1, 10))
+            rows = tagged_vis(i, n, H)
+            sid = pool.write([0], [0], [n], rows, tier_wish=rng.integers(0, 2, size=-(-n // P)))
+            for v, gva in enumerate(pool.sample_pages(sid)):
+                tier = 0 if gva < pool.region_start[1] else 1
+                assert pool.region_start[tier] <= gva < pool.region_start[tier] + ws * mx[tier]
+                assert pool.region_start[tier] + rank * mx[tier] <= gva < pool.region_start[tier] + (rank + 1) * mx[tier]
+                assert (gva - pool.seg_start[tier]) % pool.pb == 0
+            for v in range(n):
+                gva = pool.sample_pages(sid)[v // P] + (v % P) * pool.rb
+                t, frame, off = pool.translate(gva)
+                assert np.array_equal(pool.frames[t][frame][off // pool.rb], rows[v])
+
+
+def test_conservation_and_reuse():
+    """I6: allocated + free = total, no page in two samples; LIFO reuse."""
+    pool = OraclePool(hidden=8, page_tokens=4, hbm_pages=64, alloc="scatter")
+    rng = np.random.default_rng(5)
+    live = {}
+    for step in range(400):
+        if live and rng.integers(0, 2):
+            k = list(live)[int(rng.integers(0, len(live)))]
+            pool.free(k)
+            del live[k]
+        else:
+            n = int(rng.integers(1, 30))
+            try:
+                sid = pool.write([0], [0], [n])
+            except PoolError as e:
+                assert e.code == "ENOMEM"
+                continue
+            live[sid] = pool.sample_pages(sid)
+        pages = [g for v in live.values() for g in v]
+        assert len(pages) == len(set(pages))
+        assert len(pages) + pool.free_pages()[0] == 64
+    # Write A, free A, write B of the same page count: B gets A's pages in order.
+    a = pool.write([0], [0], [9])
+    pa = pool.sample_pages(a)
+    pool.free(a)
+    b = pool.write([0], [0], [12])
+    assert pool.sample_pages(b) == pa
+
+
+def test_contig_runs():
+    """I7: under "contig" every sample's pages are consecutive GVA pages."""
+    pool = OraclePool(hidden=8, page_tokens=4, hbm_pages=256, alloc="contig")
+    rng = np.random.default_rng(9)
+    live = []
+    for step in range(300):
+        if live and rng.integers(0, 3) == 0:
+            pool.free(live.pop(int(rng.integers(0, len(live)))))
+            continue
+        try:
+            sid = pool.write([0], [0], [int(rng.integers(1, 60))])
+        except PoolError:
+            continue
+        live.append(sid)
+        g = pool.sample_pages(sid)
+        assert all(g[i + 1] - g[i] == pool.pb for i in range(len(g) - 1))
+
+
+def test_error_paths():
+    pool = OraclePool(hidden=8, page_tokens=4, hbm_pages=4, alloc="contig", vocab=10)
+    for bad in [dict(text_ids=[1, 2], img_pos=[3], img_ntok=[1]),        # position > T
+                dict(text_ids=[1, 2], img_pos=[2, 1], img_ntok=[1, 1]),  # not sorted
+                dict(text_ids=[10], img_pos=[], img_ntok=[]),            # id >= vocab
+                dict(text_ids=[], img_pos=[], img_ntok=[]),              # empty sample
+                dict(text_ids=[1], img_pos=[0], img_ntok=[-1])]:
+        with pytest.raises(PoolError) as e:
+            pool.write(**bad)
+        assert e.value.code == "EINVAL"
+    sid = pool.write([1, 2], [1], [16])
+    with pytest.raises(PoolError) as e:
+        pool.write([1], [0], [1])
+    assert e.value.code == "ENOMEM"
+    with pytest.raises(PoolError) as e:
+        pool.pack([sid], tagged_table(10, 8), out_rows_cap=17)
+    assert e.value.code == "ECAPACITY"
+    pool.free(sid)
+    for call in (lambda: pool.free(sid), lambda: pool.pack([sid], None)):
+        with pytest.raises(PoolError) as e:
+            call()
+        assert e.value.code == "ENOENT"
+
+
+def test_tier_mask_split_equals_full():
+    """A pack restricted to HBM-tier (plus text) rows followed by one
+    restricted to DRAM-tier rows writes the same bytes as one full pack."""
+    cfg = scaled(CONFIGS["tiered"], hidden=16, hbm_pages=400, host_pages=400, vocab=500)
+    specs = gen_samples(cfg, 1, count=5)
+    table = tagged_table(cfg.vocab, cfg.hidden)
+    pool = OraclePool(cfg.hidden, cfg.page_tokens, cfg.hbm_pages, cfg.host_pages, "scatter", cfg.vocab)
+    rng = np.random.default_rng(3)
+    ids = [pool.write(s.text_ids, s.img_pos, s.img_ntok, tagged_vis(i, s.n_vis, cfg.hidden),
+                      tier_wish=rng.integers(0, 2, size=-(-s.n_vis // cfg.page_tokens)))
+           for i, s in enumerate(specs)]
+    full = pool.pack(ids, table)
+    out = np.full_like(full[0], 0x5555)
+    a = pool.pack(ids, table, tier_mask=MASK_HBM, out=out)
+    host_rows = np.all(out == 0x5555, axis=1)
+    assert 0 < host_rows.sum() < len(out)
+    b = pool.pack(ids, table, tier_mask=MASK_HOST, out=out)
+    assert b[1] is None
+    assert np.array_equal(out, full[0]) and np.array_equal(a[1], full[1]) and np.array_equal(a[2], full[2])
+
+
+def test_churn_sequence_is_feasible():
+    """The churn op sequence never asks a scatter pool for more pages than it
+    has free, and ends at or below the target occupancy."""
+    cfg = scaled(CONFIGS["frag70b"], hbm_pages=3000)
+    ops = churn_ops(cfg, 0, steps=2000)
+    pool = OraclePool(hidden=8, page_tokens=cfg.page_tokens, hbm_pages=cfg.hbm_pages, alloc="scatter")
+    keys = {}
+    for op in ops:
+        if op.kind == "write":
+            keys[op.key] = pool.write(op.spec.text_ids, op.spec.img_pos, op.spec.img_ntok)
+        else:
+            pool.free(keys.pop(op.key))
+    assert cfg.hbm_pages - pool.free_pages()[0] <= 0.5 * cfg.hbm_pages
+    assert sum(op.kind == "write" for op in ops) > 500
