@@ -1,0 +1,240 @@
+/*
+ * flowpool.h -- C ABI of libflowpool: the consumer side of a unified memory
+ * pool for decoupled VLM training, on one MI355X (gfx950).
+ *
+ * Producers (frozen vision encoders) write each sample's vision embeddings
+ * into pages of the pool, together with the sample's text token ids and the
+ * metadata that pairs them (paper Sec. 3.1 workflow, Sec. 3.2 "write"). A
+ * planner groups resident samples into cost-balanced microbatches (Sec. 3.4,
+ * Eq. 3). The backbone consumes a microbatch by sample id: the library
+ * resolves every visual row's GVA through the page table, gathers the page
+ * rows and the text-embedding-table rows and packs them into one varlen
+ * microbatch with cu_seqlens and position ids (Sec. 3.1 "consumes
+ * microbatches based on the GVA", Sec. 3.2 translation through local page
+ * tables).
+ *
+ * Conventions for every entry point:
+ *  - Return value: FP_OK (0) or a negative FP_E* status. Nothing throws or
+ *    aborts across the ABI. fp_last_error() returns a message for the last
+ *    failing call on the calling thread.
+ *  - A failing call leaves the pool unchanged and launches nothing.
+ *  - "host" pointers are ordinary CPU memory read or written before the call
+ *    returns; "device" pointers must be readable/writable by the GPU (device
+ *    memory, or pinned host memory mapped into the GPU address space).
+ *  - `stream` is a hipStream_t cast to void* (NULL = the null stream). Work
+ *    is enqueued on it; ordering against other streams is the caller's job.
+ *  - Embeddings are bf16, row-major, H elements per row; the library moves
+ *    them as raw 16-bit words (NaN payloads, signed zeros and denormals are
+ *    preserved exactly).
+ *  - A pool is not safe for concurrent calls from several threads; calls are
+ *    serialised internally by a mutex, but stream ordering between a write,
+ *    a free and a pack that touch the same sample is the caller's job.
+ */
+#ifndef FLOWPOOL_H
+#define FLOWPOOL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FP_ABI_VERSION 1
+
+typedef struct fp_pool fp_pool;   /* opaque; created and owned by the library */
+typedef int32_t fp_status;
+
+enum {
+  FP_OK = 0,
+  FP_EINVAL = -1,     /* bad argument (value, size, id, position, policy) */
+  FP_ENOMEM = -2,     /* pool pages, sample slots or metadata arena exhausted */
+  FP_ENOENT = -3,     /* unknown or already-freed sample id */
+  FP_ECAPACITY = -4,  /* microbatch rows exceed the output capacity */
+  FP_EALIGN = -5,     /* pointer not aligned as required */
+  FP_EHIP = -6,       /* a HIP runtime call failed (message names it) */
+  FP_ESTATE = -7      /* call not valid in the pool's state */
+};
+
+enum { FP_ALLOC_CONTIG = 0, FP_ALLOC_SCATTER = 1 };
+enum { FP_TIER_HBM = 0, FP_TIER_HOST = 1 };
+enum { FP_TIER_MASK_HBM = 1, FP_TIER_MASK_HOST = 2, FP_TIER_MASK_ALL = 3 };
+
+/* Pool configuration (Sec. 3.2).
+ *  hidden        H, bf16 elements per row; 2*H must be a multiple of 16.
+ *  page_tokens   P, rows per page; page bytes pb = P * 2H.
+ *  hbm_pages     pages backed by device memory (HBM tier).
+ *  host_pages    pages backed by pinned host memory that kernels read over
+ *                PCIe (DRAM tier); 0 = untiered.
+ *  alloc_policy  FP_ALLOC_CONTIG: a sample's pages are the lowest-index run
+ *                of consecutive free pages in one tier (HBM tried first).
+ *                FP_ALLOC_SCATTER: pages are popped one at a time from a
+ *                per-tier LIFO free stack (page 0 first on a fresh pool);
+ *                a freed sample's pages are pushed last-page-first.
+ *  device        HIP device ordinal the pool lives on.
+ *  vocab         text ids must lie in [0, vocab); 0 = samples carry no text.
+ *  gva_start     base of the GVA space, a multiple of 4096; 0 = 0x100000000000.
+ *                The HBM region is [gva_start, gva_start + world_size*hbm_pages*pb),
+ *                the DRAM region follows it; this rank owns
+ *                [region + rank*max_size, region + (rank+1)*max_size) of each.
+ *  world_size, rank   must be 1 and 0 in this library (single process).
+ *  max_samples   resident sample slots; 0 = 65536.
+ *  meta_bytes    device metadata arena (text ids, image positions, page
+ *                lists); 0 = 64 MiB.
+ *  frame_shuffle_seed  0 = physical frames bound to GVA pages in order; else
+ *                a seeded permutation of frames (placement-independence tests).
+ *  chunk_bytes   the library allocates tier backing in chunks of this many
+ *                bytes (rounded down to whole pages); 0 = 1 GiB.
+ *  hbm_backing, host_backing  reserved, must be NULL (the library allocates
+ *                and frees all backing memory).
+ */
+typedef struct fp_pool_config {
+  int32_t hidden;
+  int32_t page_tokens;
+  int64_t hbm_pages;
+  int64_t host_pages;
+  int32_t alloc_policy;
+  int32_t device;
+  int64_t vocab;
+  uint64_t gva_start;
+  int32_t world_size;
+  int32_t rank;
+  int64_t max_samples;
+  int64_t meta_bytes;
+  uint64_t frame_shuffle_seed;
+  int64_t chunk_bytes;
+  void* hbm_backing;
+  void* host_backing;
+} fp_pool_config;
+
+/* Library ABI version (FP_ABI_VERSION of the build). */
+int32_t fp_abi_version(void);
+
+/* Message for the last non-OK status returned on this thread ("" if none).
+ * The string is owned by the library and valid until the next call. */
+const char* fp_last_error(void);
+
+/* Fill *cfg with defaults (all zero except world_size = 1). */
+void fp_config_init(fp_pool_config* cfg);
+
+/* Create a pool (Sec. 3.2 initialisation): reserve this rank's GVA segments,
+ * allocate the tiers' physical memory, bind it to the GVA pages through the
+ * page table and upload the table to the device. cfg: host. *out receives the
+ * pool handle. Errors: EINVAL (bad field), EHIP (allocation failed). */
+fp_status pool_create(const fp_pool_config* cfg, fp_pool** out);
+
+/* Destroy a pool and free all its memory. The caller must have synchronised
+ * every stream that still uses it. NULL is accepted. */
+fp_status pool_destroy(fp_pool* p);
+
+/* Producer write (Sec. 3.2 "vision embeddings and text tokens are written
+ * into the GVA segment of their own process"; Sec. 3.1 pairing metadata).
+ *  text_ids        host int32[n_text], each in [0, vocab).
+ *  img_pos         host int32[n_img], nondecreasing, each in [0, n_text]: image
+ *                  j is placed before text token img_pos[j] (after all text
+ *                  when equal to n_text); equal positions keep image order.
+ *  img_ntok        host int32[n_img] >= 0, visual rows of each image.
+ *  vis_emb         device bf16 [sum(img_ntok), H] row-major, images
+ *                  concatenated in order, 16-byte aligned; it is read on
+ *                  `stream` after the call returns and must stay valid until
+ *                  that work completes. NULL reserves the pages without
+ *                  writing them (their rows are then unspecified).
+ *  page_tier_wish  host uint8[ceil(sum(img_ntok)/P)] of FP_TIER_* per page
+ *                  (SCATTER only; a full tier falls back to the other); NULL =
+ *                  HBM first.
+ * The sample's visual rows fill its own pages densely in order (last page
+ * possibly partial). All-or-nothing. *out_sample_id (host) receives a new id,
+ * never reused, >= 1.
+ * Errors: EINVAL (positions, counts, ids, empty sample, wish), EALIGN,
+ * ENOMEM (pages, slots or metadata exhausted), EHIP. */
+fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
+                            const int32_t* img_pos, const int32_t* img_ntok, int32_t n_img,
+                            const void* vis_emb, const uint8_t* page_tier_wish,
+                            void* stream, uint64_t* out_sample_id);
+
+/* Release a sample: its pages, metadata and slot return to the free lists at
+ * once. The caller guarantees no enqueued pack or plan still reads it.
+ * Errors: ENOENT. */
+fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
+
+/* Planner (Sec. 3.4): evaluate each sample's cost K*l + l^2 (the per-sample
+ * cost l + l^2/K scaled by K; l = text + visual rows) with a GPU kernel over
+ * the device sample table, then partition greedily into n_mb microbatches of
+ * at most `capacity` tokens: samples by decreasing cost (ties: lower index),
+ * each to the fitting microbatch of least accumulated cost (ties: lower
+ * microbatch index), deferred (-1) if none fits; deferred samples stay
+ * resident. Samples of one microbatch keep their order in sample_ids.
+ *  sample_ids       host uint64[n], distinct, resident.
+ *  out_assign       host int32[n]: microbatch index or -1.
+ *  out_mb_tokens    host int32[n_mb]: tokens per microbatch.
+ *  out_mb_cost_scaled  host int64[n_mb]: sum of K*l + l^2 per microbatch.
+ *  out_mb_max_len   host int32[n_mb] or NULL: longest sample per microbatch
+ *                   (with out_mb_tokens this gives Eq. 3).
+ *  out_sample_cost_scaled  host int64[n] or NULL: the per-sample costs.
+ * Synchronous: returns after `stream` has finished the cost kernel.
+ * Errors: EINVAL (n_mb < 1, capacity < 1, cost_k < 1, duplicates), ENOENT, EHIP. */
+fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n,
+                            int32_t capacity, int32_t n_mb, int32_t cost_k,
+                            int32_t* out_assign, int32_t* out_mb_tokens,
+                            int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
+                            int64_t* out_sample_cost_scaled, void* stream);
+
+/* The greedy partition of plan_microbatches on given lengths and costs, host
+ * only (no pool, no GPU). lengths: host int32[n] >= 1; costs_scaled: host
+ * int64[n]; outputs as in plan_microbatches. Errors: EINVAL. */
+fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
+                         int32_t capacity, int32_t n_mb, int32_t* out_assign,
+                         int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
+                         int32_t* out_mb_max_len);
+
+/* Consumer pack: the hot path (Sec. 3.1, Sec. 3.2). For samples
+ * sample_ids[0..n) in order, writes the packed microbatch:
+ *  out_emb           device bf16 [out_rows_cap, H], 16-byte aligned. Row
+ *                    cu[k] + r holds row r of sample k: text rows are
+ *                    embed_table[id] and image rows are the producer's rows,
+ *                    interleaved as described at pool_write_sample. Rows
+ *                    >= n_tokens are not touched.
+ *  out_cu_seqlens    device int32[n+1] (or NULL): 0, l_0, l_0+l_1, ...
+ *  out_position_ids  device int32[out_rows_cap] (or NULL): r within sample.
+ *  embed_table       device bf16 [vocab, H], 16-byte aligned; may be NULL when
+ *                    no sample has text. vocab must be >= the pool's vocab.
+ *  out_n_tokens, out_max_seqlen  host int32 (or NULL): total and longest l.
+ *  tier_mask         FP_TIER_MASK_HBM copies text rows and rows on HBM pages
+ *                    and writes cu_seqlens/position ids; FP_TIER_MASK_HOST
+ *                    copies rows on host-tier pages; FP_TIER_MASK_ALL both.
+ *                    Two launches with the two masks write what one ALL does.
+ * Asynchronous on `stream`. Duplicated ids are packed twice.
+ * Errors: EINVAL, ENOENT, ECAPACITY (sum of l > out_rows_cap), EALIGN, EHIP. */
+fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n,
+                          const void* embed_table, int64_t vocab,
+                          void* out_emb, int64_t out_rows_cap,
+                          int32_t* out_cu_seqlens, int32_t* out_position_ids,
+                          int32_t* out_n_tokens, int32_t* out_max_seqlen,
+                          int32_t tier_mask, void* stream);
+
+/* Introspection (tests, benchmarks); host outputs, any may be NULL. */
+fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages,
+                     int64_t* n_samples);
+
+/* Page GVAs of a sample in visual-row order. gvas: host uint64[cap]; *n (host)
+ * receives the page count even when cap is too small (then EINVAL). */
+fp_status pool_sample_pages(const fp_pool* p, uint64_t sample_id, uint64_t* gvas,
+                            int32_t cap, int32_t* n);
+
+/* Sample metadata: *length = text + visual rows, *n_text, *n_vis (host, any NULL). */
+fp_status pool_sample_info(const fp_pool* p, uint64_t sample_id, int32_t* length,
+                           int32_t* n_text, int32_t* n_vis);
+
+/* Translate a GVA through the page table: *tier (FP_TIER_*) and *phys, the
+ * device-visible address of that byte. Errors: EINVAL (unmapped GVA). */
+fp_status pool_translate(const fp_pool* p, uint64_t gva, int32_t* tier, uint64_t* phys);
+
+/* GVA layout: region starts and this rank's segment starts for the two tiers
+ * (host uint64[2] each, may be NULL) and the page size in bytes. */
+fp_status pool_layout(const fp_pool* p, uint64_t* region_start, uint64_t* segment_start,
+                      int64_t* page_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLOWPOOL_H */

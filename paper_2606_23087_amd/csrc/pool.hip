@@ -1,0 +1,767 @@
+// Host side of libflowpool: the C ABI of include/flowpool.h.
+//
+// Pool state (paper Sec. 3.2): this rank's GVA segments for the HBM and DRAM
+// tiers, the physical backing of each tier (device chunks; pinned, mapped
+// host chunks), the page table GVA page -> physical page (host mirror plus a
+// device copy that the kernels walk), the page allocators, the device sample
+// table and metadata arena that pair each sample's text ids with its image
+// pages (Sec. 3.1), and a small ring of pinned staging buffers for the
+// asynchronous metadata uploads.
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
+#include "flowpool.h"
+#include "fp_internal.h"
+
+using fp::SampleDesc;
+
+namespace {
+
+thread_local std::string t_err;
+
+fp_status fail(fp_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return code;
+}
+
+#define FP_HIP(call)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (call);                                                           \
+    if (e_ != hipSuccess) return fail(FP_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr uint64_t kDefaultGvaStart = 0x0000100000000000ull;
+constexpr int64_t kDefaultMaxSamples = 65536;
+constexpr int64_t kDefaultMetaBytes = 64ll << 20;
+constexpr int64_t kDefaultChunkBytes = 1ll << 30;
+constexpr int64_t kMaxSampleRows = 1 << 24;
+constexpr int kRing = 8;
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(dev) == hipSuccess) ok = true;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+// First-fit allocator over [0, size) with coalescing (metadata arena).
+struct RangeAlloc {
+  std::map<int64_t, int64_t> free_;  // offset -> length
+  void init(int64_t size) {
+    free_.clear();
+    if (size > 0) free_[0] = size;
+  }
+  int64_t alloc(int64_t n) {
+    for (auto it = free_.begin(); it != free_.end(); ++it) {
+      if (it->second >= n) {
+        const int64_t off = it->first, len = it->second;
+        free_.erase(it);
+        if (len > n) free_[off + n] = len - n;
+        return off;
+      }
+    }
+    return -1;
+  }
+  void release(int64_t off, int64_t n) {
+    auto next = free_.lower_bound(off);
+    if (next != free_.end() && off + n == next->first) {
+      n += next->second;
+      next = free_.erase(next);
+    }
+    if (next != free_.begin()) {
+      auto prev = std::prev(next);
+      if (prev->first + prev->second == off) {
+        prev->second += n;
+        return;
+      }
+    }
+    free_[off] = n;
+  }
+};
+
+// Pinned host buffer + device buffer + completion event, reused round-robin.
+struct Stage {
+  uint8_t* host = nullptr;
+  size_t host_cap = 0;
+  uint8_t* dev = nullptr;
+  size_t dev_cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+struct SampleRec {
+  int32_t slot;
+  int32_t len, n_text, n_img, n_vis;
+  int64_t meta_off, meta_len;
+  std::vector<uint64_t> pages;   // GVAs in visual-row order
+};
+
+uint64_t splitmix64(uint64_t& s) {
+  uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+int64_t align16(int64_t x) { return (x + 15) & ~int64_t(15); }
+
+}  // namespace
+
+struct fp_pool {
+  fp_pool_config cfg{};
+  std::mutex mu;
+  int64_t rb = 0, pb = 0;
+  int64_t n_pages[2] = {0, 0};
+  uint64_t gva_start = 0;
+  uint64_t region_start[2] = {0, 0};
+  uint64_t seg_start[2] = {0, 0};
+  uint64_t max_size[2] = {0, 0};
+  // physical backing
+  std::vector<void*> chunks[2];
+  int64_t frames_per_chunk = 1;
+  std::vector<uint64_t> pte;          // host mirror, index = global vpn
+  uint64_t* pte_dev = nullptr;
+  // allocators, page index inside the tier's segment
+  std::vector<uint8_t> used[2];
+  std::vector<int64_t> stack[2];      // scatter: LIFO, back() pops first
+  int64_t n_free[2] = {0, 0};
+  // samples
+  SampleDesc* desc_dev = nullptr;
+  std::vector<int32_t> free_slots;
+  uint8_t* meta_dev = nullptr;
+  RangeAlloc meta;
+  std::unordered_map<uint64_t, SampleRec> samples;
+  uint64_t next_id = 1;
+  // staging
+  Stage ring[kRing];
+  int ring_next = 0;
+  int tile_rows = 1;
+
+  uint64_t page_gva(int tier, int64_t idx) const { return seg_start[tier] + (uint64_t)idx * (uint64_t)pb; }
+  int page_index(uint64_t gva, int64_t* idx) const {
+    for (int t = 0; t < 2; ++t) {
+      if (gva >= seg_start[t] && gva < seg_start[t] + max_size[t]) {
+        *idx = (int64_t)((gva - seg_start[t]) / (uint64_t)pb);
+        return t;
+      }
+    }
+    return -1;
+  }
+};
+
+namespace {
+
+fp_status stage_acquire(fp_pool* p, size_t host_bytes, size_t dev_bytes, Stage** out) {
+  Stage& s = p->ring[p->ring_next];
+  p->ring_next = (p->ring_next + 1) % kRing;
+  if (s.pending) {
+    FP_HIP(hipEventSynchronize(s.ev));
+    s.pending = false;
+  }
+  if (host_bytes > s.host_cap) {
+    if (s.host) FP_HIP(hipHostFree(s.host));
+    s.host = nullptr;
+    s.host_cap = 0;
+    size_t cap = std::max<size_t>(host_bytes, 1 << 20);
+    FP_HIP(hipHostMalloc((void**)&s.host, cap, hipHostMallocDefault));
+    s.host_cap = cap;
+  }
+  if (dev_bytes > s.dev_cap) {
+    if (s.dev) FP_HIP(hipFree(s.dev));
+    s.dev = nullptr;
+    s.dev_cap = 0;
+    size_t cap = std::max<size_t>(dev_bytes, 1 << 18);
+    FP_HIP(hipMalloc((void**)&s.dev, cap));
+    s.dev_cap = cap;
+  }
+  *out = &s;
+  return FP_OK;
+}
+
+fp_status stage_release(Stage* s, hipStream_t stream) {
+  FP_HIP(hipEventRecord(s->ev, stream));
+  s->pending = true;
+  return FP_OK;
+}
+
+void free_all(fp_pool* p) {
+  for (auto& s : p->ring) {
+    if (s.ev) (void)hipEventSynchronize(s.ev);
+    if (s.host) (void)hipHostFree(s.host);
+    if (s.dev) (void)hipFree(s.dev);
+    if (s.ev) (void)hipEventDestroy(s.ev);
+    s = Stage{};
+  }
+  for (void* c : p->chunks[0]) (void)hipFree(c);
+  for (void* c : p->chunks[1]) (void)hipHostFree(c);
+  p->chunks[0].clear();
+  p->chunks[1].clear();
+  if (p->pte_dev) (void)hipFree(p->pte_dev);
+  if (p->desc_dev) (void)hipFree(p->desc_dev);
+  if (p->meta_dev) (void)hipFree(p->meta_dev);
+  p->pte_dev = nullptr;
+  p->desc_dev = nullptr;
+  p->meta_dev = nullptr;
+}
+
+// Pages for one sample, all-or-nothing. Returns FP_ENOMEM without changes.
+fp_status alloc_pages(fp_pool* p, int64_t n, const uint8_t* wish, std::vector<uint64_t>* out) {
+  out->clear();
+  if (n == 0) return FP_OK;
+  if (p->cfg.alloc_policy == FP_ALLOC_CONTIG) {
+    for (int t = 0; t < 2; ++t) {
+      const std::vector<uint8_t>& used = p->used[t];
+      int64_t run = 0;
+      for (int64_t i = 0; i < p->n_pages[t]; ++i) {
+        run = used[i] ? 0 : run + 1;
+        if (run == n) {
+          const int64_t first = i - n + 1;
+          for (int64_t j = first; j <= i; ++j) {
+            p->used[t][j] = 1;
+            out->push_back(p->page_gva(t, j));
+          }
+          p->n_free[t] -= n;
+          return FP_OK;
+        }
+      }
+    }
+    return fail(FP_ENOMEM, "no run of %lld free pages", (long long)n);
+  }
+  int64_t left[2] = {(int64_t)p->stack[0].size(), (int64_t)p->stack[1].size()};
+  std::vector<uint8_t> tiers((size_t)n);
+  for (int64_t j = 0; j < n; ++j) {
+    int t = wish ? wish[j] : FP_TIER_HBM;
+    if (left[t] == 0) t = 1 - t;
+    if (left[t] == 0) return fail(FP_ENOMEM, "%lld pages do not fit", (long long)n);
+    --left[t];
+    tiers[(size_t)j] = (uint8_t)t;
+  }
+  for (int64_t j = 0; j < n; ++j) {
+    const int t = tiers[(size_t)j];
+    const int64_t i = p->stack[t].back();
+    p->stack[t].pop_back();
+    p->used[t][i] = 1;
+    p->n_free[t] -= 1;
+    out->push_back(p->page_gva(t, i));
+  }
+  return FP_OK;
+}
+
+void release_pages(fp_pool* p, const std::vector<uint64_t>& pages) {
+  for (auto it = pages.rbegin(); it != pages.rend(); ++it) {
+    int64_t i = 0;
+    const int t = p->page_index(*it, &i);
+    p->used[t][i] = 0;
+    p->n_free[t] += 1;
+    if (p->cfg.alloc_policy == FP_ALLOC_SCATTER) p->stack[t].push_back(i);
+  }
+}
+
+fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
+                 int32_t n_mb, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
+                 int32_t* mb_max) {
+  std::vector<int32_t> order((size_t)n);
+  std::iota(order.begin(), order.end(), 0);
+  std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return costs[a] > costs[b] || (costs[a] == costs[b] && a < b);
+  });
+  std::vector<int64_t> tok((size_t)n_mb, 0), cst((size_t)n_mb, 0);
+  std::vector<int32_t> mx((size_t)n_mb, 0);
+  for (int32_t i = 0; i < n; ++i) assign[i] = -1;
+  for (int32_t i : order) {
+    int best = -1;
+    for (int j = 0; j < n_mb; ++j) {
+      if (tok[(size_t)j] + lengths[i] <= capacity &&
+          (best < 0 || cst[(size_t)j] < cst[(size_t)best]))
+        best = j;
+    }
+    if (best >= 0) {
+      assign[i] = best;
+      tok[(size_t)best] += lengths[i];
+      cst[(size_t)best] += costs[i];
+      mx[(size_t)best] = std::max(mx[(size_t)best], lengths[i]);
+    }
+  }
+  for (int j = 0; j < n_mb; ++j) {
+    if (mb_tokens) mb_tokens[j] = (int32_t)tok[(size_t)j];
+    if (mb_cost) mb_cost[j] = cst[(size_t)j];
+    if (mb_max) mb_max[j] = mx[(size_t)j];
+  }
+  return FP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t fp_abi_version(void) { return FP_ABI_VERSION; }
+
+const char* fp_last_error(void) { return t_err.c_str(); }
+
+void fp_config_init(fp_pool_config* cfg) {
+  if (!cfg) return;
+  std::memset(cfg, 0, sizeof(*cfg));
+  cfg->world_size = 1;
+}
+
+fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
+  if (!cfg_in || !out) return fail(FP_EINVAL, "null argument");
+  *out = nullptr;
+  fp_pool_config c = *cfg_in;
+  if (c.hidden < 8 || ((2ll * c.hidden) % 16) != 0 || c.hidden > (1 << 20))
+    return fail(FP_EINVAL, "hidden %d: 2*hidden must be a positive multiple of 16", c.hidden);
+  if (c.page_tokens < 1 || c.page_tokens > (1 << 20)) return fail(FP_EINVAL, "page_tokens %d", c.page_tokens);
+  if (c.hbm_pages < 0 || c.host_pages < 0 || c.hbm_pages + c.host_pages < 1 ||
+      c.hbm_pages + c.host_pages > (1ll << 31))
+    return fail(FP_EINVAL, "page counts %lld/%lld", (long long)c.hbm_pages, (long long)c.host_pages);
+  if (c.alloc_policy != FP_ALLOC_CONTIG && c.alloc_policy != FP_ALLOC_SCATTER)
+    return fail(FP_EINVAL, "alloc_policy %d", c.alloc_policy);
+  if (c.world_size != 1 || c.rank != 0)
+    return fail(FP_EINVAL, "world_size/rank %d/%d: this library runs one process", c.world_size, c.rank);
+  if (c.vocab < 0 || c.vocab > (1ll << 31)) return fail(FP_EINVAL, "vocab %lld", (long long)c.vocab);
+  if (c.hbm_backing || c.host_backing) return fail(FP_EINVAL, "caller-provided backing is not supported");
+  if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
+  if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
+  if (c.max_samples == 0) c.max_samples = kDefaultMaxSamples;
+  if (c.max_samples < 1 || c.max_samples > (1ll << 31) - 1) return fail(FP_EINVAL, "max_samples");
+  if (c.meta_bytes == 0) c.meta_bytes = kDefaultMetaBytes;
+  if (c.meta_bytes < 16) return fail(FP_EINVAL, "meta_bytes");
+  if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunkBytes;
+  if (c.chunk_bytes < 0) return fail(FP_EINVAL, "chunk_bytes");
+  int ndev = 0;
+  FP_HIP(hipGetDeviceCount(&ndev));
+  if (c.device < 0 || c.device >= ndev) return fail(FP_EINVAL, "device %d of %d", c.device, ndev);
+  DeviceGuard guard(c.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice(%d) failed", c.device);
+
+  fp_pool* p = new fp_pool();
+  p->cfg = c;
+  p->rb = 2ll * c.hidden;
+  p->pb = p->rb * c.page_tokens;
+  p->n_pages[0] = c.hbm_pages;
+  p->n_pages[1] = c.host_pages;
+  p->gva_start = c.gva_start;
+  // Sec. 3.2: per tier a region [start, start + world_size*max_size); this
+  // rank's segment [start + rank*max_size, start + (rank+1)*max_size); the
+  // DRAM region follows the HBM region.
+  for (int t = 0; t < 2; ++t) p->max_size[t] = (uint64_t)p->n_pages[t] * (uint64_t)p->pb;
+  p->region_start[0] = c.gva_start;
+  p->region_start[1] = c.gva_start + (uint64_t)c.world_size * p->max_size[0];
+  for (int t = 0; t < 2; ++t) p->seg_start[t] = p->region_start[t] + (uint64_t)c.rank * p->max_size[t];
+  p->tile_rows = (int)std::max<int64_t>(1, std::min<int64_t>(fp::kMaxTileRows, 65536 / p->rb));
+
+  auto bail = [&](fp_status s) {
+    std::string keep = t_err;
+    free_all(p);
+    delete p;
+    t_err = keep;
+    return s;
+  };
+
+  // Physical backing in chunks of whole pages.
+  p->frames_per_chunk = std::max<int64_t>(1, c.chunk_bytes / p->pb);
+  for (int t = 0; t < 2; ++t) {
+    for (int64_t f = 0; f < p->n_pages[t]; f += p->frames_per_chunk) {
+      const int64_t frames = std::min(p->frames_per_chunk, p->n_pages[t] - f);
+      void* ptr = nullptr;
+      hipError_t e = (t == 0) ? hipMalloc(&ptr, (size_t)(frames * p->pb))
+                              : hipHostMalloc(&ptr, (size_t)(frames * p->pb), hipHostMallocMapped);
+      if (e != hipSuccess)
+        return bail(fail(FP_EHIP, "allocating %s backing (%lld bytes): %s", t ? "host" : "HBM",
+                         (long long)(frames * p->pb), hipGetErrorString(e)));
+      if (t == 1) {
+        void* dptr = nullptr;
+        e = hipHostGetDevicePointer(&dptr, ptr, 0);
+        if (e != hipSuccess || dptr != ptr) {
+          (void)hipHostFree(ptr);
+          return bail(fail(FP_EHIP, "host backing is not mapped at the same address"));
+        }
+      }
+      p->chunks[t].push_back(ptr);
+    }
+  }
+  // Page table: GVA page (HBM pages, then host pages) -> physical frame.
+  const int64_t total = p->n_pages[0] + p->n_pages[1];
+  p->pte.resize((size_t)total);
+  uint64_t seed = c.frame_shuffle_seed;
+  for (int t = 0; t < 2; ++t) {
+    std::vector<int64_t> order((size_t)p->n_pages[t]);
+    std::iota(order.begin(), order.end(), 0);
+    if (seed) {
+      for (int64_t i = p->n_pages[t] - 1; i > 0; --i) {
+        const int64_t j = (int64_t)(splitmix64(seed) % (uint64_t)(i + 1));
+        std::swap(order[(size_t)i], order[(size_t)j]);
+      }
+    }
+    for (int64_t i = 0; i < p->n_pages[t]; ++i) {
+      const int64_t f = order[(size_t)i];
+      const uint64_t addr = (uint64_t)p->chunks[t][(size_t)(f / p->frames_per_chunk)] +
+                            (uint64_t)(f % p->frames_per_chunk) * (uint64_t)p->pb;
+      const int64_t vpn = (int64_t)((p->page_gva(t, i) - p->gva_start) / (uint64_t)p->pb);
+      p->pte[(size_t)vpn] = addr | fp::PTE_VALID | (t ? fp::PTE_HOST : 0);
+    }
+    p->used[t].assign((size_t)p->n_pages[t], 0);
+    p->stack[t].resize((size_t)p->n_pages[t]);
+    for (int64_t i = 0; i < p->n_pages[t]; ++i) p->stack[t][(size_t)i] = p->n_pages[t] - 1 - i;
+    p->n_free[t] = p->n_pages[t];
+  }
+  hipError_t e = hipMalloc((void**)&p->pte_dev, sizeof(uint64_t) * (size_t)total);
+  if (e == hipSuccess)
+    e = hipMemcpy(p->pte_dev, p->pte.data(), sizeof(uint64_t) * (size_t)total, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMalloc((void**)&p->desc_dev, sizeof(SampleDesc) * (size_t)c.max_samples);
+  if (e == hipSuccess) e = hipMalloc((void**)&p->meta_dev, (size_t)c.meta_bytes);
+  for (int i = 0; e == hipSuccess && i < kRing; ++i)
+    e = hipEventCreateWithFlags(&p->ring[i].ev, hipEventDisableTiming);
+  if (e != hipSuccess) return bail(fail(FP_EHIP, "pool metadata allocation: %s", hipGetErrorString(e)));
+  p->meta.init(c.meta_bytes);
+  p->free_slots.resize((size_t)c.max_samples);
+  for (int64_t i = 0; i < c.max_samples; ++i) p->free_slots[(size_t)i] = (int32_t)(c.max_samples - 1 - i);
+  *out = p;
+  return FP_OK;
+}
+
+fp_status pool_destroy(fp_pool* p) {
+  if (!p) return FP_OK;
+  {
+    DeviceGuard guard(p->cfg.device);
+    free_all(p);
+  }
+  delete p;
+  return FP_OK;
+}
+
+fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
+                            const int32_t* img_pos, const int32_t* img_ntok, int32_t n_img,
+                            const void* vis_emb, const uint8_t* page_tier_wish, void* stream,
+                            uint64_t* out_sample_id) {
+  if (!p || !out_sample_id) return fail(FP_EINVAL, "null argument");
+  std::lock_guard<std::mutex> lock(p->mu);
+  if (n_text < 0 || n_img < 0) return fail(FP_EINVAL, "negative count");
+  if ((n_text && !text_ids) || (n_img && (!img_pos || !img_ntok))) return fail(FP_EINVAL, "null array");
+  int64_t n_vis = 0;
+  for (int32_t j = 0; j < n_img; ++j) {
+    if (img_ntok[j] < 0) return fail(FP_EINVAL, "image %d has %d rows", j, img_ntok[j]);
+    if (img_pos[j] < 0 || img_pos[j] > n_text || (j && img_pos[j] < img_pos[j - 1]))
+      return fail(FP_EINVAL, "image %d placeholder %d (text %d)", j, img_pos[j], n_text);
+    n_vis += img_ntok[j];
+  }
+  const int64_t len = n_vis + n_text;
+  if (len < 1 || len > kMaxSampleRows) return fail(FP_EINVAL, "sample length %lld", (long long)len);
+  for (int32_t i = 0; i < n_text; ++i)
+    if (text_ids[i] < 0 || text_ids[i] >= p->cfg.vocab)
+      return fail(FP_EINVAL, "text id %d at %d outside [0, %lld)", text_ids[i], i, (long long)p->cfg.vocab);
+  const int64_t n_pages = (n_vis + p->cfg.page_tokens - 1) / p->cfg.page_tokens;
+  if (page_tier_wish) {
+    if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "tier wishes need the scatter policy");
+    for (int64_t j = 0; j < n_pages; ++j)
+      if (page_tier_wish[j] > 1) return fail(FP_EINVAL, "tier wish %d", page_tier_wish[j]);
+  }
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  const uint8_t* vis_dev = nullptr;
+  if (vis_emb && n_vis > 0) {
+    if ((uintptr_t)vis_emb % 16) return fail(FP_EALIGN, "vis_emb must be 16-byte aligned");
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, vis_emb) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(FP_EINVAL, "vis_emb is not device-accessible memory");
+    }
+    vis_dev = (const uint8_t*)(attr.devicePointer ? attr.devicePointer : vis_emb);
+  }
+  if (p->free_slots.empty()) return fail(FP_ENOMEM, "all %lld sample slots in use", (long long)p->cfg.max_samples);
+  const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);
+  int64_t meta_off = 0;
+  if (meta_len > 0) {
+    meta_off = p->meta.alloc(meta_len);
+    if (meta_off < 0) return fail(FP_ENOMEM, "metadata arena full (%lld bytes wanted)", (long long)meta_len);
+  }
+  SampleRec rec;
+  fp_status st = alloc_pages(p, n_pages, page_tier_wish, &rec.pages);
+  if (st != FP_OK) {
+    if (meta_len > 0) p->meta.release(meta_off, meta_len);
+    return st;
+  }
+  auto rollback = [&](fp_status s) {
+    std::string keep = t_err;
+    release_pages(p, rec.pages);
+    if (meta_len > 0) p->meta.release(meta_off, meta_len);
+    t_err = keep;
+    return s;
+  };
+  hipStream_t hs = (hipStream_t)stream;
+  SampleDesc d{};
+  d.len = (int32_t)len;
+  d.n_text = n_text;
+  d.n_img = n_img;
+  d.n_vis = (int32_t)n_vis;
+  d.n_pages = (int32_t)n_pages;
+  d.page_off = meta_off;
+  d.img_off = meta_off + align16(8 * n_pages);
+  d.text_off = d.img_off + align16(8ll * n_img);
+  if (meta_len > 0) {
+    Stage* s = nullptr;
+    st = stage_acquire(p, (size_t)meta_len, 0, &s);
+    if (st != FP_OK) return rollback(st);
+    std::memcpy(s->host, rec.pages.data(), 8 * (size_t)n_pages);
+    int32_t* img = (int32_t*)(s->host + (d.img_off - meta_off));
+    for (int32_t j = 0; j < n_img; ++j) {
+      img[2 * j] = img_pos[j];
+      img[2 * j + 1] = img_ntok[j];
+    }
+    if (n_text) std::memcpy(s->host + (d.text_off - meta_off), text_ids, 4 * (size_t)n_text);
+    hipError_t e = hipMemcpyAsync(p->meta_dev + meta_off, s->host, (size_t)meta_len,
+                                  hipMemcpyHostToDevice, hs);
+    if (e != hipSuccess) return rollback(fail(FP_EHIP, "metadata upload: %s", hipGetErrorString(e)));
+    st = stage_release(s, hs);
+    if (st != FP_OK) return rollback(st);
+  }
+  const int32_t slot = p->free_slots.back();
+  fp::WriteArgs wa{};
+  wa.desc = d;
+  wa.desc_table = p->desc_dev;
+  wa.slot = slot;
+  wa.meta = p->meta_dev;
+  wa.pte = p->pte_dev;
+  wa.gva_start = p->gva_start;
+  wa.page_bytes = (uint64_t)p->pb;
+  wa.vis = vis_dev;
+  wa.row_bytes = (int32_t)p->rb;
+  wa.page_tokens = p->cfg.page_tokens;
+  wa.tile_rows = p->tile_rows;
+  hipError_t e = fp::launch_write(wa, hs);
+  if (e != hipSuccess) return rollback(fail(FP_EHIP, "write kernel: %s", hipGetErrorString(e)));
+  p->free_slots.pop_back();
+  rec.slot = slot;
+  rec.len = (int32_t)len;
+  rec.n_text = n_text;
+  rec.n_img = n_img;
+  rec.n_vis = (int32_t)n_vis;
+  rec.meta_off = meta_off;
+  rec.meta_len = meta_len;
+  const uint64_t id = p->next_id++;
+  p->samples.emplace(id, std::move(rec));
+  *out_sample_id = id;
+  return FP_OK;
+}
+
+fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  auto it = p->samples.find(sample_id);
+  if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
+  release_pages(p, it->second.pages);
+  if (it->second.meta_len > 0) p->meta.release(it->second.meta_off, it->second.meta_len);
+  p->free_slots.push_back(it->second.slot);
+  p->samples.erase(it);
+  return FP_OK;
+}
+
+fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
+                         int32_t capacity, int32_t n_mb, int32_t* out_assign,
+                         int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
+                         int32_t* out_mb_max_len) {
+  if (n < 0 || n_mb < 1 || capacity < 1 || capacity > (1 << 28))
+    return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d", n, n_mb, capacity);
+  if (n && (!lengths || !costs_scaled || !out_assign)) return fail(FP_EINVAL, "null array");
+  for (int32_t i = 0; i < n; ++i)
+    if (lengths[i] < 1 || costs_scaled[i] < 0) return fail(FP_EINVAL, "sample %d length/cost", i);
+  return greedy(lengths, costs_scaled, n, capacity, n_mb, out_assign, out_mb_tokens, out_mb_cost_scaled,
+                out_mb_max_len);
+}
+
+fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
+                            int32_t n_mb, int32_t cost_k, int32_t* out_assign, int32_t* out_mb_tokens,
+                            int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
+                            int64_t* out_sample_cost_scaled, void* stream) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  if (n < 0 || n_mb < 1 || capacity < 1 || capacity > (1 << 28) || cost_k < 1 || cost_k > (1 << 24))
+    return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d, cost_k %d", n, n_mb, capacity, cost_k);
+  if (n && (!sample_ids || !out_assign)) return fail(FP_EINVAL, "null array");
+  std::vector<int32_t> slots((size_t)n), lens((size_t)n);
+  std::unordered_set<uint64_t> seen;
+  seen.reserve((size_t)n * 2);
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = p->samples.find(sample_ids[i]);
+    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+    if (!seen.insert(sample_ids[i]).second)
+      return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
+    slots[(size_t)i] = it->second.slot;
+    lens[(size_t)i] = it->second.len;
+  }
+  std::vector<int64_t> costs((size_t)n);
+  if (n > 0) {
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    hipStream_t hs = (hipStream_t)stream;
+    const size_t slot_bytes = align16(4ll * n);
+    Stage* s = nullptr;
+    fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, slot_bytes + 8 * (size_t)n, &s);
+    if (st != FP_OK) return st;
+    std::memcpy(s->host, slots.data(), 4 * (size_t)n);
+    FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
+    FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->dev, n, cost_k, (int64_t*)(s->dev + slot_bytes), hs));
+    FP_HIP(hipMemcpyAsync(s->host + slot_bytes, s->dev + slot_bytes, 8 * (size_t)n, hipMemcpyDeviceToHost, hs));
+    FP_HIP(hipStreamSynchronize(hs));
+    std::memcpy(costs.data(), s->host + slot_bytes, 8 * (size_t)n);
+    st = stage_release(s, hs);
+    if (st != FP_OK) return st;
+  }
+  if (out_sample_cost_scaled) std::memcpy(out_sample_cost_scaled, costs.data(), 8 * (size_t)n);
+  return greedy(lens.data(), costs.data(), n, capacity, n_mb, out_assign, out_mb_tokens, out_mb_cost_scaled,
+                out_mb_max_len);
+}
+
+fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,
+                          int64_t vocab, void* out_emb, int64_t out_rows_cap, int32_t* out_cu_seqlens,
+                          int32_t* out_position_ids, int32_t* out_n_tokens, int32_t* out_max_seqlen,
+                          int32_t tier_mask, void* stream) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  if (n < 0 || n > fp::kMaxPackSamples) return fail(FP_EINVAL, "n %d outside [0, %d]", n, fp::kMaxPackSamples);
+  if (n && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
+  if (tier_mask < 1 || tier_mask > 3) return fail(FP_EINVAL, "tier_mask %d", tier_mask);
+  if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
+  if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
+  if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
+  fp::PackArgs a{};
+  std::vector<int32_t> big_slots;
+  int32_t* slots = a.slots_inline;
+  if (n > fp::kInlineSlots) {
+    big_slots.resize((size_t)n);
+    slots = big_slots.data();
+  }
+  int64_t total = 0, n_text = 0;
+  int32_t mx = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = p->samples.find(sample_ids[i]);
+    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+    slots[i] = it->second.slot;
+    total += it->second.len;
+    n_text += it->second.n_text;
+    mx = std::max(mx, it->second.len);
+  }
+  if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
+  if (total > 0x7fffffffll) return fail(FP_EINVAL, "microbatch too large");
+  if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
+  if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
+    if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
+    if (vocab < p->cfg.vocab) return fail(FP_EINVAL, "table vocab %lld < pool vocab %lld", (long long)vocab, (long long)p->cfg.vocab);
+  }
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  hipStream_t hs = (hipStream_t)stream;
+  a.desc = p->desc_dev;
+  a.meta = p->meta_dev;
+  a.pte = p->pte_dev;
+  a.gva_start = p->gva_start;
+  a.page_bytes = (uint64_t)p->pb;
+  a.table = (const uint8_t*)embed_table;
+  a.out = (uint8_t*)out_emb;
+  a.cu = out_cu_seqlens;
+  a.pos = out_position_ids;
+  a.n = n;
+  a.n_tokens = (int32_t)total;
+  a.row_bytes = (int32_t)p->rb;
+  a.page_tokens = p->cfg.page_tokens;
+  a.tier_mask = tier_mask;
+  a.tile_rows = p->tile_rows;
+  Stage* s = nullptr;
+  if (n > fp::kInlineSlots) {
+    fp_status st = stage_acquire(p, 4 * (size_t)n, 4 * (size_t)n, &s);
+    if (st != FP_OK) return st;
+    std::memcpy(s->host, slots, 4 * (size_t)n);
+    FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
+    a.slots_dev = (const int32_t*)s->dev;
+  }
+  hipError_t e = fp::launch_pack(a, hs);
+  if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
+  if (s) {
+    fp_status st = stage_release(s, hs);
+    if (st != FP_OK) return st;
+  }
+  if (out_n_tokens) *out_n_tokens = (int32_t)total;
+  if (out_max_seqlen) *out_max_seqlen = mx;
+  return FP_OK;
+}
+
+fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages, int64_t* n_samples) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  fp_pool* q = const_cast<fp_pool*>(p);
+  std::lock_guard<std::mutex> lock(q->mu);
+  if (free_hbm_pages) *free_hbm_pages = p->n_free[0];
+  if (free_host_pages) *free_host_pages = p->n_free[1];
+  if (n_samples) *n_samples = (int64_t)p->samples.size();
+  return FP_OK;
+}
+
+fp_status pool_sample_pages(const fp_pool* p, uint64_t sample_id, uint64_t* gvas, int32_t cap, int32_t* n) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  fp_pool* q = const_cast<fp_pool*>(p);
+  std::lock_guard<std::mutex> lock(q->mu);
+  auto it = p->samples.find(sample_id);
+  if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
+  const int32_t cnt = (int32_t)it->second.pages.size();
+  if (n) *n = cnt;
+  if (cap < cnt) return fail(FP_EINVAL, "capacity %d < %d pages", cap, cnt);
+  if (cnt && !gvas) return fail(FP_EINVAL, "null gvas");
+  if (cnt) std::memcpy(gvas, it->second.pages.data(), 8 * (size_t)cnt);
+  return FP_OK;
+}
+
+fp_status pool_sample_info(const fp_pool* p, uint64_t sample_id, int32_t* length, int32_t* n_text,
+                           int32_t* n_vis) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  fp_pool* q = const_cast<fp_pool*>(p);
+  std::lock_guard<std::mutex> lock(q->mu);
+  auto it = p->samples.find(sample_id);
+  if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
+  if (length) *length = it->second.len;
+  if (n_text) *n_text = it->second.n_text;
+  if (n_vis) *n_vis = it->second.n_vis;
+  return FP_OK;
+}
+
+fp_status pool_translate(const fp_pool* p, uint64_t gva, int32_t* tier, uint64_t* phys) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  int64_t idx = 0;
+  const int t = p->page_index(gva, &idx);
+  if (t < 0) return fail(FP_EINVAL, "GVA %#llx is not mapped", (unsigned long long)gva);
+  const uint64_t page = p->page_gva(t, idx);
+  const uint64_t e = p->pte[(size_t)((page - p->gva_start) / (uint64_t)p->pb)];
+  if (tier) *tier = (e & fp::PTE_HOST) ? FP_TIER_HOST : FP_TIER_HBM;
+  if (phys) *phys = (e & fp::PTE_ADDR_MASK) + (gva - page);
+  return FP_OK;
+}
+
+fp_status pool_layout(const fp_pool* p, uint64_t* region_start, uint64_t* segment_start, int64_t* page_bytes) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  for (int t = 0; t < 2; ++t) {
+    if (region_start) region_start[t] = p->region_start[t];
+    if (segment_start) segment_start[t] = p->seg_start[t];
+  }
+  if (page_bytes) *page_bytes = p->pb;
+  return FP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,247 @@
+"""ctypes binding of libflowpool (include/flowpool.h). Argument marshalling only.
+
+Every function has the name of the C entry point it calls. Host arrays are
+numpy arrays; device buffers are torch tensors or raw integer addresses;
+streams are torch streams, raw hipStream_t integers, or None (torch's current
+stream). A non-OK status raises ``FlowPoolError`` with the library's message.
+
+The library must have been built (``python -m paper_2606_23087_amd.build`` or
+``__graft_entry__.build()``); importing this module without it fails loudly.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libflowpool.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run paper_2606_23087_amd/build.py first")
+
+_lib = C.CDLL(LIB_PATH)
+
+FP_OK, FP_EINVAL, FP_ENOMEM, FP_ENOENT, FP_ECAPACITY, FP_EALIGN, FP_EHIP, FP_ESTATE = 0, -1, -2, -3, -4, -5, -6, -7
+STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ENOENT", -4: "ECAPACITY", -5: "EALIGN",
+                -6: "EHIP", -7: "ESTATE"}
+FP_ALLOC_CONTIG, FP_ALLOC_SCATTER = 0, 1
+FP_TIER_HBM, FP_TIER_HOST = 0, 1
+FP_TIER_MASK_HBM, FP_TIER_MASK_HOST, FP_TIER_MASK_ALL = 1, 2, 3
+ALLOC_POLICIES = {"contig": FP_ALLOC_CONTIG, "scatter": FP_ALLOC_SCATTER}
+
+
+class fp_pool_config(C.Structure):
+    _fields_ = [
+        ("hidden", C.c_int32), ("page_tokens", C.c_int32),
+        ("hbm_pages", C.c_int64), ("host_pages", C.c_int64),
+        ("alloc_policy", C.c_int32), ("device", C.c_int32),
+        ("vocab", C.c_int64), ("gva_start", C.c_uint64),
+        ("world_size", C.c_int32), ("rank", C.c_int32),
+        ("max_samples", C.c_int64), ("meta_bytes", C.c_int64),
+        ("frame_shuffle_seed", C.c_uint64), ("chunk_bytes", C.c_int64),
+        ("hbm_backing", C.c_void_p), ("host_backing", C.c_void_p),
+    ]
+
+
+class FlowPoolError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        self.status = status
+        self.code = STATUS_NAMES.get(status, str(status))
+        super().__init__(f"{where}: {self.code}: {message}")
+
+
+_P = C.c_void_p
+_i32p = C.POINTER(C.c_int32)
+_i64p = C.POINTER(C.c_int64)
+_u64p = C.POINTER(C.c_uint64)
+_u8p = C.POINTER(C.c_uint8)
+
+_SIGS = {
+    "fp_abi_version": (C.c_int32, []),
+    "fp_last_error": (C.c_char_p, []),
+    "fp_config_init": (None, [C.POINTER(fp_pool_config)]),
+    "pool_create": (C.c_int32, [C.POINTER(fp_pool_config), C.POINTER(_P)]),
+    "pool_destroy": (C.c_int32, [_P]),
+    "pool_write_sample": (C.c_int32, [_P, _i32p, C.c_int32, _i32p, _i32p, C.c_int32, _P, _u8p, _P, _u64p]),
+    "pool_free_sample": (C.c_int32, [_P, C.c_uint64]),
+    "plan_microbatches": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                      _i32p, _i32p, _i64p, _i32p, _i64p, _P]),
+    "plan_partition": (C.c_int32, [_i32p, _i64p, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i64p, _i32p]),
+    "pack_microbatch": (C.c_int32, [_P, _u64p, C.c_int32, _P, C.c_int64, _P, C.c_int64, _P, _P,
+                                    _i32p, _i32p, C.c_int32, _P]),
+    "pool_stats": (C.c_int32, [_P, _i64p, _i64p, _i64p]),
+    "pool_sample_pages": (C.c_int32, [_P, C.c_uint64, _u64p, C.c_int32, _i32p]),
+    "pool_sample_info": (C.c_int32, [_P, C.c_uint64, _i32p, _i32p, _i32p]),
+    "pool_translate": (C.c_int32, [_P, C.c_uint64, _i32p, _u64p]),
+    "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+def _check(status: int, where: str) -> None:
+    if status != FP_OK:
+        raise FlowPoolError(status, where, _lib.fp_last_error().decode(errors="replace"))
+
+
+def _arr(a, dtype, ptype):
+    """Contiguous numpy array of ``dtype`` and a ctypes pointer to it (None if a is None)."""
+    if a is None:
+        return None, None
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(ptype)
+
+
+def _ptr(x) -> Optional[int]:
+    """Device address of a torch tensor / integer / None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+# ------------------------------------------------------------------ entry points
+
+def fp_abi_version() -> int:
+    return int(_lib.fp_abi_version())
+
+
+def fp_last_error() -> str:
+    return _lib.fp_last_error().decode(errors="replace")
+
+
+def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int = 0,
+                alloc: str = "contig", vocab: int = 0, device: int = 0, gva_start: int = 0,
+                max_samples: int = 0, meta_bytes: int = 0, frame_shuffle_seed: int = 0,
+                chunk_bytes: int = 0, world_size: int = 1, rank: int = 0) -> int:
+    cfg = fp_pool_config()
+    _lib.fp_config_init(C.byref(cfg))
+    cfg.hidden, cfg.page_tokens = hidden, page_tokens
+    cfg.hbm_pages, cfg.host_pages = hbm_pages, host_pages
+    cfg.alloc_policy = ALLOC_POLICIES[alloc] if isinstance(alloc, str) else int(alloc)
+    cfg.device, cfg.vocab, cfg.gva_start = device, vocab, gva_start
+    cfg.world_size, cfg.rank = world_size, rank
+    cfg.max_samples, cfg.meta_bytes = max_samples, meta_bytes
+    cfg.frame_shuffle_seed, cfg.chunk_bytes = frame_shuffle_seed, chunk_bytes
+    out = _P()
+    _check(_lib.pool_create(C.byref(cfg), C.byref(out)), "pool_create")
+    return int(out.value)
+
+
+def pool_destroy(pool: int) -> None:
+    _check(_lib.pool_destroy(pool), "pool_destroy")
+
+
+def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page_tier_wish=None,
+                      stream=None) -> int:
+    t, tp = _arr(text_ids, np.int32, _i32p)
+    p, pp = _arr(img_pos, np.int32, _i32p)
+    v, vp = _arr(img_ntok, np.int32, _i32p)
+    w, wp = _arr(page_tier_wish, np.uint8, _u8p)
+    sid = C.c_uint64()
+    _check(_lib.pool_write_sample(pool, tp, len(t), pp, vp, len(p), _ptr(vis_emb), wp, _stream(stream),
+                                  C.byref(sid)), "pool_write_sample")
+    return int(sid.value)
+
+
+def pool_free_sample(pool: int, sample_id: int) -> None:
+    _check(_lib.pool_free_sample(pool, sample_id), "pool_free_sample")
+
+
+def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: int, stream=None):
+    """Returns dict(assign, mb_tokens, mb_cost_scaled, mb_max_len, sample_cost_scaled)."""
+    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    n = len(ids)
+    assign = np.empty(n, np.int32)
+    tok = np.empty(n_mb, np.int32)
+    cst = np.empty(n_mb, np.int64)
+    mx = np.empty(n_mb, np.int32)
+    sc = np.empty(n, np.int64)
+    _check(_lib.plan_microbatches(pool, idp, n, capacity, n_mb, cost_k,
+                                  assign.ctypes.data_as(_i32p), tok.ctypes.data_as(_i32p),
+                                  cst.ctypes.data_as(_i64p), mx.ctypes.data_as(_i32p),
+                                  sc.ctypes.data_as(_i64p), _stream(stream)), "plan_microbatches")
+    return dict(assign=assign, mb_tokens=tok, mb_cost_scaled=cst, mb_max_len=mx, sample_cost_scaled=sc)
+
+
+def plan_partition(lengths, costs_scaled, capacity: int, n_mb: int):
+    """Host-only greedy partition. Returns dict(assign, mb_tokens, mb_cost_scaled, mb_max_len)."""
+    ln, lp = _arr(lengths, np.int32, _i32p)
+    cs, cp = _arr(costs_scaled, np.int64, _i64p)
+    n = len(ln)
+    assign = np.empty(n, np.int32)
+    tok = np.empty(n_mb, np.int32)
+    cst = np.empty(n_mb, np.int64)
+    mx = np.empty(n_mb, np.int32)
+    _check(_lib.plan_partition(lp, cp, n, capacity, n_mb, assign.ctypes.data_as(_i32p),
+                               tok.ctypes.data_as(_i32p), cst.ctypes.data_as(_i64p),
+                               mx.ctypes.data_as(_i32p)), "plan_partition")
+    return dict(assign=assign, mb_tokens=tok, mb_cost_scaled=cst, mb_max_len=mx)
+
+
+def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out_rows_cap: int,
+                    out_cu_seqlens=None, out_position_ids=None, tier_mask: int = FP_TIER_MASK_ALL,
+                    stream=None):
+    """Enqueue the pack of ``sample_ids`` into ``out_emb``. Returns (n_tokens, max_seqlen)."""
+    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    n_tok = C.c_int32()
+    mx = C.c_int32()
+    _check(_lib.pack_microbatch(pool, idp, len(ids), _ptr(embed_table), vocab, _ptr(out_emb), out_rows_cap,
+                                _ptr(out_cu_seqlens), _ptr(out_position_ids), C.byref(n_tok), C.byref(mx),
+                                tier_mask, _stream(stream)), "pack_microbatch")
+    return int(n_tok.value), int(mx.value)
+
+
+def pool_stats(pool: int):
+    a, b, c = C.c_int64(), C.c_int64(), C.c_int64()
+    _check(_lib.pool_stats(pool, C.byref(a), C.byref(b), C.byref(c)), "pool_stats")
+    return dict(free_hbm_pages=a.value, free_host_pages=b.value, n_samples=c.value)
+
+
+def pool_sample_pages(pool: int, sample_id: int):
+    n = C.c_int32()
+    st = _lib.pool_sample_pages(pool, sample_id, None, 0, C.byref(n))
+    if st != FP_OK and not (st == FP_EINVAL and n.value > 0):
+        _check(st, "pool_sample_pages")
+    out = np.empty(max(n.value, 1), np.uint64)
+    _check(_lib.pool_sample_pages(pool, sample_id, out.ctypes.data_as(_u64p), len(out), C.byref(n)),
+           "pool_sample_pages")
+    return out[:n.value]
+
+
+def pool_sample_info(pool: int, sample_id: int):
+    a, b, c = C.c_int32(), C.c_int32(), C.c_int32()
+    _check(_lib.pool_sample_info(pool, sample_id, C.byref(a), C.byref(b), C.byref(c)), "pool_sample_info")
+    return dict(length=a.value, n_text=b.value, n_vis=c.value)
+
+
+def pool_translate(pool: int, gva: int):
+    t, ph = C.c_int32(), C.c_uint64()
+    _check(_lib.pool_translate(pool, gva, C.byref(t), C.byref(ph)), "pool_translate")
+    return int(t.value), int(ph.value)
+
+
+def pool_layout(pool: int):
+    rs = (C.c_uint64 * 2)()
+    ss = (C.c_uint64 * 2)()
+    pb = C.c_int64()
+    _check(_lib.pool_layout(pool, rs, ss, C.byref(pb)), "pool_layout")
+    return dict(region_start=list(rs), segment_start=list(ss), page_bytes=pb.value)

@@ -1,0 +1,137 @@
+"""Drives libflowpool through a synthetic workload on the GPU (tests, bench, smoke).
+
+Builds a pool from a workload configuration, optionally fragments it with
+the churn op sequence, writes the measured samples (producer side), plans
+microbatches and packs them (consumer side). Every library call goes through
+``paper_2606_23087_amd.flowpool``; this module only allocates torch tensors
+and passes their addresses.
+"""
+
+from __future__ import annotations
+
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import flowpool as fp
+from .workloads import (TAG_TEXT, TAG_VIS, SampleSpec, WorkloadConfig, churn_ops, gen_samples,
+                        page_tier_draws, table_torch, visual_rows_torch)
+
+
+def tagged_rows_torch(n_rows: int, hidden: int, seed: int, tag: int, a, b, device="cuda"):
+    """Random-bit rows whose first four words are (tag, lo16(a), hi16(a), b);
+    a and b are int tensors of length n_rows (or scalars)."""
+    g = torch.Generator(device=device)
+    g.manual_seed((int(seed) * 0x632BE5AB + int(tag)) & ((1 << 63) - 1))
+    x = torch.randint(0, 1 << 16, (n_rows, hidden), generator=g, device=device, dtype=torch.int32)
+    a = torch.as_tensor(a, device=device, dtype=torch.int64).expand(n_rows)
+    b = torch.as_tensor(b, device=device, dtype=torch.int64).expand(n_rows)
+    x[:, 0] = tag
+    x[:, 1] = (a & 0xFFFF).to(torch.int32)
+    x[:, 2] = ((a >> 16) & 0xFFFF).to(torch.int32)
+    x[:, 3] = (b & 0xFFFF).to(torch.int32)
+    return _u16(x)
+
+
+def _u16(x: torch.Tensor) -> torch.Tensor:
+    """int32 tensor holding 0..65535 -> int16 tensor with the same 16-bit patterns."""
+    return (x - ((x >= 32768).to(torch.int32) << 16)).to(torch.int16)
+
+
+def vis_rows(cfg: WorkloadConfig, seed: int, index: int, n_vis: int, mode: str, device="cuda"):
+    """Visual rows of sample ``index`` on the device, as a bf16-sized tensor."""
+    if mode == "normal":
+        return visual_rows_torch(cfg, seed, index, n_vis, device)
+    if mode == "tagged":
+        return tagged_rows_torch(n_vis, cfg.hidden, seed * 7919 + index, TAG_VIS, index,
+                                 torch.arange(n_vis, device=device), device)
+    raise ValueError(mode)
+
+
+def table_rows(cfg: WorkloadConfig, seed: int, mode: str, device="cuda"):
+    if mode == "normal":
+        return table_torch(cfg, seed, device)
+    if mode == "tagged":
+        return tagged_rows_torch(cfg.vocab, cfg.hidden, seed, TAG_TEXT,
+                                 torch.arange(cfg.vocab, device=device), 0, device)
+    raise ValueError(mode)
+
+
+class GpuWorkload:
+    """A pool on the GPU holding one workload's resident samples."""
+
+    def __init__(self, cfg: WorkloadConfig, seed: int, mode: str = "normal",
+                 specs: Optional[List[SampleSpec]] = None,
+                 vis_fn: Optional[Callable[[int, SampleSpec], torch.Tensor]] = None,
+                 table: Optional[torch.Tensor] = None, churn: bool = True,
+                 frame_shuffle_seed: int = 0, device: int = 0, log=None):
+        self.cfg = cfg
+        self.seed = seed
+        self.device = device
+        self.pool = fp.pool_create(hidden=cfg.hidden, page_tokens=cfg.page_tokens, hbm_pages=cfg.hbm_pages,
+                                   host_pages=cfg.host_pages, alloc=cfg.alloc, vocab=cfg.vocab,
+                                   device=device, frame_shuffle_seed=frame_shuffle_seed)
+        dev = f"cuda:{device}"
+        self.churn_ids: Dict[int, int] = {}
+        if churn and cfg.churn_steps:
+            for op in churn_ops(cfg, seed):
+                if op.kind == "write":
+                    s = op.spec
+                    self.churn_ids[op.key] = fp.pool_write_sample(self.pool, s.text_ids, s.img_pos, s.img_ntok)
+                else:
+                    fp.pool_free_sample(self.pool, self.churn_ids.pop(op.key))
+            if log:
+                log(f"churn done: {len(self.churn_ids)} churn samples resident, {fp.pool_stats(self.pool)}")
+        self.specs = specs if specs is not None else gen_samples(cfg, seed)
+        self.table = table if table is not None else table_rows(cfg, seed, mode, dev)
+        self.ids: List[int] = []
+        for i, s in enumerate(self.specs):
+            vis = vis_fn(i, s) if vis_fn is not None else (vis_rows(cfg, seed, i, s.n_vis, mode, dev)
+                                                         if s.n_vis else None)
+            wish = None
+            if cfg.tier_split:
+                wish = page_tier_draws(seed, i, -(-s.n_vis // cfg.page_tokens))
+            self.ids.append(fp.pool_write_sample(self.pool, s.text_ids, s.img_pos, s.img_ntok, vis, wish))
+            del vis
+        torch.cuda.synchronize(device)
+
+    def plan(self, ids: Optional[Sequence[int]] = None, stream=None):
+        cfg = self.cfg
+        ids = self.ids if ids is None else list(ids)
+        return fp.plan_microbatches(self.pool, ids, cfg.capacity, cfg.n_mb, cfg.cost_k, stream)
+
+    def microbatches(self, plan, ids: Optional[Sequence[int]] = None) -> List[List[int]]:
+        """Sample ids of each microbatch, keeping the order of ``ids``."""
+        ids = self.ids if ids is None else list(ids)
+        out: List[List[int]] = [[] for _ in range(len(plan["mb_tokens"]))]
+        for sid, j in zip(ids, plan["assign"].tolist()):
+            if j >= 0:
+                out[j].append(sid)
+        return out
+
+    def alloc_outputs(self, rows: Optional[int] = None, fill: Optional[int] = None):
+        rows = self.cfg.capacity if rows is None else rows
+        dev = f"cuda:{self.device}"
+        out = torch.empty((rows, self.cfg.hidden), dtype=torch.int16, device=dev)
+        if fill is not None:
+            out.fill_(fill)
+        cu = torch.full((self.cfg.capacity + 1,), -1, dtype=torch.int32, device=dev)
+        pos = torch.full((rows,), -1, dtype=torch.int32, device=dev)
+        return out, cu, pos
+
+    def pack(self, sample_ids, out, cu=None, pos=None, tier_mask=fp.FP_TIER_MASK_ALL, stream=None):
+        return fp.pack_microbatch(self.pool, sample_ids, self.table, self.cfg.vocab, out, out.shape[0],
+                                  cu, pos, tier_mask, stream)
+
+    def close(self):
+        if self.pool:
+            torch.cuda.synchronize(self.device)
+            fp.pool_destroy(self.pool)
+            self.pool = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,256 @@
+"""GPU parity of the HIP path against the CPU oracle, element by element, on
+seeded inputs small enough for the oracle (each microbatch spans many
+workgroup tiles and ends in a ragged tail).
+
+Every case prints its name, seed and shape before touching the GPU.
+Bar: bit-exact (pure indexing and raw 16-bit copies; integer plan).
+"""
+
+import numpy as np
+import pytest
+
+from gpu_common import oracle_plan, oracle_pool_for, say, to_dev, to_host
+from oracle.pack import definitional_pack
+from oracle.pool import MASK_HBM, MASK_HOST
+from paper_2606_23087_amd.workloads import (CONFIGS, SampleSpec, gen_samples, scaled, table_np,
+                                            visual_rows_np)
+from tagging import decode, tagged_table, tagged_vis
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def fp():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_23087_amd import flowpool
+    return flowpool
+
+
+def _inputs(cfg, seed, specs, mode):
+    if mode == "tagged":
+        table = tagged_table(cfg.vocab, cfg.hidden, seed)
+        vis = [tagged_vis(i, s.n_vis, cfg.hidden, seed) for i, s in enumerate(specs)]
+    elif mode == "bits":
+        table = table_np(cfg, seed, mode="bits")
+        vis = [visual_rows_np(cfg, seed, i, s.n_vis, mode="bits") for i, s in enumerate(specs)]
+    else:
+        table = table_np(cfg, seed)
+        vis = [visual_rows_np(cfg, seed, i, s.n_vis) for i, s in enumerate(specs)]
+    return table, vis
+
+
+def _run_case(fp, cfg, seed, specs, mode="tagged", frame_shuffle_seed=0, check_pages=True):
+    """Write specs into a GPU pool and the oracle pool, plan both, pack every
+    microbatch on the GPU and compare everything with the oracle."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    say(f"case {cfg.name} seed={seed} mode={mode} H={cfg.hidden} P={cfg.page_tokens} "
+        f"samples={len(specs)} shuffle={frame_shuffle_seed}")
+    table, vis = _inputs(cfg, seed, specs, mode)
+    w = GpuWorkload(cfg, seed, specs=specs, table=to_dev(table),
+                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None,
+                    frame_shuffle_seed=frame_shuffle_seed)
+    try:
+        opool, oids = oracle_pool_for(cfg, seed, specs, vis)
+        if check_pages:
+            for gid, oid in zip(w.ids, oids):
+                assert fp.pool_sample_pages(w.pool, gid).tolist() == opool.sample_pages(oid)
+        plan = w.plan()
+        assign, tok, cst, mem = oracle_plan(cfg, specs)
+        assert plan["assign"].tolist() == assign
+        assert plan["mb_tokens"].tolist() == tok and plan["mb_cost_scaled"].tolist() == cst
+        out, cu, pos = w.alloc_outputs(fill=0x3C3C)
+        for j, idx in enumerate(mem):
+            gids = [w.ids[i] for i in idx]
+            n_tok, mx = w.pack(gids, out, cu, pos)
+            torch.cuda.synchronize()
+            want = opool.pack([oids[i] for i in idx], table)
+            ref = definitional_pack([specs[i] for i in idx], [vis[i] for i in idx], table)
+            assert np.array_equal(want[0], ref[0]) and np.array_equal(want[1], ref[1])
+            assert n_tok == want[3] and mx == want[4]
+            got = to_host(out[:n_tok])
+            assert np.array_equal(got, want[0]), f"microbatch {j}: rows differ"
+            assert np.array_equal(to_host(out[n_tok:]), np.full((out.shape[0] - n_tok, cfg.hidden), 0x3C3C,
+                                                                dtype=np.uint16)), "rows past n_tokens touched"
+            assert cu[:len(idx) + 1].cpu().numpy().tolist() == want[1].tolist()
+            assert pos[:n_tok].cpu().numpy().tolist() == want[2].tolist()
+            out.fill_(0x3C3C)
+        return w, opool, oids, table, vis
+    except Exception:
+        w.close()
+        raise
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("mode", ["tagged", "normal"])
+def test_tiny_full_pipeline(fp, seed, mode):
+    cfg = CONFIGS["tiny"]
+    w, *_ = _run_case(fp, cfg, seed, gen_samples(cfg, seed), mode)
+    w.close()
+
+
+# Real hidden sizes, page sizes and sample shapes; fewer samples, small pools
+# and a reduced vocabulary so the oracle finishes in seconds.
+SMALL = {
+    "qwen": dict(hbm_pages=600, vocab=3000, capacity=16384, n_mb=2, count=9),
+    "frag70b": dict(hbm_pages=1200, vocab=3000, capacity=16384, n_mb=2, count=5, churn_steps=300),
+    "video": dict(hbm_pages=400, vocab=3000, capacity=40000, n_mb=2, count=5),
+    "tiered": dict(hbm_pages=150, host_pages=150, vocab=3000, capacity=12000, n_mb=2, count=6),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("seed", [0, 1])
+def test_small_configs(fp, name, seed):
+    kw = dict(SMALL[name])
+    count = kw.pop("count")
+    cfg = scaled(CONFIGS[name], **kw)
+    w, opool, oids, table, vis = _run_case(fp, cfg, seed, gen_samples(cfg, seed, count=count),
+                                           "tagged" if seed == 0 else "bits")
+    w.close()
+
+
+def test_all_bit_patterns(fp):
+    """Every one of the 65536 16-bit patterns (NaN payloads, signed zeros,
+    denormals, infinities) is copied unchanged."""
+    cfg = scaled(CONFIGS["tiny"], vocab=300, hbm_pages=512, capacity=5000, n_mb=1)
+    specs = [SampleSpec(np.arange(10, 200, dtype=np.int32) % 300, np.array([7, 150], np.int32),
+                        np.array([256, 300], np.int32))]
+    say("case all-bit-patterns")
+    table = np.arange(300 * 256, dtype=np.uint32).astype(np.uint16).reshape(300, 256)
+    vis = [(np.arange(556 * 256, dtype=np.uint32) * 7 + 3).astype(np.uint16).reshape(556, 256)]
+    allpat = np.zeros(1 << 16, bool)
+    allpat[vis[0].ravel()] = True
+    assert allpat.all()
+    from paper_2606_23087_amd.harness import GpuWorkload
+    w = GpuWorkload(cfg, 0, specs=specs, table=to_dev(table), vis_fn=lambda i, s: to_dev(vis[i]))
+    out, cu, pos = w.alloc_outputs(rows=1000)
+    n, _ = w.pack(w.ids, out, cu, pos)
+    torch.cuda.synchronize()
+    want = definitional_pack(specs, vis, table)
+    assert np.array_equal(to_host(out[:n]), want[0])
+    w.close()
+
+
+def test_placement_independence(fp):
+    """The same samples packed from pools whose physical frames are bound in
+    different orders give identical bytes (Sec. 3.1 / Sec. 3.2: consumers
+    read by GVA, unaware of physical placement)."""
+    cfg = scaled(CONFIGS["qwen"], hbm_pages=600, vocab=3000, capacity=16384, n_mb=2)
+    specs = gen_samples(cfg, 4, count=8)
+    for shuffle in (0, 12345):
+        w, *_ = _run_case(fp, cfg, 4, specs, "tagged", frame_shuffle_seed=shuffle)
+        w.close()
+
+
+def test_edge_cases(fp):
+    """Degenerate samples and microbatches: text only, images only, empty
+    images, images at position 0 and at the end, one-row samples, an empty
+    microbatch, more than 256 samples in one microbatch, duplicated ids."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    say("case edge-cases")
+    H = 3584
+    cfg = scaled(CONFIGS["qwen"], hbm_pages=400, vocab=500, capacity=4000, n_mb=1)
+    rng = np.random.default_rng(7)
+    specs = [
+        SampleSpec(np.array([5, 6, 7], np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32)),
+        SampleSpec(np.zeros(0, np.int32), np.array([0, 0], np.int32), np.array([70, 1], np.int32)),
+        SampleSpec(np.array([1, 2], np.int32), np.array([0, 1, 2, 2], np.int32), np.array([0, 64, 0, 65], np.int32)),
+        SampleSpec(np.array([9], np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32)),
+        SampleSpec(np.zeros(0, np.int32), np.array([0], np.int32), np.array([1], np.int32)),
+    ]
+    specs += [SampleSpec(rng.integers(0, 500, size=int(rng.integers(1, 4))).astype(np.int32),
+                         np.zeros(0, np.int32), np.zeros(0, np.int32)) for _ in range(300)]
+    table = tagged_table(500, H)
+    vis = [tagged_vis(i, s.n_vis, H) for i, s in enumerate(specs)]
+    w = GpuWorkload(cfg, 0, specs=specs, table=to_dev(table),
+                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None)
+    out, cu, pos = w.alloc_outputs(rows=2000, fill=0x1111)
+    cu = torch.full((400,), -1, dtype=torch.int32, device="cuda")
+    groups = [[0], [1], [2], [3], [4], [0, 1, 2, 3, 4], list(range(len(specs))), [2, 2, 0, 2], []]
+    for g in groups:
+        say(f"  edge group of {len(g)} samples")
+        n, mx = w.pack([w.ids[i] for i in g], out, cu, pos)
+        torch.cuda.synchronize()
+        want = definitional_pack([specs[i] for i in g], [vis[i] for i in g], table)
+        assert n == len(want[0]) and mx == want[3]
+        assert np.array_equal(to_host(out[:n]), want[0])
+        assert cu[:len(g) + 1].cpu().numpy().tolist() == want[1].tolist()
+        assert pos[:n].cpu().numpy().tolist() == want[2].tolist()
+        assert bool((out[n:] == 0x1111).all())
+        out.fill_(0x1111)
+    w.close()
+
+
+def test_error_paths(fp):
+    from paper_2606_23087_amd.harness import GpuWorkload
+    say("case error-paths")
+    cfg = scaled(CONFIGS["tiny"], hbm_pages=8, capacity=512, n_mb=2)
+    specs = gen_samples(cfg, 0, count=1)
+    w = GpuWorkload(cfg, 0, specs=specs, mode="tagged")
+    pool = w.pool
+    out, cu, pos = w.alloc_outputs()
+    before = fp.pool_stats(pool)
+    bad = [
+        (dict(text_ids=[1, 2], img_pos=[3], img_ntok=[1]), "EINVAL"),
+        (dict(text_ids=[1, 2], img_pos=[2, 1], img_ntok=[1, 1]), "EINVAL"),
+        (dict(text_ids=[1000], img_pos=[], img_ntok=[]), "EINVAL"),
+        (dict(text_ids=[], img_pos=[], img_ntok=[]), "EINVAL"),
+        (dict(text_ids=[1], img_pos=[0], img_ntok=[8 * 16 + 1]), "ENOMEM"),
+    ]
+    for kw, code in bad:
+        with pytest.raises(fp.FlowPoolError) as e:
+            fp.pool_write_sample(pool, **kw)
+        assert e.value.code == code
+        assert fp.pool_stats(pool) == before
+    sid = w.ids[0]
+    n = specs[0].length
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out, n - 1)
+    assert e.value.code == "ECAPACITY"
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, int(out.data_ptr()) + 2, n)
+    assert e.value.code == "EALIGN"
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab - 1, out, n)
+    assert e.value.code == "EINVAL"
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.plan_microbatches(pool, [sid, sid], 512, 2, 4096)
+    assert e.value.code == "EINVAL"
+    fp.pool_free_sample(pool, sid)
+    for call in (lambda: fp.pool_free_sample(pool, sid),
+                 lambda: fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out, 512),
+                 lambda: fp.plan_microbatches(pool, [sid], 512, 2, 4096)):
+        with pytest.raises(fp.FlowPoolError) as e:
+            call()
+        assert e.value.code == "ENOENT"
+    w.close()
+
+
+def test_tier_mask_split(fp):
+    """Host-tier rows read zero-copy over PCIe: a pack with the HBM mask and
+    one with the host mask write together what one full pack writes."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    cfg = scaled(CONFIGS["tiered"], hbm_pages=150, host_pages=150, vocab=3000, capacity=12000, n_mb=2)
+    specs = gen_samples(cfg, 3, count=6)
+    w, opool, oids, table, vis = _run_case(fp, cfg, 3, specs, "tagged")
+    say("case tier-mask-split")
+    plan = w.plan()
+    mbs = w.microbatches(plan)
+    full, cu, pos = w.alloc_outputs(fill=0)
+    part, cu2, pos2 = w.alloc_outputs(fill=0x2222)
+    for j, g in enumerate(mbs):
+        n, _ = w.pack(g, full, cu, pos)
+        n2, _ = w.pack(g, part, cu2, pos2, tier_mask=fp.FP_TIER_MASK_HBM)
+        torch.cuda.synchronize()
+        gi = [w.ids.index(x) for x in g]
+        want_hbm = opool.pack([oids[i] for i in gi], table, tier_mask=MASK_HBM,
+                              out=np.full((n, cfg.hidden), 0x2222, np.uint16))
+        assert np.array_equal(to_host(part[:n]), want_hbm[0])
+        fp.pack_microbatch(w.pool, g, None, 0, part, part.shape[0], None, None, fp.FP_TIER_MASK_HOST)
+        torch.cuda.synchronize()
+        assert torch.equal(part[:n], full[:n]) and torch.equal(cu, cu2) and torch.equal(pos, pos2)
+        part.fill_(0x2222)
+    w.close()

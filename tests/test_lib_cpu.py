@@ -1,0 +1,77 @@
+"""The C-ABI library without a GPU: it loads, exports every entry point the
+header declares, and its host-only greedy partition equals the oracle's."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from oracle.plan import cost_scaled, greedy_partition
+
+fp = pytest.importorskip("paper_2606_23087_amd.flowpool",
+                         reason="libflowpool.so not built (run __graft_entry__.build())")
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "flowpool.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:fp_status|int32_t|const char\s*\*|void)\s+(\w+)\s*\(", src, flags=re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert {"pool_create", "pool_write_sample", "pool_free_sample", "plan_microbatches",
+            "pack_microbatch"} <= set(names)
+    lib = ctypes.CDLL(fp.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(fp.EXPORTED)
+    assert fp.fp_abi_version() == 1
+
+
+def test_config_struct_matches_header():
+    # fp_pool_config: 2*i32, 2*i64, 2*i32, i64, u64, 2*i32, 2*i64, u64, i64, 2 ptrs
+    assert ctypes.sizeof(fp.fp_pool_config) == 8 + 16 + 8 + 8 + 8 + 8 + 16 + 8 + 8 + 16
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_plan_partition_equals_oracle(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(0, 300))
+    M = int(rng.integers(1, 70))
+    K = int(rng.integers(1, 9000))
+    lengths = rng.integers(1, 5000, size=n)
+    if seed % 3 == 0 and n:
+        lengths = rng.choice([100, 200, 300], size=n)       # many ties
+    C = int(rng.integers(5000, 40000))
+    costs = [cost_scaled(int(l), K) for l in lengths]
+    got = fp.plan_partition(lengths, costs, C, M)
+    assign, tok, cst = greedy_partition([int(x) for x in lengths], K, C, M)
+    assert got["assign"].tolist() == assign
+    assert got["mb_tokens"].tolist() == tok and got["mb_cost_scaled"].tolist() == cst
+    mx = [max([int(lengths[i]) for i in range(n) if assign[i] == j], default=0) for j in range(M)]
+    assert got["mb_max_len"].tolist() == mx
+
+
+def test_plan_partition_errors():
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.plan_partition([1, 2], [1, 2], 10, 0)
+    assert e.value.code == "EINVAL"
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.plan_partition([0], [0], 10, 1)
+    assert e.value.code == "EINVAL"
+    assert fp.plan_partition([], [], 10, 2)["mb_tokens"].tolist() == [0, 0]
+
+
+def test_pool_create_rejects_bad_config_without_gpu():
+    # Argument checks come before any device call.
+    for kw in [dict(hidden=4), dict(hidden=12), dict(page_tokens=0), dict(hbm_pages=0),
+               dict(alloc=7), dict(world_size=2)]:
+        args = dict(hidden=256, page_tokens=16, hbm_pages=4)
+        args.update(kw)
+        with pytest.raises(fp.FlowPoolError) as e:
+            fp.pool_create(**args)
+        assert e.value.code == "EINVAL"
