@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged translate-gather-pack on one MI355X.
+
+One step = one pass of the whole hot path over the resident samples of one
+workload: the planner (GPU cost kernel + greedy partition into M
+microbatches) followed by pack_microbatch of every microbatch (prefix sum,
+page walk, visual-row gather, text-table gather, position ids).
+
+Prints ONE JSON line. ``value`` is the whole-step effective bandwidth:
+algorithmic bytes of all packs / wall time of the timed steps (inputs already
+resident in HBM). ``roofline`` is for the pack kernel alone: algorithmic
+bytes per launch / mean launch duration from HIP events recorded on the pack
+stream around every pack in the timed steps. ``cpu_baseline`` times the CPU
+oracle's pool pack on a bounded sample of the same microbatches.
+
+Algorithmic bytes of one pack (each valid row read once and written once):
+  2*n_tokens*row_bytes + 4*n_text (ids) + 16*pages (GVA + PTE)
+  + 4*n_tokens (position ids) + 4*(n+1) (cu_seqlens) + 48*n (descriptors)
+  + 8*images (placeholder pairs)
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E peak
+PCIE_PEAK_GBPS = 63.0           # PCIe Gen5 x16, one direction
+
+METRIC = "pack_microbatch effective GB/s and % of HBM peak (hidden 3584 bf16)"
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def pack_bytes(cfg, specs) -> int:
+    rb = cfg.row_bytes
+    tokens = sum(s.length for s in specs)
+    n_text = sum(s.n_text for s in specs)
+    pages = sum(-(-s.n_vis // cfg.page_tokens) for s in specs)
+    images = sum(len(s.img_ntok) for s in specs)
+    n = len(specs)
+    return 2 * tokens * rb + 4 * n_text + 16 * pages + 4 * tokens + 4 * (n + 1) + 48 * n + 8 * images
+
+
+def kernel_source_hash() -> str:
+    path = os.path.join(ROOT, "paper_2606_23087_amd", "csrc", "kernels.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per pack launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"pack_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_sha256:\s*([0-9a-f]+)", text)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t or m.group(1) != kernel_source_hash():
+        return None
+    return float(t.group(1))
+
+
+def cpu_baseline(cfg, w, mbs, seed: int, budget_s: float):
+    """Time the oracle's pool pack on the samples of the first microbatches."""
+    import numpy as np
+    import torch
+
+    from oracle.pool import OraclePool
+    from paper_2606_23087_amd.harness import vis_rows
+    from paper_2606_23087_amd.workloads import page_tier_draws
+
+    take = [mb for mb in mbs if mb][:2]
+    index = {sid: i for i, sid in enumerate(w.ids)}
+    pool = OraclePool(cfg.hidden, cfg.page_tokens, cfg.hbm_pages, cfg.host_pages, cfg.alloc, cfg.vocab)
+    table = w.table.cpu().view(torch.int16).numpy().view(np.uint16)
+    oid = {}
+    for mb in take:
+        for sid in mb:
+            i = index[sid]
+            s = w.specs[i]
+            rows = vis_rows(cfg, seed, i, s.n_vis, "normal").cpu().view(torch.int16).numpy().view(np.uint16) \
+                if s.n_vis else np.zeros((0, cfg.hidden), np.uint16)
+            wish = page_tier_draws(seed, i, -(-s.n_vis // cfg.page_tokens)) if cfg.tier_split else None
+            oid[sid] = pool.write(s.text_ids, s.img_pos, s.img_ntok, rows, tier_wish=wish)
+    total_bytes = 0
+    t0 = time.perf_counter()
+    packs = 0
+    while True:
+        for mb in take:
+            pool.pack([oid[s] for s in mb], table)
+            total_bytes += pack_bytes(cfg, [w.specs[index[s]] for s in mb])
+            packs += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=round(total_bytes / el / 1e9, 4), unit="GB/s", cores=1, kind="oracle",
+                sample=f"{len(take)} of {cfg.n_mb} microbatches of seed {seed} "
+                       f"({sum(len(m) for m in take)} samples), packed {packs} times in {el:.1f} s "
+                       f"by the single-threaded numpy pool oracle",
+                cpu_model=platform.processor() or platform.machine(),
+                os_cpu_count=os.cpu_count(), affinity=len(os.sched_getaffinity(0)))
+
+
+def d2d_ceiling(nbytes: int = 1 << 30, iters: int = 10) -> float:
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / iters
+    del a, b
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen", choices=["tiny", "qwen", "frag70b", "video", "tiered"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--buffers", type=int, default=4, help="rotating output buffers")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle timing")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run one plain 1 GiB copy (reference for HBM byte counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this build "
+              "(run with --gpus 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2606_23087_amd import flowpool as fp
+    from paper_2606_23087_amd.harness import GpuWorkload
+    from paper_2606_23087_amd.workloads import CONFIGS
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = CONFIGS[args.workload]
+    t_setup = time.perf_counter()
+    log(f"workload {cfg.name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}")
+    w = GpuWorkload(cfg, args.seed, mode="normal", log=log)
+    log(f"pool built: {len(w.ids)} samples in {time.perf_counter() - t_setup:.1f} s, {fp.pool_stats(w.pool)}")
+    spec_of = {sid: s for sid, s in zip(w.ids, w.specs)}
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log("calibration copy: 1 GiB read + 1 GiB written")
+
+    pack_stream = torch.cuda.Stream()
+    plan_stream = torch.cuda.Stream()
+    outs = [w.alloc_outputs() for _ in range(max(1, args.buffers))]
+
+    def one_step(events=None):
+        plan = w.plan(stream=plan_stream)
+        mbs = w.microbatches(plan)
+        k = 0
+        for j, mb in enumerate(mbs):
+            out, cu, pos = outs[j % len(outs)]
+            if events is not None:
+                events[k][0].record(pack_stream)
+            w.pack(mb, out, cu, pos, stream=pack_stream)
+            if events is not None:
+                events[k][1].record(pack_stream)
+            k += 1
+        return plan, mbs
+
+    plan, mbs = one_step()
+    step_bytes = sum(pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs)
+    step_tokens = int(plan["mb_tokens"].sum())
+    deferred = int((plan["assign"] < 0).sum())
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"warmup done: {len(mbs)} microbatches, {step_tokens} tokens, {step_bytes / 1e6:.1f} MB per step, "
+        f"{deferred} samples deferred")
+
+    n_packs = sum(1 for _ in mbs)
+    events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n_packs)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    durs = np.array([[s.elapsed_time(e) * 1e-3 for s, e in ev] for ev in events])   # seconds
+    mb_bytes = np.array([pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs], dtype=np.float64)
+
+    value = step_bytes * args.steps / wall / 1e9
+    kernel_gbps = mb_bytes.sum() * args.steps / durs.sum() / 1e9
+    per_call = (mb_bytes[None, :] / durs / 1e9).ravel()
+    traffic = counter_traffic(cfg.name)
+    mean_bytes = float(mb_bytes.mean())
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-h{cfg.hidden}", "hidden": cfg.hidden, "page_tokens": cfg.page_tokens,
+                   "pool_pages": cfg.hbm_pages + cfg.host_pages, "alloc": cfg.alloc, "capacity": cfg.capacity,
+                   "n_mb": cfg.n_mb, "cost_k": cfg.cost_k, "samples": len(w.ids), "seed": args.seed,
+                   "parallelism": "none (1 GPU)"},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "tokens_per_s": round(step_tokens * args.steps / wall, 1),
+        "step_tokens": step_tokens,
+        "step_bytes": step_bytes,
+        "deferred_samples": deferred,
+        "pack_kernel": {"launches": int(durs.size), "mean_us": round(float(durs.mean()) * 1e6, 3),
+                        "median_call_GBps": round(float(np.median(per_call)), 2),
+                        "aggregate_GBps": round(kernel_gbps, 2)},
+        "roofline": {"bound": "hbm", "achieved": round(kernel_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(kernel_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": (round(traffic) if traffic else None),
+                     "traffic_over_algorithmic": (round(traffic / mean_bytes, 4) if traffic else None)},
+    }
+    imb = plan["mb_cost_scaled"].max() / plan["mb_cost_scaled"].mean()
+    result["plan"] = {"max_over_mean_cost": round(float(imb), 5),
+                      "eq3_max": round(float(max((t / cfg.capacity) + (m / cfg.capacity) ** 2
+                                                 for t, m in zip(plan["mb_tokens"], plan["mb_max_len"]))), 5)}
+    result["d2d_copy_ceiling_GBps"] = round(d2d_ceiling(), 1)
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        result["cpu_baseline"] = cpu_baseline(cfg, w, mbs, args.seed, args.cpu_budget)
+    else:
+        result["cpu_baseline"] = None
+    w.close()
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

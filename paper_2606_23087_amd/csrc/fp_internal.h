@@ -32,30 +32,52 @@ constexpr uint64_t PTE_HOST = 2ull;
 constexpr uint64_t PTE_ADDR_MASK = ~0xFull;
 
 constexpr int kBlock = 256;          // threads per workgroup for all kernels
-constexpr int kInlineSlots = 256;    // sample slots passed by value to k_pack
-constexpr int kMaxTileRows = 64;     // rows resolved per workgroup tile
-constexpr int kMaxPackSamples = 8192;   // keeps the LDS prefix-sum array at <= 32 KiB
+constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
+constexpr int kVecsPerThread = 8;    // 16-byte vectors each k_pack thread moves
+constexpr int kChunkVecs = kBlock * kVecsPerThread;   // output vectors per k_pack workgroup (32 KiB)
+constexpr int kInlineSamples = 64;   // sample headers passed by value to k_pack
+constexpr int kInlineImages = 128;   // image pairs passed by value to k_pack
+constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds k_pack's LDS use)
+constexpr int kMaxPackImages = 1024;
 
-// Everything one pack launch needs, passed by value (kernel arguments are
-// captured at launch, so no host staging buffer is involved for n <= 256).
+// Per-sample header of a microbatch, taken from the pool's host mirror of
+// the sample metadata (the variable-length parts stay in device memory).
+struct alignas(16) PackSample {
+  int32_t len;        // rows = text + visual
+  int32_t n_img;
+  int32_t img_base;   // index of the sample's first (position, rows) pair
+  int32_t n_text;
+  int64_t text_off;   // metadata-arena byte offset of the text ids
+  int64_t page_off;   // metadata-arena byte offset of the page GVAs
+};
+static_assert(sizeof(PackSample) == 32, "PackSample layout");
+
+// Everything one pack launch needs, passed by value. Kernel arguments are
+// captured at launch, so microbatches of up to kInlineSamples samples and
+// kInlineImages images need no staging copy; larger ones point at a staged
+// device copy of the same arrays.
 struct PackArgs {
-  const SampleDesc* desc;     // device sample table
   const uint8_t* meta;        // device metadata arena
   const uint64_t* pte;        // device page table, index = (gva - gva_start) / page_bytes
   uint64_t gva_start;
   uint64_t page_bytes;
-  const uint8_t* table;       // embedding table (may be null when no text rows)
+  const uint8_t* table;       // embedding table (may be null when no text row is copied)
   uint8_t* out;               // packed rows
   int32_t* cu;                // cu_seqlens or null
   int32_t* pos;               // position ids or null
-  const int32_t* slots_dev;   // slot list in device memory, or null = slots_inline
+  const PackSample* samples_dev;   // staged headers, or null = samples[]
+  const int2* imgs_dev;            // staged image pairs, or null = imgs[]
   int32_t n;                  // samples
+  int32_t n_imgs;             // image pairs
   int32_t n_tokens;           // total rows
   int32_t row_bytes;
   int32_t page_tokens;
   int32_t tier_mask;
-  int32_t tile_rows;          // rows per workgroup tile (<= kMaxTileRows)
-  int32_t slots_inline[kInlineSlots];
+  int32_t max_chunk_rows;     // rows one chunk can touch
+  uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
+  int32_t div_shift;
+  PackSample samples[kInlineSamples];
+  int2 imgs[kInlineImages];
 };
 
 struct WriteArgs {
@@ -72,6 +94,7 @@ struct WriteArgs {
   int32_t tile_rows;
 };
 
+size_t pack_lds_bytes(const PackArgs& a);
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream);
 hipError_t launch_write(const WriteArgs& a, hipStream_t stream);
 hipError_t launch_cost(const SampleDesc* desc, const int32_t* slots, int32_t n, int64_t k,

@@ -19,134 +19,187 @@
 namespace fp {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// Global-address-space views: loads through them compile to global_load
+// (vector memory counter only) instead of flat loads, which also count
+// against the LDS counter and force the compiler to wait for each one.
+typedef __attribute__((address_space(1))) const u32x4 g_u32x4_c;
+typedef __attribute__((address_space(1))) u32x4 g_u32x4;
 
 __device__ __forceinline__ u32x4 load16(const uint8_t* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return __builtin_nontemporal_load((g_u32x4_c*)p);
 }
 
 __device__ __forceinline__ void store16(uint8_t* p, u32x4 v) {
-  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+  __builtin_nontemporal_store(v, (g_u32x4*)p);
 }
 
-__device__ __forceinline__ int32_t slot_at(const PackArgs& a, int i) {
-  return a.slots_dev ? a.slots_dev[i] : a.slots_inline[i];
+template <typename T>
+__device__ __forceinline__ T ld_global(const T* p) {
+  return *(const __attribute__((address_space(1))) T*)p;
 }
 
-// Copies `rows` rows of `row_bytes` bytes: row r goes from src[r] to
-// dst_base + r * row_bytes; a null src[r] skips the row. The rows x 16-byte
-// vectors of the tile are spread evenly over the workgroup, U loads per
-// thread in flight before their stores.
-template <int U>
-__device__ __forceinline__ void copy_tile(const uint8_t* const* src, uint8_t* dst_base, int rows,
-                                          int row_bytes) {
-  const int vpr = row_bytes >> 4;
-  const int total = rows * vpr;
-  for (int e0 = threadIdx.x; e0 < total; e0 += kBlock * U) {
-    u32x4 v[U];
-    int rr[U], cc[U];
-    bool live[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int e = e0 + u * kBlock;
-      live[u] = e < total;
-      rr[u] = live[u] ? e / vpr : 0;
-      cc[u] = e - rr[u] * vpr;
-      const uint8_t* s = src[rr[u]];
-      live[u] = live[u] && s != nullptr;
-      if (live[u]) v[u] = load16(s + (size_t)cc[u] * 16);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (live[u]) store16(dst_base + (size_t)rr[u] * row_bytes + (size_t)cc[u] * 16, v[u]);
-    }
-  }
+__device__ __forceinline__ PackSample ld_sample(const PackSample* p) {
+  const g_u32x4_c* q = (const g_u32x4_c*)p;
+  const u32x4 lo = q[0], hi = q[1];
+  PackSample s;
+  __builtin_memcpy(&s, &lo, 16);
+  __builtin_memcpy(reinterpret_cast<uint8_t*>(&s) + 16, &hi, 16);
+  return s;
 }
 
-template <int U>
-__global__ __launch_bounds__(kBlock) void k_pack(PackArgs a) {
-  extern __shared__ int32_t s_cu[];                 // [n + 1]
-  __shared__ const uint8_t* s_src[kMaxTileRows];
-  __shared__ int32_t s_wsum[kBlock / 64];
+__device__ __forceinline__ int2 ld_pair(const int2* p) {
+  const uint64_t v = ld_global(reinterpret_cast<const uint64_t*>(p));
+  int2 r;
+  r.x = (int)(uint32_t)v;
+  r.y = (int)(uint32_t)(v >> 32);
+  return r;
+}
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int n = a.n;
-
-  // Exclusive prefix sum of the sample lengths, in plan order -> s_cu.
-  if (tid == 0) s_cu[0] = 0;
+// Block-wide exclusive prefix sum of len[0..n) into cu[0..n] (cu[0] = 0).
+__device__ __forceinline__ void block_scan_lengths(const PackSample* smp, int n, int32_t* cu,
+                                                   int32_t* wsum) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) cu[0] = 0;
   int carry = 0;
   for (int base = 0; base < n; base += kBlock) {
     const int i = base + tid;
-    int v = (i < n) ? a.desc[slot_at(a, i)].len : 0;
+    int v = (i < n) ? smp[i].len : 0;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const int t = __shfl_up(v, d, 64);
       if (lane >= d) v += t;
     }
-    if (lane == 63) s_wsum[wave] = v;
+    if (lane == 63) wsum[wave] = v;
     __syncthreads();
     int before = 0, all = 0;
 #pragma unroll
     for (int w = 0; w < kBlock / 64; ++w) {
-      before += (w < wave) ? s_wsum[w] : 0;
-      all += s_wsum[w];
+      before += (w < wave) ? wsum[w] : 0;
+      all += wsum[w];
     }
-    if (i < n) s_cu[i + 1] = carry + before + v;
+    if (i < n) cu[i + 1] = carry + before + v;
     carry += all;
     __syncthreads();
   }
+}
+
+// Index of the sample holding packed row `row`: last k with cu[k] <= row.
+__device__ __forceinline__ int sample_of(const int32_t* cu, int n, int row) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Source address of row r of sample sp (null if the tier mask skips it).
+__device__ __forceinline__ const uint8_t* resolve_row(const PackArgs& a, const PackSample& sp,
+                                                      const int2* img, int r) {
+  // Image j of the sample starts after img.x of its text rows and all rows
+  // of the images before it; text rows fill the gaps.
+  int vis_before = 0, vis_idx = -1;
+  for (int j = 0; j < sp.n_img; ++j) {
+    const int2 pr = img[sp.img_base + j];
+    const int start = pr.x + vis_before;
+    if (r < start) break;
+    if (r < start + pr.y) { vis_idx = vis_before + (r - start); break; }
+    vis_before += pr.y;
+  }
+  if (vis_idx < 0) {
+    if (!(a.tier_mask & 1)) return nullptr;
+    const int32_t id = ld_global(reinterpret_cast<const int32_t*>(a.meta + sp.text_off) + (r - vis_before));
+    return a.table + (size_t)id * a.row_bytes;
+  }
+  // Page walk: visual row -> page GVA -> page-table entry -> physical row.
+  const int lp = vis_idx / a.page_tokens;
+  const int off = vis_idx - lp * a.page_tokens;
+  const uint64_t gva = ld_global(reinterpret_cast<const uint64_t*>(a.meta + sp.page_off) + lp);
+  const uint64_t pte = ld_global(a.pte + (gva - a.gva_start) / a.page_bytes);
+  if (!(a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))) return nullptr;
+  return reinterpret_cast<const uint8_t*>(pte & PTE_ADDR_MASK) + (size_t)off * a.row_bytes;
+}
+
+// One workgroup packs one chunk of kChunkVecs 16-byte vectors of the output
+// (rows are contiguous in the output, so a chunk is a contiguous byte range
+// that may start and end inside rows): it stages the microbatch's sample
+// headers in LDS, computes the prefix sum of their lengths, resolves the
+// source of every row the chunk touches, then moves kVecsPerThread vectors
+// per thread with all loads in flight before the stores.
+__global__ __launch_bounds__(kBlock) void k_pack(PackArgs a) {
+  extern __shared__ __align__(16) uint8_t s_dyn[];
+  __shared__ int32_t s_wsum[kBlock / 64];
+  __shared__ int32_t s_skip;                        // some row of the chunk is not copied
+  PackSample* s_smp = reinterpret_cast<PackSample*>(s_dyn);
+  int2* s_img = reinterpret_cast<int2*>(s_smp + a.n);
+  uint64_t* s_src = reinterpret_cast<uint64_t*>(s_img + a.n_imgs);
+  int32_t* s_cu = reinterpret_cast<int32_t*>(s_src + a.max_chunk_rows);
+  const int tid = threadIdx.x;
+
+  if (tid == 0) s_skip = 0;
+  const PackSample* gs = a.samples_dev ? a.samples_dev : a.samples;
+  const int2* gi = a.imgs_dev ? a.imgs_dev : a.imgs;
+  for (int i = tid; i < a.n; i += kBlock) s_smp[i] = ld_sample(gs + i);
+  for (int i = tid; i < a.n_imgs; i += kBlock) s_img[i] = ld_pair(gi + i);
+  __syncthreads();
+  block_scan_lengths(s_smp, a.n, s_cu, s_wsum);
 
   const bool write_meta = (a.tier_mask & 1) != 0;
   if (blockIdx.x == 0 && a.cu && write_meta) {
-    for (int i = tid; i <= n; i += kBlock) a.cu[i] = s_cu[i];
+    for (int i = tid; i <= a.n; i += kBlock) a.cu[i] = s_cu[i];
   }
 
-  const int row0 = blockIdx.x * a.tile_rows;
-  const int rows = min(a.tile_rows, a.n_tokens - row0);
-
-  // Resolve each row of the tile to its source address (one thread per row).
-  if (tid < rows) {
-    const int row = row0 + tid;
-    int lo = 0, hi = n - 1;                          // last k with cu[k] <= row
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_cu[mid] <= row) lo = mid; else hi = mid - 1;
-    }
-    const int r = row - s_cu[lo];
-    const SampleDesc d = a.desc[slot_at(a, lo)];
-    // Image j starts after img_pos[j] text rows and all earlier images' rows.
-    const int2* img = reinterpret_cast<const int2*>(a.meta + d.img_off);
-    int vis_before = 0;
-    int vis_idx = -1;
-    for (int j = 0; j < d.n_img; ++j) {
-      const int2 pr = img[j];
-      const int start = pr.x + vis_before;
-      if (r < start) break;
-      if (r < start + pr.y) { vis_idx = vis_before + (r - start); break; }
-      vis_before += pr.y;
-    }
-    const uint8_t* src = nullptr;
-    if (vis_idx < 0) {
-      if (write_meta) {
-        const int32_t id = reinterpret_cast<const int32_t*>(a.meta + d.text_off)[r - vis_before];
-        src = a.table + (size_t)id * a.row_bytes;
-      }
-    } else {
-      const int lp = vis_idx / a.page_tokens;
-      const int off = vis_idx - lp * a.page_tokens;
-      const uint64_t gva = reinterpret_cast<const uint64_t*>(a.meta + d.page_off)[lp];
-      const uint64_t pte = a.pte[(gva - a.gva_start) / a.page_bytes];
-      const int want = (pte & PTE_HOST) ? 2 : 1;
-      if (a.tier_mask & want)
-        src = reinterpret_cast<const uint8_t*>(pte & PTE_ADDR_MASK) + (size_t)off * a.row_bytes;
-    }
-    s_src[tid] = src;
-    if (a.pos && write_meta) a.pos[row] = r;
+  const int vpr = a.row_bytes >> 4;
+  const int total = a.n_tokens * vpr;                 // the host keeps this below 2^31
+  const int v0 = blockIdx.x * kChunkVecs;
+  const int v1 = min(v0 + kChunkVecs, total);
+  const int r0 = v0 / vpr;
+  const int rows = v1 > v0 ? (v1 - 1) / vpr - r0 + 1 : 0;
+  for (int t = tid; t < rows; t += kBlock) {
+    const int row = r0 + t;
+    const int k = sample_of(s_cu, a.n, row);
+    const int r = row - s_cu[k];
+    const uint8_t* src = resolve_row(a, s_smp[k], s_img, r);
+    s_src[t] = reinterpret_cast<uint64_t>(src);
+    if (!src) s_skip = 1;
+    if (a.pos && write_meta && row * vpr >= v0) a.pos[row] = r;
   }
   __syncthreads();
 
-  copy_tile<U>(s_src, a.out + (size_t)row0 * a.row_bytes, rows, a.row_bytes);
+  // Vector e of the chunk belongs to row e / vpr (multiply-shift division).
+  // A vector is live if it lies in the chunk and its row is copied; only
+  // live vectors get an address, dead ones are never loaded or stored.
+  uint64_t from[kVecsPerThread];
+  bool live[kVecsPerThread];
+#pragma unroll
+  for (int u = 0; u < kVecsPerThread; ++u) {
+    const int e = v0 + u * kBlock + tid;
+    from[u] = 0;
+    live[u] = false;
+    if (e < v1) {
+      const int row = (int)(((uint64_t)(uint32_t)e * a.div_mul) >> a.div_shift);
+      const uint64_t base = s_src[row - r0];
+      live[u] = base != 0;
+      from[u] = live[u] ? base + (uint64_t)(e - row * vpr) * 16 : 0;
+    }
+  }
+  u32x4 v[kVecsPerThread];
+  if (v1 - v0 == kChunkVecs && !s_skip) {
+    // Whole chunk, every row copied: no predication, so the compiler can keep
+    // all loads in flight and wait for them one at a time before each store.
+#pragma unroll
+    for (int u = 0; u < kVecsPerThread; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
+#pragma unroll
+    for (int u = 0; u < kVecsPerThread; ++u)
+      store16(a.out + (size_t)(v0 + u * kBlock + tid) * 16, v[u]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < kVecsPerThread; ++u)
+      if (live[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
+#pragma unroll
+    for (int u = 0; u < kVecsPerThread; ++u)
+      if (live[u]) store16(a.out + (size_t)(v0 + u * kBlock + tid) * 16, v[u]);
+  }
 }
 
 template <int U>
@@ -198,10 +251,15 @@ __global__ __launch_bounds__(kBlock) void k_cost(const SampleDesc* __restrict__ 
 
 constexpr int kUnroll = 8;
 
+size_t pack_lds_bytes(const PackArgs& a) {
+  return sizeof(PackSample) * (size_t)a.n + sizeof(int2) * (size_t)a.n_imgs +
+         sizeof(void*) * (size_t)a.max_chunk_rows + sizeof(int32_t) * (size_t)(a.n + 1);
+}
+
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
-  const int grid = a.n_tokens > 0 ? (a.n_tokens + a.tile_rows - 1) / a.tile_rows : 1;
-  const size_t lds = sizeof(int32_t) * (size_t)(a.n + 1);
-  hipLaunchKernelGGL(k_pack<kUnroll>, dim3(grid), dim3(kBlock), lds, stream, a);
+  const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
+  const int grid = vecs > 0 ? (int)((vecs + kChunkVecs - 1) / kChunkVecs) : 1;
+  hipLaunchKernelGGL(k_pack, dim3(grid), dim3(kBlock), pack_lds_bytes(a), stream, a);
   return hipGetLastError();
 }
 

@@ -113,7 +113,9 @@ struct SampleRec {
   int32_t slot;
   int32_t len, n_text, n_img, n_vis;
   int64_t meta_off, meta_len;
+  int64_t text_off, page_off;    // metadata-arena offsets of text ids and page GVAs
   std::vector<uint64_t> pages;   // GVAs in visual-row order
+  std::vector<int32_t> img;      // (placeholder position, rows) per image
 };
 
 uint64_t splitmix64(uint64_t& s) {
@@ -558,6 +560,13 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   rec.n_vis = (int32_t)n_vis;
   rec.meta_off = meta_off;
   rec.meta_len = meta_len;
+  rec.text_off = d.text_off;
+  rec.page_off = d.page_off;
+  rec.img.resize(2 * (size_t)n_img);
+  for (int32_t j = 0; j < n_img; ++j) {
+    rec.img[2 * (size_t)j] = img_pos[j];
+    rec.img[2 * (size_t)j + 1] = img_ntok[j];
+  }
   const uint64_t id = p->next_id++;
   p->samples.emplace(id, std::move(rec));
   *out_sample_id = id;
@@ -644,25 +653,24 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
   if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
   if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
-  fp::PackArgs a{};
-  std::vector<int32_t> big_slots;
-  int32_t* slots = a.slots_inline;
-  if (n > fp::kInlineSlots) {
-    big_slots.resize((size_t)n);
-    slots = big_slots.data();
-  }
-  int64_t total = 0, n_text = 0;
+  std::vector<const SampleRec*> recs((size_t)n);
+  int64_t total = 0, n_text = 0, n_imgs = 0;
   int32_t mx = 0;
   for (int32_t i = 0; i < n; ++i) {
     auto it = p->samples.find(sample_ids[i]);
     if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-    slots[i] = it->second.slot;
-    total += it->second.len;
-    n_text += it->second.n_text;
-    mx = std::max(mx, it->second.len);
+    const SampleRec& r = it->second;
+    recs[(size_t)i] = &r;
+    total += r.len;
+    n_text += r.n_text;
+    n_imgs += r.n_img;
+    mx = std::max(mx, r.len);
   }
+  if (n_imgs > fp::kMaxPackImages)
+    return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
   if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
-  if (total > 0x7fffffffll) return fail(FP_EINVAL, "microbatch too large");
+  const int64_t vpr = p->rb / 16;
+  if (total * vpr > 0x7fffffffll) return fail(FP_EINVAL, "microbatch of %lld rows is too large", (long long)total);
   if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
   if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
     if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
@@ -671,7 +679,7 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   DeviceGuard guard(p->cfg.device);
   if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
   hipStream_t hs = (hipStream_t)stream;
-  a.desc = p->desc_dev;
+  fp::PackArgs a{};
   a.meta = p->meta_dev;
   a.pte = p->pte_dev;
   a.gva_start = p->gva_start;
@@ -681,18 +689,46 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   a.cu = out_cu_seqlens;
   a.pos = out_position_ids;
   a.n = n;
+  a.n_imgs = (int32_t)n_imgs;
   a.n_tokens = (int32_t)total;
   a.row_bytes = (int32_t)p->rb;
   a.page_tokens = p->cfg.page_tokens;
   a.tier_mask = tier_mask;
-  a.tile_rows = p->tile_rows;
+  a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
+  // Division of a vector index e < 2^31 by vpr as a multiply and a shift:
+  // with s = 31 + ceil(log2 vpr) and m = ceil(2^s / vpr), e / vpr == (e * m) >> s.
+  int ceil_log2 = 0;
+  while ((1ll << ceil_log2) < vpr) ++ceil_log2;
+  a.div_shift = 31 + ceil_log2;
+  a.div_mul = (uint64_t)(((1ull << a.div_shift) + (uint64_t)vpr - 1) / (uint64_t)vpr);
+  const bool staged = n > fp::kInlineSamples || n_imgs > fp::kInlineImages;
+  std::vector<fp::PackSample> big_s;
+  std::vector<int2> big_i;
+  fp::PackSample* smp = a.samples;
+  int2* img = a.imgs;
+  if (staged) {
+    big_s.resize((size_t)n);
+    big_i.resize((size_t)n_imgs);
+    smp = big_s.data();
+    img = big_i.data();
+  }
+  int32_t base = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const SampleRec& r = *recs[(size_t)i];
+    smp[i] = fp::PackSample{r.len, r.n_img, base, r.n_text, r.text_off, r.page_off};
+    for (int32_t j = 0; j < r.n_img; ++j) img[base + j] = int2{r.img[2 * (size_t)j], r.img[2 * (size_t)j + 1]};
+    base += r.n_img;
+  }
   Stage* s = nullptr;
-  if (n > fp::kInlineSlots) {
-    fp_status st = stage_acquire(p, 4 * (size_t)n, 4 * (size_t)n, &s);
+  if (staged) {
+    const size_t sb = sizeof(fp::PackSample) * (size_t)n, ib = sizeof(int2) * (size_t)n_imgs;
+    fp_status st = stage_acquire(p, sb + ib, sb + ib, &s);
     if (st != FP_OK) return st;
-    std::memcpy(s->host, slots, 4 * (size_t)n);
-    FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
-    a.slots_dev = (const int32_t*)s->dev;
+    std::memcpy(s->host, smp, sb);
+    if (ib) std::memcpy(s->host + sb, img, ib);
+    FP_HIP(hipMemcpyAsync(s->dev, s->host, sb + ib, hipMemcpyHostToDevice, hs));
+    a.samples_dev = (const fp::PackSample*)s->dev;
+    a.imgs_dev = (const int2*)(s->dev + sb);
   }
   hipError_t e = fp::launch_pack(a, hs);
   if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));

@@ -1,0 +1,113 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times (same pool, same pack entry point, a non-default stream,
+rotating output buffers).
+
+The oracle cannot materialise every byte here, so each microbatch is checked
+by properties that hold at any size plus sampled rows:
+- the plan (assignment, tokens, cost per microbatch) equals the oracle's;
+- every sample's page GVAs equal the oracle pool's (same churn history);
+- cu_seqlens and position ids equal the oracle's, in full;
+- the tag words of EVERY packed row name exactly the source the oracle's
+  layout gives (sample, visual index or text id);
+- sampled rows (first, last, and random ones) equal, in all H words, the
+  input row the oracle names for them.
+"""
+
+import numpy as np
+import pytest
+
+from gpu_common import oracle_plan, oracle_pool_for, say, to_host
+from oracle.pack import row_sources
+from paper_2606_23087_amd.workloads import CONFIGS, TAG_TEXT, TAG_VIS
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def fp():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_23087_amd import flowpool
+    return flowpool
+
+
+def _expected_tags(idx, specs_mb):
+    src = row_sources(specs_mb)
+    tags = np.zeros((len(src), 4), np.uint16)
+    pos = np.zeros(len(src), np.int32)
+    last, count = -1, 0
+    for r, (kind, s, x) in enumerate(src):
+        count = count + 1 if s == last else 0
+        last = s
+        pos[r] = count
+        if kind == "text":
+            tags[r] = (TAG_TEXT, x & 0xFFFF, x >> 16, 0)
+        else:
+            g = idx[s]
+            tags[r] = (TAG_VIS, g & 0xFFFF, g >> 16, x & 0xFFFF)
+    return src, tags, pos
+
+
+@pytest.mark.parametrize("name", ["qwen", "frag70b", "video", "tiered"])
+def test_full_size(fp, name):
+    from paper_2606_23087_amd.harness import GpuWorkload, vis_rows
+    cfg = CONFIGS[name]
+    seed = 0
+    say(f"full-size {name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}")
+    w = GpuWorkload(cfg, seed, mode="tagged", log=say)
+    try:
+        say(f"  {len(w.ids)} samples written; replaying in the oracle pool")
+        opool, oids = oracle_pool_for(cfg, seed, w.specs, None, with_bytes=False)
+        for gid, oid in zip(w.ids, oids):
+            assert fp.pool_sample_pages(w.pool, gid).tolist() == opool.sample_pages(oid)
+        plan = w.plan()
+        assign, tok, cst, mem = oracle_plan(cfg, w.specs)
+        assert plan["assign"].tolist() == assign
+        assert plan["mb_tokens"].tolist() == tok and plan["mb_cost_scaled"].tolist() == cst
+        mbs = w.microbatches(plan)
+        assert mbs == [[w.ids[i] for i in m] for m in mem]
+        stream = torch.cuda.Stream()
+        outs = [w.alloc_outputs() for _ in range(4)]
+        rng = np.random.default_rng(11)
+        host_table = None
+        for j, idx in enumerate(mem):
+            out, cu, pos = outs[j % 4]
+            n, mx = w.pack([w.ids[i] for i in idx], out, cu, pos, stream=stream)
+            stream.synchronize()
+            specs_mb = [w.specs[i] for i in idx]
+            src, tags, pos_want = _expected_tags(idx, specs_mb)
+            lens = [s.length for s in specs_mb]
+            assert n == len(src) == sum(lens) and mx == max(lens)
+            assert cu[:len(idx) + 1].cpu().numpy().tolist() == [0] + np.cumsum(lens).tolist()
+            assert np.array_equal(pos[:n].cpu().numpy(), pos_want)
+            got_tags = to_host(out[:n, :4])
+            bad = np.nonzero(np.any(got_tags != tags, axis=1))[0]
+            assert bad.size == 0, f"microbatch {j}: {bad.size} rows with wrong source, first {bad[:5]}"
+            picks = sorted(set([0, n - 1] + rng.integers(0, n, size=24).tolist()))
+            vis_cache = {}
+            for r in picks:
+                kind, s, x = src[r]
+                if kind == "text":
+                    want = to_host(w.table[x])
+                else:
+                    g = idx[s]
+                    if g not in vis_cache:
+                        vis_cache[g] = vis_rows(cfg, seed, g, w.specs[g].n_vis, "tagged")
+                    want = to_host(vis_cache[g][x])
+                assert np.array_equal(to_host(out[r]), want), f"microbatch {j} row {r} ({kind})"
+        say(f"  {len(mem)} microbatches checked")
+        if cfg.host_pages:
+            say("  tier-mask split at full size")
+            full, cu, pos = w.alloc_outputs(fill=0)
+            part, cu2, pos2 = w.alloc_outputs(fill=0x2222)
+            for g in mbs[:4]:
+                n, _ = w.pack(g, full, cu, pos, stream=stream)
+                w.pack(g, part, cu2, pos2, tier_mask=fp.FP_TIER_MASK_HBM, stream=stream)
+                w.pack(g, part, None, None, tier_mask=fp.FP_TIER_MASK_HOST, stream=stream)
+                stream.synchronize()
+                assert torch.equal(part[:n], full[:n]) and torch.equal(cu, cu2) and torch.equal(pos, pos2)
+    finally:
+        w.close()
+        torch.cuda.empty_cache()
