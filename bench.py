@@ -54,8 +54,14 @@ def pack_bytes(cfg, specs) -> int:
 
 
 def kernel_source_hash() -> str:
+    """Hash of the kernel source with comments and whitespace removed, so that
+    only a change to the code itself invalidates recorded counters."""
     path = os.path.join(ROOT, "paper_2606_23087_amd", "csrc", "kernels.hip")
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = re.sub(r"\s+", "", src)
+    return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
 def counter_traffic(workload: str):
@@ -111,6 +117,60 @@ def cpu_baseline(cfg, w, mbs, seed: int, budget_s: float):
                        f"by the single-threaded numpy pool oracle",
                 cpu_model=platform.processor() or platform.machine(),
                 os_cpu_count=os.cpu_count(), affinity=len(os.sched_getaffinity(0)))
+
+
+def host_tier_rows(cfg, w, sid, spec) -> int:
+    """Visual rows of a sample that sit on host-tier pages (from the pool's page table)."""
+    from paper_2606_23087_amd import flowpool as fp
+    rows = 0
+    for i, gva in enumerate(fp.pool_sample_pages(w.pool, sid).tolist()):
+        tier, _ = fp.pool_translate(w.pool, int(gva))
+        if tier == fp.FP_TIER_HOST:
+            rows += min(cfg.page_tokens, spec.n_vis - i * cfg.page_tokens)
+    return rows
+
+
+def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
+    """Tiered pool: time the HBM-tier part (text rows + rows on HBM pages) and
+    the host-tier part (rows on pinned host pages, read over PCIe) as separate
+    masked launches, and both masks concurrently on two streams."""
+    import torch
+    from paper_2606_23087_amd import flowpool as fp
+    host_rows = [sum(host_tier_rows(cfg, w, s, spec_of[s]) for s in mb) for mb in mbs]
+    tot_rows = [sum(spec_of[s].length for s in mb) for mb in mbs]
+    rb = cfg.row_bytes
+    second = torch.cuda.Stream()
+
+    def timed(masks_streams):
+        ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(reps):
+            for j, mb in enumerate(mbs):
+                out, cu, pos = outs[j % len(outs)]
+                for mask, st in masks_streams:
+                    if st is not stream:
+                        st.wait_stream(stream)
+                    w.pack(mb, out, cu if mask & 1 else None, pos if mask & 1 else None, tier_mask=mask, stream=st)
+                    if st is not stream:
+                        stream.wait_stream(st)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) * 1e-3 / reps
+
+    t_hbm = timed([(fp.FP_TIER_MASK_HBM, stream)])
+    t_host = timed([(fp.FP_TIER_MASK_HOST, stream)])
+    t_both = timed([(fp.FP_TIER_MASK_HBM, stream), (fp.FP_TIER_MASK_HOST, second)])
+    t_all = timed([(fp.FP_TIER_MASK_ALL, stream)])
+    hbm_bytes = 2 * (sum(tot_rows) - sum(host_rows)) * rb
+    pcie_bytes = sum(host_rows) * rb
+    return {"host_tier_row_fraction": round(sum(host_rows) / sum(tot_rows), 4),
+            "hbm_tier": {"GBps": round(hbm_bytes / t_hbm / 1e9, 1), "peak": HBM_PEAK_GBPS,
+                         "bytes": hbm_bytes, "ms": round(t_hbm * 1e3, 3)},
+            "host_tier": {"GBps": round(pcie_bytes / t_host / 1e9, 2), "peak": PCIE_PEAK_GBPS,
+                          "bytes_over_pcie": pcie_bytes, "ms": round(t_host * 1e3, 3)},
+            "both_masks_two_streams_ms": round(t_both * 1e3, 3),
+            "one_full_pack_ms": round(t_all * 1e3, 3)}
 
 
 def d2d_ceiling(nbytes: int = 1 << 30, iters: int = 10) -> float:
@@ -241,6 +301,8 @@ def main() -> int:
         "step_bytes": step_bytes,
         "deferred_samples": deferred,
         "pack_kernel": {"launches": int(durs.size), "mean_us": round(float(durs.mean()) * 1e6, 3),
+                        "call_us_p10_p50_p90_max": [round(float(np.percentile(durs, q)) * 1e6, 2) for q in (10, 50, 90, 100)],
+                        "slowest_call_mb_index": int(np.unravel_index(np.argmax(durs), durs.shape)[1]),
                         "median_call_GBps": round(float(np.median(per_call)), 2),
                         "aggregate_GBps": round(kernel_gbps, 2)},
         "roofline": {"bound": "hbm", "achieved": round(kernel_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -252,6 +314,8 @@ def main() -> int:
     result["plan"] = {"max_over_mean_cost": round(float(imb), 5),
                       "eq3_max": round(float(max((t / cfg.capacity) + (m / cfg.capacity) ** 2
                                                  for t, m in zip(plan["mb_tokens"], plan["mb_max_len"]))), 5)}
+    if cfg.host_pages:
+        result["tiers"] = tier_split(cfg, w, mbs, spec_of, outs, pack_stream)
     result["d2d_copy_ceiling_GBps"] = round(d2d_ceiling(), 1)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")

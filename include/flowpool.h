@@ -4,14 +4,13 @@
  *
  * Producers (frozen vision encoders) write each sample's vision embeddings
  * into pages of the pool, together with the sample's text token ids and the
- * metadata that pairs them (paper Sec. 3.1 workflow, Sec. 3.2 "write"). A
- * planner groups resident samples into cost-balanced microbatches (Sec. 3.4,
- * Eq. 3). The backbone consumes a microbatch by sample id: the library
- * resolves every visual row's GVA through the page table, gathers the page
- * rows and the text-embedding-table rows and packs them into one varlen
- * microbatch with cu_seqlens and position ids (Sec. 3.1 "consumes
- * microbatches based on the GVA", Sec. 3.2 translation through local page
- * tables).
+ * metadata that pairs them (paper Sec. 3.1 workflow; Sec. 3.2, producer
+ * side). A planner groups resident samples into cost-balanced microbatches
+ * (Sec. 3.4, Eq. 3). The backbone consumes a microbatch by sample id: the
+ * library resolves every visual row's GVA through the page table, gathers the
+ * page rows and the text-embedding-table rows and packs them into one varlen
+ * microbatch with cu_seqlens and position ids (Sec. 3.1: consumers address
+ * data by GVA only; Sec. 3.2: translation through locally held page tables).
  *
  * Conventions for every entry point:
  *  - Return value: FP_OK (0) or a negative FP_E* status. Nothing throws or
@@ -126,8 +125,8 @@ fp_status pool_create(const fp_pool_config* cfg, fp_pool** out);
  * every stream that still uses it. NULL is accepted. */
 fp_status pool_destroy(fp_pool* p);
 
-/* Producer write (Sec. 3.2 "vision embeddings and text tokens are written
- * into the GVA segment of their own process"; Sec. 3.1 pairing metadata).
+/* Producer write (Sec. 3.2: each producer writes vision embeddings and text
+ * tokens into its own process's GVA segment; Sec. 3.1 pairing metadata).
  *  text_ids        host int32[n_text], each in [0, vocab).
  *  img_pos         host int32[n_img], nondecreasing, each in [0, n_text]: image
  *                  j is placed before text token img_pos[j] (after all text

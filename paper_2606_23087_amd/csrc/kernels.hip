@@ -7,8 +7,8 @@
 //           vector copies of every row from its page or embedding-table row
 //           into the packed output, plus position ids.
 // k_write : the producer's write of one sample's image rows into its pages,
-//           through the same page table (Sec. 3.2 "write into the GVA
-//           segment"), and publication of the sample descriptor.
+//           through the same page table (Sec. 3.2, producer side), and
+//           publication of the sample descriptor.
 // k_cost  : per-sample cost K*l + l^2 for the planner (Sec. 3.4).
 //
 // Nothing here is a dense contraction, so there is no MFMA: the pack is a
