@@ -22,6 +22,7 @@ Algorithmic bytes of one pack (each valid row read once and written once):
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -54,10 +55,12 @@ def pack_bytes(cfg, specs) -> int:
 
 
 def kernel_source_hash() -> str:
-    """Hash of the kernel source with comments and whitespace removed, so that
-    only a change to the code itself invalidates recorded counters."""
-    path = os.path.join(ROOT, "paper_2606_23087_amd", "csrc", "kernels.hip")
-    src = open(path).read()
+    """Hash of the kernel sources (kernels.hip and the launch-layout header
+    fp_internal.h) with comments and whitespace removed, so that only a change
+    to the code itself invalidates recorded counters."""
+    src = ""
+    for name in ("kernels.hip", "fp_internal.h"):
+        src += open(os.path.join(ROOT, "paper_2606_23087_amd", "csrc", name)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     src = re.sub(r"//[^\n]*", "", src)
     src = re.sub(r"\s+", "", src)
@@ -265,11 +268,14 @@ def main() -> int:
     events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(n_packs)] for _ in range(args.steps)]
     torch.cuda.synchronize()
+    gc.collect()
+    gc.disable()          # no collector pauses between enqueues inside the timed region
     t0 = time.perf_counter()
     for k in range(args.steps):
         one_step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gc.enable()
     durs = np.array([[s.elapsed_time(e) * 1e-3 for s, e in ev] for ev in events])   # seconds
     mb_bytes = np.array([pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs], dtype=np.float64)
 

@@ -33,8 +33,9 @@ constexpr uint64_t PTE_ADDR_MASK = ~0xFull;
 
 constexpr int kBlock = 256;          // threads per workgroup for all kernels
 constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
-constexpr int kVecsPerThread = 8;    // 16-byte vectors each k_pack thread moves
-constexpr int kChunkVecs = kBlock * kVecsPerThread;   // output vectors per k_pack workgroup (32 KiB)
+constexpr int kPackBlock = 256;      // threads per k_pack workgroup
+constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves (12 KiB chunks)
+constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
 constexpr int kInlineSamples = 64;   // sample headers passed by value to k_pack
 constexpr int kInlineImages = 128;   // image pairs passed by value to k_pack
 constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds k_pack's LDS use)

@@ -61,7 +61,7 @@ __device__ __forceinline__ void block_scan_lengths(const PackSample* smp, int n,
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) cu[0] = 0;
   int carry = 0;
-  for (int base = 0; base < n; base += kBlock) {
+  for (int base = 0; base < n; base += kPackBlock) {
     const int i = base + tid;
     int v = (i < n) ? smp[i].len : 0;
 #pragma unroll
@@ -73,7 +73,7 @@ __device__ __forceinline__ void block_scan_lengths(const PackSample* smp, int n,
     __syncthreads();
     int before = 0, all = 0;
 #pragma unroll
-    for (int w = 0; w < kBlock / 64; ++w) {
+    for (int w = 0; w < kPackBlock / 64; ++w) {
       before += (w < wave) ? wsum[w] : 0;
       all += wsum[w];
     }
@@ -126,45 +126,199 @@ __device__ __forceinline__ const uint8_t* resolve_row(const PackArgs& a, const P
 // headers in LDS, computes the prefix sum of their lengths, resolves the
 // source of every row the chunk touches, then moves kVecsPerThread vectors
 // per thread with all loads in flight before the stores.
-__global__ __launch_bounds__(kBlock) void k_pack(PackArgs a) {
+// Page walk or text lookup of row r of a sample whose segment is already
+// known: vis_idx >= 0 is the row's index among the sample's visual rows,
+// otherwise text_idx is its index among the sample's text tokens.
+__device__ __forceinline__ const uint8_t* row_source(const PackArgs& a, int64_t text_off,
+                                                     int64_t page_off, int vis_idx, int text_idx) {
+  if (vis_idx < 0) {
+    if (!(a.tier_mask & 1)) return nullptr;
+    const int32_t id = ld_global(reinterpret_cast<const int32_t*>(a.meta + text_off) + text_idx);
+    return a.table + (size_t)id * a.row_bytes;
+  }
+  const int lp = vis_idx / a.page_tokens;
+  const int off = vis_idx - lp * a.page_tokens;
+  const uint64_t gva = ld_global(reinterpret_cast<const uint64_t*>(a.meta + page_off) + lp);
+  const uint64_t pte = ld_global(a.pte + (gva - a.gva_start) / a.page_bytes);
+  if (!(a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))) return nullptr;
+  return reinterpret_cast<const uint8_t*>(pte & PTE_ADDR_MASK) + (size_t)off * a.row_bytes;
+}
+
+// Reads through constant-address-space views of uniform addresses compile to
+// scalar loads (scalar cache), which do not queue behind the vector memory
+// traffic of the copies.
+typedef __attribute__((address_space(4))) const int32_t k_i32;
+typedef __attribute__((address_space(4))) const int64_t k_i64;
+typedef __attribute__((address_space(4))) const uint64_t k_u64;
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), lane);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ PackSample ld_sample_scalar(const PackSample* p) {
+  const k_i32* q = (const k_i32*)p;
+  PackSample s;
+  s.len = q[0];
+  s.n_img = q[1];
+  s.img_base = q[2];
+  s.n_text = q[3];
+  s.text_off = *(const k_i64*)(q + 4);
+  s.page_off = *(const k_i64*)(q + 6);
+  return s;
+}
+
+__device__ __forceinline__ int2 ld_pair_scalar(const int2* p) {
+  const k_i32* q = (const k_i32*)p;
+  int2 r;
+  r.x = q[0];
+  r.y = q[1];
+  return r;
+}
+
+// One workgroup packs one chunk of kChunkVecs 16-byte vectors of the output
+// (rows are contiguous in the output, so a chunk is a contiguous byte range
+// that may start and end inside rows): it finds, for every row the chunk
+// touches, the row's sample (prefix sum of sample lengths) and segment, walks
+// the page table for image rows, and then moves kVecsPerThread vectors per
+// thread with all loads in flight before the stores.
+//
+// Headers passed by value and at most kPackBlock rows per chunk (the usual case):
+// the headers are read with scalar loads in one workgroup-uniform loop that
+// also keeps the running prefix sum, so the only vector loads before the copy
+// are the page walk and the text ids. Otherwise the headers are staged in LDS
+// and scanned there.
+__global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   extern __shared__ __align__(16) uint8_t s_dyn[];
-  __shared__ int32_t s_wsum[kBlock / 64];
-  __shared__ int32_t s_skip;                        // some row of the chunk is not copied
+  __shared__ int32_t s_wsum[kPackBlock / 64];
   PackSample* s_smp = reinterpret_cast<PackSample*>(s_dyn);
   int2* s_img = reinterpret_cast<int2*>(s_smp + a.n);
   uint64_t* s_src = reinterpret_cast<uint64_t*>(s_img + a.n_imgs);
   int32_t* s_cu = reinterpret_cast<int32_t*>(s_src + a.max_chunk_rows);
   const int tid = threadIdx.x;
-
-  if (tid == 0) s_skip = 0;
-  const PackSample* gs = a.samples_dev ? a.samples_dev : a.samples;
-  const int2* gi = a.imgs_dev ? a.imgs_dev : a.imgs;
-  for (int i = tid; i < a.n; i += kBlock) s_smp[i] = ld_sample(gs + i);
-  for (int i = tid; i < a.n_imgs; i += kBlock) s_img[i] = ld_pair(gi + i);
-  __syncthreads();
-  block_scan_lengths(s_smp, a.n, s_cu, s_wsum);
+  int my_skip = 0;                                  // a row of this chunk is not copied
 
   const bool write_meta = (a.tier_mask & 1) != 0;
-  if (blockIdx.x == 0 && a.cu && write_meta) {
-    for (int i = tid; i <= a.n; i += kBlock) a.cu[i] = s_cu[i];
-  }
-
+  const bool write_cu = blockIdx.x == 0 && a.cu && write_meta;
   const int vpr = a.row_bytes >> 4;
   const int total = a.n_tokens * vpr;                 // the host keeps this below 2^31
+  const int n_chunks = (total + kChunkVecs - 1) / kChunkVecs;
   const int v0 = blockIdx.x * kChunkVecs;
   const int v1 = min(v0 + kChunkVecs, total);
   const int r0 = v0 / vpr;
   const int rows = v1 > v0 ? (v1 - 1) / vpr - r0 + 1 : 0;
-  for (int t = tid; t < rows; t += kBlock) {
-    const int row = r0 + t;
-    const int k = sample_of(s_cu, a.n, row);
-    const int r = row - s_cu[k];
-    const uint8_t* src = resolve_row(a, s_smp[k], s_img, r);
-    s_src[t] = reinterpret_cast<uint64_t>(src);
-    if (!src) s_skip = 1;
-    if (a.pos && write_meta && row * vpr >= v0) a.pos[row] = r;
+
+  if (!a.samples_dev && rows <= kPackBlock) {
+    const bool own = tid < rows;
+    const bool has_row = own;
+    const int row = r0 + tid;
+    const int owner_v0 = v0;
+    int64_t text_off = 0, page_off = 0;
+    int vis_idx = -1, text_idx = 0, r_in = 0;
+    const int last_row = r0 + rows - 1;
+    int start = 0;                                   // first row of sample i (uniform)
+    for (int i = 0; i < a.n; ++i) {
+      const PackSample sp = ld_sample_scalar(a.samples + i);
+      if (write_cu && tid == 0) a.cu[i] = start;
+      const bool mine = has_row && row >= start && row < start + sp.len;
+      if (__any(mine)) {
+        // Image j starts after pr.x of the sample's text rows and all rows of
+        // the images before it; text rows fill the gaps.
+        const int r = row - start;
+        int vis_before = 0, vidx = -1;
+        bool found = false;
+        for (int j = 0; j < sp.n_img; ++j) {
+          const int2 pr = ld_pair_scalar(a.imgs + sp.img_base + j);
+          if (!found) {
+            const int s0 = pr.x + vis_before;
+            if (r < s0) {
+              found = true;
+            } else if (r < s0 + pr.y) {
+              vidx = vis_before + (r - s0);
+              found = true;
+            } else {
+              vis_before += pr.y;
+            }
+          }
+        }
+        if (mine) {
+          r_in = r;
+          vis_idx = vidx;
+          text_idx = r - vis_before;
+          text_off = sp.text_off;
+          page_off = sp.page_off;
+        }
+      }
+      start += sp.len;
+      if (!write_cu && start > last_row) break;
+    }
+    if (write_cu && tid == 0) a.cu[a.n] = start;
+    if (rows <= 64) {
+      // Wave 0 walks the rows one after another with scalar loads; rows on
+      // the same page reuse the previous translation.
+      if (tid < 64) {
+        uint64_t my_src = 0;
+        int64_t prev_page = -1;
+        uint64_t prev_base = 0;
+        for (int t = 0; t < rows; ++t) {
+          const int vis = __builtin_amdgcn_readlane(vis_idx, t);
+          uint64_t src = 0;
+          if (vis < 0) {
+            if (a.tier_mask & 1) {
+              const int tix = __builtin_amdgcn_readlane(text_idx, t);
+              const int64_t toff = readlane64(text_off, t);
+              const int32_t id = *(const k_i32*)(a.meta + toff + 4 * (int64_t)tix);
+              src = reinterpret_cast<uint64_t>(a.table) + (uint64_t)id * (uint64_t)a.row_bytes;
+            }
+          } else {
+            const int64_t poff = readlane64(page_off, t);
+            const int lp = vis / a.page_tokens;
+            const int off = vis - lp * a.page_tokens;
+            const int64_t page_key = poff + 8 * (int64_t)lp;   // position of the page's GVA
+            if (page_key != prev_page) {
+              const uint64_t gva = *(const k_u64*)(a.meta + page_key);
+              const uint64_t pte = *(const k_u64*)(a.pte + (gva - a.gva_start) / a.page_bytes);
+              prev_base = (a.tier_mask & ((pte & PTE_HOST) ? 2 : 1)) ? (pte & PTE_ADDR_MASK) : 0;
+              prev_page = page_key;
+            }
+            src = prev_base ? prev_base + (uint64_t)off * (uint64_t)a.row_bytes : 0;
+          }
+          if (tid == t) my_src = src;
+        }
+        if (has_row) {
+          s_src[tid] = my_src;
+          if (!my_src) my_skip = 1;
+          if (a.pos && write_meta && row * vpr >= owner_v0) a.pos[row] = r_in;
+        }
+      }
+    } else if (has_row) {
+      const uint8_t* src = row_source(a, text_off, page_off, vis_idx, text_idx);
+      s_src[tid] = reinterpret_cast<uint64_t>(src);
+      if (own && !src) my_skip = 1;
+      if (a.pos && write_meta && row * vpr >= owner_v0) a.pos[row] = r_in;
+    }
+  } else {
+    const PackSample* gs = a.samples_dev ? a.samples_dev : a.samples;
+    const int2* gi = a.imgs_dev ? a.imgs_dev : a.imgs;
+    for (int i = tid; i < a.n; i += kPackBlock) s_smp[i] = ld_sample(gs + i);
+    for (int i = tid; i < a.n_imgs; i += kPackBlock) s_img[i] = ld_pair(gi + i);
+    __syncthreads();
+    block_scan_lengths(s_smp, a.n, s_cu, s_wsum);
+    if (write_cu) {
+      for (int i = tid; i <= a.n; i += kPackBlock) a.cu[i] = s_cu[i];
+    }
+    for (int t = tid; t < rows; t += kPackBlock) {
+      const int row = r0 + t;
+      const int k = sample_of(s_cu, a.n, row);
+      const int r = row - s_cu[k];
+      const uint8_t* src = resolve_row(a, s_smp[k], s_img, r);
+      s_src[t] = reinterpret_cast<uint64_t>(src);
+      if (!src) my_skip = 1;
+      if (a.pos && write_meta && row * vpr >= v0) a.pos[row] = r;
+    }
   }
-  __syncthreads();
+  const bool skip = __syncthreads_or(my_skip);
 
   // Vector e of the chunk belongs to row e / vpr (multiply-shift division).
   // A vector is live if it lies in the chunk and its row is copied; only
@@ -173,7 +327,7 @@ __global__ __launch_bounds__(kBlock) void k_pack(PackArgs a) {
   bool live[kVecsPerThread];
 #pragma unroll
   for (int u = 0; u < kVecsPerThread; ++u) {
-    const int e = v0 + u * kBlock + tid;
+    const int e = v0 + u * kPackBlock + tid;
     from[u] = 0;
     live[u] = false;
     if (e < v1) {
@@ -184,21 +338,21 @@ __global__ __launch_bounds__(kBlock) void k_pack(PackArgs a) {
     }
   }
   u32x4 v[kVecsPerThread];
-  if (v1 - v0 == kChunkVecs && !s_skip) {
+  if (v1 - v0 == kChunkVecs && !skip) {
     // Whole chunk, every row copied: no predication, so the compiler can keep
     // all loads in flight and wait for them one at a time before each store.
 #pragma unroll
     for (int u = 0; u < kVecsPerThread; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
 #pragma unroll
     for (int u = 0; u < kVecsPerThread; ++u)
-      store16(a.out + (size_t)(v0 + u * kBlock + tid) * 16, v[u]);
+      store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
   } else {
 #pragma unroll
     for (int u = 0; u < kVecsPerThread; ++u)
       if (live[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
 #pragma unroll
     for (int u = 0; u < kVecsPerThread; ++u)
-      if (live[u]) store16(a.out + (size_t)(v0 + u * kBlock + tid) * 16, v[u]);
+      if (live[u]) store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
   }
 }
 
@@ -259,7 +413,7 @@ size_t pack_lds_bytes(const PackArgs& a) {
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
   const int grid = vecs > 0 ? (int)((vecs + kChunkVecs - 1) / kChunkVecs) : 1;
-  hipLaunchKernelGGL(k_pack, dim3(grid), dim3(kBlock), pack_lds_bytes(a), stream, a);
+  hipLaunchKernelGGL(k_pack, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
   return hipGetLastError();
 }
 
