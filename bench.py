@@ -8,9 +8,12 @@ page walk, visual-row gather, text-table gather, position ids).
 
 Prints ONE JSON line. ``value`` is the whole-step effective bandwidth:
 algorithmic bytes of all packs / wall time of the timed steps (inputs already
-resident in HBM). ``roofline`` is for the pack kernel alone: algorithmic
-bytes per launch / mean launch duration from HIP events recorded on the pack
-stream around every pack in the timed steps. ``cpu_baseline`` times the CPU
+resident in HBM, planning included). ``roofline`` is for the pack kernel:
+algorithmic bytes per launch / mean launch duration, the duration being one
+HIP event pair on the pack stream around all pack launches of the timed steps
+divided by their number (back-to-back launches, inter-kernel gaps included).
+Per-call event pairs are taken in a separate untimed step: recording events
+between launches perturbs the stream they time. ``cpu_baseline`` times the CPU
 oracle's pool pack on a bounded sample of the same microbatches.
 
 Algorithmic bytes of one pack (each valid row read once and written once):
@@ -240,18 +243,20 @@ def main() -> int:
     plan_stream = torch.cuda.Stream()
     outs = [w.alloc_outputs() for _ in range(max(1, args.buffers))]
 
-    def one_step(events=None):
+    region = {}
+
+    def one_step(events=None, mark_start=False):
         plan = w.plan(stream=plan_stream)
         mbs = w.microbatches(plan)
-        k = 0
         for j, mb in enumerate(mbs):
             out, cu, pos = outs[j % len(outs)]
+            if j == 0 and mark_start:
+                region["start"].record(pack_stream)
             if events is not None:
-                events[k][0].record(pack_stream)
+                events[j][0].record(pack_stream)
             w.pack(mb, out, cu, pos, stream=pack_stream)
             if events is not None:
-                events[k][1].record(pack_stream)
-            k += 1
+                events[j][1].record(pack_stream)
         return plan, mbs
 
     plan, mbs = one_step()
@@ -264,24 +269,37 @@ def main() -> int:
     log(f"warmup done: {len(mbs)} microbatches, {step_tokens} tokens, {step_bytes / 1e6:.1f} MB per step, "
         f"{deferred} samples deferred")
 
-    n_packs = sum(1 for _ in mbs)
-    events = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(n_packs)] for _ in range(args.steps)]
+    # Timed region: K whole steps back to back. One event pair on the pack
+    # stream brackets every pack launch of the region (from the first pack of
+    # the first step to the last pack of the last step); the wall clock
+    # brackets the whole region, planning included.
+    n_packs = len(mbs)
+    region["start"] = torch.cuda.Event(enable_timing=True)
+    region["end"] = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     gc.collect()
     gc.disable()          # no collector pauses between enqueues inside the timed region
     t0 = time.perf_counter()
     for k in range(args.steps):
-        one_step(events[k])
+        one_step(mark_start=(k == 0))
+    region["end"].record(pack_stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gc.enable()
-    durs = np.array([[s.elapsed_time(e) * 1e-3 for s, e in ev] for ev in events])   # seconds
     mb_bytes = np.array([pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs], dtype=np.float64)
+    launch_s = region["start"].elapsed_time(region["end"]) * 1e-3 / (args.steps * n_packs)
+
+    # Per-call spread, from one extra step with an event pair around every
+    # launch (outside the timed region: per-call event records perturb the
+    # stream they time).
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_packs)]
+    one_step(events)
+    torch.cuda.synchronize()
+    durs = np.array([s_.elapsed_time(e_) * 1e-3 for s_, e_ in events])   # seconds
 
     value = step_bytes * args.steps / wall / 1e9
-    kernel_gbps = mb_bytes.sum() * args.steps / durs.sum() / 1e9
-    per_call = (mb_bytes[None, :] / durs / 1e9).ravel()
+    kernel_gbps = float(mb_bytes.mean()) / launch_s / 1e9
+    per_call = mb_bytes / durs / 1e9
     traffic = counter_traffic(cfg.name)
     mean_bytes = float(mb_bytes.mean())
     result = {
@@ -306,11 +324,12 @@ def main() -> int:
         "step_tokens": step_tokens,
         "step_bytes": step_bytes,
         "deferred_samples": deferred,
-        "pack_kernel": {"launches": int(durs.size), "mean_us": round(float(durs.mean()) * 1e6, 3),
-                        "call_us_p10_p50_p90_max": [round(float(np.percentile(durs, q)) * 1e6, 2) for q in (10, 50, 90, 100)],
-                        "slowest_call_mb_index": int(np.unravel_index(np.argmax(durs), durs.shape)[1]),
-                        "median_call_GBps": round(float(np.median(per_call)), 2),
-                        "aggregate_GBps": round(kernel_gbps, 2)},
+        "pack_kernel": {"launches": args.steps * n_packs, "mean_us": round(launch_s * 1e6, 3),
+                        "timing": "pack-stream event pair around all launches of the timed steps",
+                        "GBps": round(kernel_gbps, 2),
+                        "single_call_events_us_p10_p50_p90_max": [round(float(np.percentile(durs, q)) * 1e6, 2)
+                                                                   for q in (10, 50, 90, 100)],
+                        "single_call_median_GBps": round(float(np.median(per_call)), 2)},
         "roofline": {"bound": "hbm", "achieved": round(kernel_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(kernel_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": (round(traffic) if traffic else None),
