@@ -38,6 +38,10 @@ constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves
 constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
 constexpr int kInlineSamples = 64;   // sample headers passed by value to k_pack
 constexpr int kInlineImages = 128;   // image pairs passed by value to k_pack
+constexpr int kImgGroup = 8;       // image pairs read per scalar load group in k_pack
+constexpr int kLenGroup = 16;      // sample lengths read per scalar load group in k_pack
+constexpr int kWaveRows = 16;      // rows per wave resolved with scalar loads in k_pack
+static_assert(kInlineSamples % kLenGroup == 0, "length groups tile the inline headers");
 constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds k_pack's LDS use)
 constexpr int kMaxPackImages = 1024;
 
@@ -77,8 +81,13 @@ struct PackArgs {
   int32_t max_chunk_rows;     // rows one chunk can touch
   uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
   int32_t div_shift;
+  int32_t pt_shift;           // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
+  uint64_t pt_mul;
+  uint64_t pb_mul;            // d / page_bytes == umulhi64(d, pb_mul) >> pb_shift for d < 2^52
+  int32_t pb_shift;
+  alignas(16) int32_t lens[kInlineSamples];   // sample lengths, zero past n
   PackSample samples[kInlineSamples];
-  int2 imgs[kInlineImages];
+  int2 imgs[kInlineImages + kImgGroup];       // zero past n_imgs, so a group may overrun
 };
 
 struct WriteArgs {

@@ -344,6 +344,13 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
   if (c.hbm_backing || c.host_backing) return fail(FP_EINVAL, "caller-provided backing is not supported");
   if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
   if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
+  {
+    // The pack kernel divides GVA offsets below 2^52 by the page size.
+    const unsigned __int128 span = (unsigned __int128)(c.hbm_pages + c.host_pages) *
+                                   (unsigned __int128)(2ll * c.hidden) * (unsigned __int128)c.page_tokens;
+    if (span >= ((unsigned __int128)1 << 52) || (unsigned __int128)c.gva_start + span > ~(uint64_t)0)
+      return fail(FP_EINVAL, "GVA span of the pool exceeds 2^52 bytes or the address space");
+  }
   if (c.max_samples == 0) c.max_samples = kDefaultMaxSamples;
   if (c.max_samples < 1 || c.max_samples > (1ll << 31) - 1) return fail(FP_EINVAL, "max_samples");
   if (c.meta_bytes == 0) c.meta_bytes = kDefaultMetaBytes;
@@ -701,6 +708,25 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   while ((1ll << ceil_log2) < vpr) ++ceil_log2;
   a.div_shift = 31 + ceil_log2;
   a.div_mul = (uint64_t)(((1ull << a.div_shift) + (uint64_t)vpr - 1) / (uint64_t)vpr);
+  // The same for a visual-row index by page_tokens.
+  const int64_t pt = p->cfg.page_tokens;
+  ceil_log2 = 0;
+  while ((1ll << ceil_log2) < pt) ++ceil_log2;
+  a.pt_shift = 31 + ceil_log2;
+  a.pt_mul = (uint64_t)(((1ull << a.pt_shift) + (uint64_t)pt - 1) / (uint64_t)pt);
+  // GVA offset d < 2^52 by page_bytes: with c = ceil(log2 pb), N = max(52, 64 - c)
+  // and s = N + c, m = ceil(2^s / pb) fits in 64 bits and d / pb == (d * m) >> s,
+  // taken as the high 64 bits of the 128-bit product shifted by s - 64.
+  {
+    const uint64_t pbu = (uint64_t)p->pb;
+    int c = 0;
+    while ((1ull << c) < pbu) ++c;
+    const int nbits = std::max(52, 64 - c);
+    const int sh = nbits + c;
+    const unsigned __int128 m = (((unsigned __int128)1 << sh) + pbu - 1) / pbu;
+    a.pb_mul = (uint64_t)m;
+    a.pb_shift = sh - 64;
+  }
   const bool staged = n > fp::kInlineSamples || n_imgs > fp::kInlineImages;
   std::vector<fp::PackSample> big_s;
   std::vector<int2> big_i;
@@ -716,6 +742,7 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   for (int32_t i = 0; i < n; ++i) {
     const SampleRec& r = *recs[(size_t)i];
     smp[i] = fp::PackSample{r.len, r.n_img, base, r.n_text, r.text_off, r.page_off};
+    if (!staged) a.lens[i] = r.len;
     for (int32_t j = 0; j < r.n_img; ++j) img[base + j] = int2{r.img[2 * (size_t)j], r.img[2 * (size_t)j + 1]};
     base += r.n_img;
   }

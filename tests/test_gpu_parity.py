@@ -254,3 +254,61 @@ def test_tier_mask_split(fp):
         assert torch.equal(part[:n], full[:n]) and torch.equal(cu, cu2) and torch.equal(pos, pos2)
         part.fill_(0x2222)
     w.close()
+
+
+def _head_specs(rng, n, max_img, vocab):
+    """n samples of 1..29 text tokens; sample i has i % (max_img + 1) images of 0..40 rows each at
+    random placeholder positions (some empty, some at 0 or at the end)."""
+    specs = []
+    for i in range(n):
+        t = int(rng.integers(1, 30))           # a sample holds at least one row
+        k = i % (max_img + 1)
+        pos = np.sort(rng.integers(0, t + 1, size=k)).astype(np.int32)
+        ntok = rng.integers(0, 41, size=k).astype(np.int32)
+        specs.append(SampleSpec(rng.integers(0, vocab, size=t).astype(np.int32), pos, ntok))
+    return specs
+
+
+@pytest.mark.parametrize("hidden,page_tokens", [(8, 3), (16, 16), (64, 5), (96, 7), (128, 1),
+                                                (256, 16), (3584, 64), (8192, 32)])
+def test_chunk_head_shapes(fp, hidden, page_tokens):
+    """Row resolution at every chunk shape: many rows per chunk (small H,
+    staged in LDS) down to chunks inside one row (large H); page sizes that
+    are not powers of two; 17..64 samples with inline headers, samples with
+    more than eight images, the 64-sample and 128-image limits of the inline
+    headers and microbatches just past them."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    say(f"case chunk-head H={hidden} P={page_tokens}")
+    vocab = 257
+    rng = np.random.default_rng(hidden * 1000 + page_tokens)
+    specs = _head_specs(rng, 70, 11, vocab) + _head_specs(rng, 70, 1, vocab)
+    n_vis = sum(s.n_vis for s in specs)
+    pages = sum(-(-s.n_vis // page_tokens) for s in specs) + 8
+    cfg = scaled(CONFIGS["tiny"], hidden=hidden, page_tokens=page_tokens, hbm_pages=pages,
+                 vocab=vocab, capacity=n_vis + 4000, n_mb=1)
+    table = tagged_table(vocab, hidden)
+    vis = [tagged_vis(i, s.n_vis, hidden) for i, s in enumerate(specs)]
+    w = GpuWorkload(cfg, 0, specs=specs, table=to_dev(table),
+                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None)
+    try:
+        total = sum(s.length for s in specs)
+        out, cu, pos = w.alloc_outputs(rows=total + 64, fill=0x4545)
+        cu = torch.full((150,), -1, dtype=torch.int32, device="cuda")
+        imgs = np.cumsum([len(s.img_ntok) for s in specs])
+        n128 = int(np.searchsorted(imgs, 128, side="right"))     # first n samples hold <= 128 images
+        groups = [list(range(17)), list(range(n128)), list(range(n128 + 1)),
+                  list(range(70, 134)), list(range(70, 135)), list(range(70)),
+                  [11, 23, 11, 35, 140 - 1]]
+        for g in groups:
+            say(f"  group of {len(g)} samples, {sum(len(specs[i].img_ntok) for i in g)} images")
+            n, mx = w.pack([w.ids[i] for i in g], out, cu, pos)
+            torch.cuda.synchronize()
+            want = definitional_pack([specs[i] for i in g], [vis[i] for i in g], table)
+            assert n == len(want[0]) and mx == want[3]
+            assert np.array_equal(to_host(out[:n]), want[0])
+            assert cu[:len(g) + 1].cpu().numpy().tolist() == want[1].tolist()
+            assert pos[:n].cpu().numpy().tolist() == want[2].tolist()
+            assert bool((out[n:] == 0x4545).all())
+            out.fill_(0x4545)
+    finally:
+        w.close()
