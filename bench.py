@@ -196,6 +196,59 @@ def d2d_ceiling(nbytes: int = 1 << 30, iters: int = 10) -> float:
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+SCHED_CAPACITIES = (2048, 4096, 8192, 16384, 32768)
+
+
+def scheduler_bench(args) -> int:
+    """Overhead of the dynamic packing scheduler (Alg. 1) per scheduling call,
+    host only: one call packs a window of n_ranks * mb_per_rank * L tokens of
+    qwen-workload sample lengths (clipped to L) into microbatches of L tokens,
+    buckets them and deals them to n_ranks ranks. The oracle is timed on the
+    same call as the CPU baseline and must give the same plan."""
+    import statistics
+
+    import numpy as np
+
+    from oracle.schedule import dynamic_packing
+    from paper_2606_23087_amd import flowpool as fp
+    from paper_2606_23087_amd.workloads import schedule_lengths
+
+    N, K, per = args.sched_ranks, args.sched_buckets, args.sched_mb_per_rank
+    rows = []
+    for L in SCHED_CAPACITIES:
+        lens = schedule_lengths(args.seed, L, N * per * L)
+        r = fp.plan_dynamic_packing(lens, L, N, K)
+        ts = []
+        for _ in range(args.sched_reps):
+            t0 = time.perf_counter()
+            r = fp.plan_dynamic_packing(lens, L, N, K)
+            ts.append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        want = dynamic_packing([int(x) for x in lens], L, N, K)
+        t_oracle = time.perf_counter() - t0
+        same = (want["mb_of_seq"] == r["mb_of_seq"].tolist() and want["mb_rank"] == r["mb_rank"].tolist()
+                and want["mb_slot"] == r["mb_slot"].tolist() and want["mb_bucket"] == r["mb_bucket"].tolist())
+        rank_cost = np.zeros(N)
+        np.add.at(rank_cost, r["mb_rank"], r["mb_cost_scaled"].astype(float))
+        rows.append(dict(L=L, sequences=int(len(lens)), microbatches=int(r["n_mb"]),
+                         ms_median=round(statistics.median(ts) * 1e3, 4), ms_min=round(min(ts) * 1e3, 4),
+                         oracle_ms=round(t_oracle * 1e3, 2), same_plan_as_oracle=bool(same),
+                         fill=round(float(lens.sum()) / (r["n_mb"] * L), 4),
+                         rank_cost_max_over_mean=round(float(rank_cost.max() / rank_cost.mean()), 4)))
+        log(f"scheduler L={L}: {rows[-1]}")
+    print(json.dumps({
+        "metric": "dynamic packing scheduler overhead per scheduling call (Alg. 1)",
+        "value": rows[-1]["ms_median"], "unit": "ms", "higher_is_better": False,
+        "data": "synthetic (qwen-workload sample lengths, clipped to L)",
+        "config": {"workload": "alg1-scheduler", "n_ranks": N, "n_buckets": K, "window_tokens": f"{N * per} * L",
+                   "capacities": list(SCHED_CAPACITIES), "reps": args.sched_reps, "seed": args.seed},
+        "per_capacity": rows,
+        "cpu_baseline": {"value": rows[-1]["oracle_ms"], "unit": "ms", "cores": 1, "kind": "oracle",
+                         "sample": "the same call at L = 32768, once, single-threaded Python"},
+    }), flush=True)
+    return 0 if all(x["same_plan_as_oracle"] for x in rows) else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,8 +261,16 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB copy (reference for HBM byte counters)")
+    ap.add_argument("--scheduler", action="store_true",
+                    help="time the dynamic packing scheduler (Alg. 1) on the host instead of the pack")
+    ap.add_argument("--sched-ranks", type=int, default=32)
+    ap.add_argument("--sched-buckets", type=int, default=4)
+    ap.add_argument("--sched-mb-per-rank", type=int, default=8)
+    ap.add_argument("--sched-reps", type=int, default=50)
     args = ap.parse_args()
 
+    if args.scheduler:
+        return scheduler_bench(args)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this build "
               "(run with --gpus 1)", file=sys.stderr)

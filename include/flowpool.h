@@ -185,6 +185,46 @@ fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, in
                          int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
                          int32_t* out_mb_max_len);
 
+/* Dynamic packing scheduler (Alg. 1, Sec. 3.4), host only (no pool, no GPU).
+ * Phase 1, best fit: sequences are taken in input order; each goes to the open
+ * microbatch whose residual capacity is the smallest that still holds it
+ * (found by a segment tree over residuals [0, capacity]; equal residuals: the
+ * microbatch opened first), else it opens a new microbatch of `capacity`
+ * tokens; a microbatch whose residual falls below the shortest length of the
+ * call is closed. Microbatches are numbered in the order they are opened.
+ * Phase 2, load balancing: each microbatch's Eq. 3 cost, returned exactly as
+ * capacity * sum(l) + l_max^2 (= capacity^2 * Cost); buckets of similar cost
+ * by one-dimensional k-means (min(n_buckets, microbatches) centroids started
+ * at the costs of sorted positions floor((2k+1) m / 2K), nearest centroid
+ * with ties to the lower index, exact rational centroids, at most 100
+ * rounds; bucket 0 holds the cheapest); buckets from the costliest down, each
+ * one's microbatches in decreasing cost (ties: lower index) dealt to ranks
+ * 0..N-1, then N-1..0, and so on, restarting at rank 0 for every bucket.
+ *  lengths             host int32[n], each in [1, capacity]
+ *  capacity            L, tokens per microbatch, at most 2^20
+ *  n_ranks, n_buckets  N >= 1 data-parallel ranks, K >= 1 buckets
+ * Outputs (host, caller-owned, any may be NULL; per-microbatch arrays need
+ * room for n entries, of which *out_n_mb are written):
+ *  out_mb_of_seq[n]    microbatch of each sequence
+ *  out_mb_tokens, out_mb_max_len, out_mb_cost_scaled, out_mb_bucket,
+ *  out_mb_rank         the rank a microbatch is dealt to
+ *  out_mb_slot         its position in that rank's dispatch order
+ * Deterministic. Errors: EINVAL. */
+fp_status plan_dynamic_packing(const int32_t* lengths, int32_t n, int32_t capacity,
+                               int32_t n_ranks, int32_t n_buckets, int32_t* out_mb_of_seq,
+                               int32_t* out_n_mb, int32_t* out_mb_tokens, int32_t* out_mb_max_len,
+                               int64_t* out_mb_cost_scaled, int32_t* out_mb_bucket,
+                               int32_t* out_mb_rank, int32_t* out_mb_slot);
+
+/* plan_dynamic_packing over resident samples: sequence i is sample_ids[i]
+ * with its pool length (text + image rows). Errors: EINVAL (also a sample
+ * longer than capacity), ENOENT. */
+fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
+                            int32_t n_ranks, int32_t n_buckets, int32_t* out_mb_of_seq,
+                            int32_t* out_n_mb, int32_t* out_mb_tokens, int32_t* out_mb_max_len,
+                            int64_t* out_mb_cost_scaled, int32_t* out_mb_bucket,
+                            int32_t* out_mb_rank, int32_t* out_mb_slot);
+
 /* Consumer pack: the hot path (Sec. 3.1, Sec. 3.2). For samples
  * sample_ids[0..n) in order, writes the packed microbatch:
  *  out_emb           device bf16 [out_rows_cap, H], 16-byte aligned. Row

@@ -22,6 +22,7 @@
 
 #include "flowpool.h"
 #include "fp_internal.h"
+#include "schedule.h"
 
 using fp::SampleDesc;
 
@@ -646,6 +647,78 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
   if (out_sample_cost_scaled) std::memcpy(out_sample_cost_scaled, costs.data(), 8 * (size_t)n);
   return greedy(lens.data(), costs.data(), n, capacity, n_mb, out_assign, out_mb_tokens, out_mb_cost_scaled,
                 out_mb_max_len);
+}
+
+namespace {
+
+constexpr int32_t kMaxPackingCapacity = 1 << 20;
+
+fp_status packing_outputs(const fp::PackingPlan& plan, int32_t* out_mb_of_seq, int32_t* out_n_mb,
+                          int32_t* out_mb_tokens, int32_t* out_mb_max_len, int64_t* out_mb_cost_scaled,
+                          int32_t* out_mb_bucket, int32_t* out_mb_rank, int32_t* out_mb_slot) {
+  const size_t m = plan.tokens.size();
+  if (out_n_mb) *out_n_mb = (int32_t)m;
+  if (out_mb_of_seq) std::copy(plan.mb_of_seq.begin(), plan.mb_of_seq.end(), out_mb_of_seq);
+  if (out_mb_tokens) std::copy(plan.tokens.begin(), plan.tokens.end(), out_mb_tokens);
+  if (out_mb_max_len) std::copy(plan.max_len.begin(), plan.max_len.end(), out_mb_max_len);
+  if (out_mb_cost_scaled) std::copy(plan.cost.begin(), plan.cost.end(), out_mb_cost_scaled);
+  if (out_mb_bucket) std::copy(plan.bucket.begin(), plan.bucket.end(), out_mb_bucket);
+  if (out_mb_rank) std::copy(plan.rank.begin(), plan.rank.end(), out_mb_rank);
+  if (out_mb_slot) std::copy(plan.slot.begin(), plan.slot.end(), out_mb_slot);
+  return FP_OK;
+}
+
+fp_status check_packing_args(int32_t n, int32_t capacity, int32_t n_ranks, int32_t n_buckets) {
+  if (n < 0) return fail(FP_EINVAL, "n %d", n);
+  if (capacity < 1 || capacity > kMaxPackingCapacity)
+    return fail(FP_EINVAL, "capacity %d outside [1, %d]", capacity, kMaxPackingCapacity);
+  if (n_ranks < 1) return fail(FP_EINVAL, "n_ranks %d", n_ranks);
+  if (n_buckets < 1) return fail(FP_EINVAL, "n_buckets %d", n_buckets);
+  return FP_OK;
+}
+
+}  // namespace
+
+fp_status plan_dynamic_packing(const int32_t* lengths, int32_t n, int32_t capacity, int32_t n_ranks,
+                               int32_t n_buckets, int32_t* out_mb_of_seq, int32_t* out_n_mb,
+                               int32_t* out_mb_tokens, int32_t* out_mb_max_len, int64_t* out_mb_cost_scaled,
+                               int32_t* out_mb_bucket, int32_t* out_mb_rank, int32_t* out_mb_slot) {
+  fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
+  if (st != FP_OK) return st;
+  if (n > 0 && !lengths) return fail(FP_EINVAL, "null lengths");
+  for (int32_t i = 0; i < n; ++i)
+    if (lengths[i] < 1 || lengths[i] > capacity)
+      return fail(FP_EINVAL, "length %d of sequence %d outside [1, %d]", lengths[i], i, capacity);
+  fp::PackingPlan plan;
+  fp::dynamic_packing(lengths, n, capacity, n_ranks, n_buckets, &plan);
+  return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
+                         out_mb_bucket, out_mb_rank, out_mb_slot);
+}
+
+fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
+                            int32_t n_ranks, int32_t n_buckets, int32_t* out_mb_of_seq, int32_t* out_n_mb,
+                            int32_t* out_mb_tokens, int32_t* out_mb_max_len, int64_t* out_mb_cost_scaled,
+                            int32_t* out_mb_bucket, int32_t* out_mb_rank, int32_t* out_mb_slot) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
+  if (st != FP_OK) return st;
+  if (n > 0 && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
+  std::vector<int32_t> lens((size_t)n);
+  {
+    std::lock_guard<std::mutex> lock(p->mu);
+    for (int32_t i = 0; i < n; ++i) {
+      auto it = p->samples.find(sample_ids[i]);
+      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+      lens[(size_t)i] = it->second.len;
+      if (lens[(size_t)i] > capacity)
+        return fail(FP_EINVAL, "sample %llu of length %d exceeds capacity %d",
+                    (unsigned long long)sample_ids[i], lens[(size_t)i], capacity);
+    }
+  }
+  fp::PackingPlan plan;
+  fp::dynamic_packing(lens.data(), n, capacity, n_ranks, n_buckets, &plan);
+  return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
+                         out_mb_bucket, out_mb_rank, out_mb_slot);
 }
 
 fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,

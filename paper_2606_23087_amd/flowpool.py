@@ -78,6 +78,10 @@ _SIGS = {
     "pool_sample_info": (C.c_int32, [_P, C.c_uint64, _i32p, _i32p, _i32p]),
     "pool_translate": (C.c_int32, [_P, C.c_uint64, _i32p, _u64p]),
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
+    "plan_dynamic_packing": (C.c_int32, [_i32p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
+                                         _i32p, _i32p, _i64p, _i32p, _i32p, _i32p]),
+    "plan_pool_packing": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
+                                      _i32p, _i32p, _i64p, _i32p, _i32p, _i32p]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -195,6 +199,35 @@ def plan_partition(lengths, costs_scaled, capacity: int, n_mb: int):
                                tok.ctypes.data_as(_i32p), cst.ctypes.data_as(_i64p),
                                mx.ctypes.data_as(_i32p)), "plan_partition")
     return dict(assign=assign, mb_tokens=tok, mb_cost_scaled=cst, mb_max_len=mx)
+
+
+def _packing_call(fn, name, head, n, capacity, n_ranks, n_buckets):
+    mb_of_seq = np.empty(n, np.int32)
+    n_mb = C.c_int32()
+    per = [np.empty(max(n, 1), t) for t in (np.int32, np.int32, np.int64, np.int32, np.int32, np.int32)]
+    ptrs = [a.ctypes.data_as(_i64p if a.dtype == np.int64 else _i32p) for a in per]
+    _check(fn(*head, n, capacity, n_ranks, n_buckets, mb_of_seq.ctypes.data_as(_i32p), C.byref(n_mb), *ptrs),
+           name)
+    m = n_mb.value
+    keys = ("mb_tokens", "mb_max_len", "mb_cost_scaled", "mb_bucket", "mb_rank", "mb_slot")
+    out = dict(mb_of_seq=mb_of_seq, n_mb=m)
+    out.update({k: a[:m].copy() for k, a in zip(keys, per)})
+    return out
+
+
+def plan_dynamic_packing(lengths, capacity: int, n_ranks: int, n_buckets: int):
+    """Alg. 1 on host lengths. Returns dict(mb_of_seq, n_mb, mb_tokens, mb_max_len,
+    mb_cost_scaled, mb_bucket, mb_rank, mb_slot)."""
+    ln, lp = _arr(lengths, np.int32, _i32p)
+    return _packing_call(_lib.plan_dynamic_packing, "plan_dynamic_packing", (lp,), len(ln), capacity,
+                         n_ranks, n_buckets)
+
+
+def plan_pool_packing(pool: int, sample_ids, capacity: int, n_ranks: int, n_buckets: int):
+    """Alg. 1 on resident samples (their pool lengths); same result as plan_dynamic_packing."""
+    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    return _packing_call(_lib.plan_pool_packing, "plan_pool_packing", (pool, idp), len(ids), capacity,
+                         n_ranks, n_buckets)
 
 
 def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out_rows_cap: int,

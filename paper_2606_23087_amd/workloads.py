@@ -202,6 +202,20 @@ def gen_samples(cfg: WorkloadConfig, seed: int, min_tokens: Optional[int] = None
     return out
 
 
+def schedule_lengths(seed: int, capacity: int, tokens: int, cfg_name: str = "qwen") -> np.ndarray:
+    """Sequence lengths for the dynamic packing scheduler: the lengths (text
+    plus image rows) of one workload's samples in write order, clipped to the
+    capacity, until their sum reaches ``tokens``."""
+    st = SampleStream(CONFIGS[cfg_name], seed)
+    out: List[int] = []
+    total = 0
+    while total < tokens:
+        length = min(st.next().length, capacity)
+        out.append(length)
+        total += length
+    return np.array(out, dtype=np.int32)
+
+
 # ---------------------------------------------------------------- embeddings
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:

@@ -312,3 +312,39 @@ def test_chunk_head_shapes(fp, hidden, page_tokens):
             out.fill_(0x4545)
     finally:
         w.close()
+
+
+def test_dynamic_packing_then_pack(fp):
+    """Alg. 1 over resident samples (plan_pool_packing) gives the oracle's
+    plan, and every microbatch it forms, packed in each rank's dispatch
+    order, equals the definitional pack of its samples."""
+    from oracle.schedule import dynamic_packing
+    from paper_2606_23087_amd.harness import GpuWorkload
+    cfg = scaled(CONFIGS["qwen"], hbm_pages=900, vocab=3000, capacity=16384, n_mb=2)
+    specs = gen_samples(cfg, 5, count=14)
+    say(f"case dynamic-packing samples={len(specs)}")
+    table, vis = _inputs(cfg, 5, specs, "tagged")
+    w = GpuWorkload(cfg, 5, specs=specs, table=to_dev(table),
+                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None)
+    try:
+        L, N, K = 8192 + 2048, 3, 2
+        keep = [i for i, s in enumerate(specs) if s.length <= L]
+        got = fp.plan_pool_packing(w.pool, [w.ids[i] for i in keep], L, N, K)
+        want = dynamic_packing([specs[i].length for i in keep], L, N, K)
+        assert got["mb_of_seq"].tolist() == want["mb_of_seq"]
+        for key in ("mb_tokens", "mb_max_len", "mb_cost_scaled", "mb_bucket", "mb_rank", "mb_slot"):
+            assert got[key].tolist() == want[key], key
+        out, cu, pos = w.alloc_outputs(rows=L, fill=0x3C3C)
+        for rank in range(N):
+            order = sorted((s, j) for j, (r, s) in enumerate(zip(want["mb_rank"], want["mb_slot"])) if r == rank)
+            for _, j in order:
+                idx = [keep[q] for q, m in enumerate(want["mb_of_seq"]) if m == j]
+                n, mx = w.pack([w.ids[i] for i in idx], out, cu, pos)
+                torch.cuda.synchronize()
+                ref = definitional_pack([specs[i] for i in idx], [vis[i] for i in idx], table)
+                assert n == want["mb_tokens"][j] == len(ref[0]) and mx == want["mb_max_len"][j]
+                assert np.array_equal(to_host(out[:n]), ref[0])
+                assert cu[:len(idx) + 1].cpu().numpy().tolist() == ref[1].tolist()
+                assert pos[:n].cpu().numpy().tolist() == ref[2].tolist()
+    finally:
+        w.close()
