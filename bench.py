@@ -249,6 +249,88 @@ def scheduler_bench(args) -> int:
     return 0 if all(x["same_plan_as_oracle"] for x in rows) else 1
 
 
+def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
+    """Pack GB/s of the workload's microbatches alone and while a producer
+    thread keeps writing new samples on its own stream (and freeing the oldest
+    beyond a window of 16), both timed over the same packs."""
+    import collections
+    import threading
+
+    import numpy as np
+    import torch
+
+    from paper_2606_23087_amd import flowpool as fp
+    from paper_2606_23087_amd.harness import vis_rows
+    from paper_2606_23087_amd.workloads import gen_samples
+
+    pspecs = gen_samples(cfg, args.seed + 1000, count=32)
+    pvis = [vis_rows(cfg, args.seed + 1000, i, s.n_vis, "normal") if s.n_vis else None
+            for i, s in enumerate(pspecs)]
+    prod_stream = torch.cuda.Stream()
+    mb_bytes = sum(pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs)
+    passes = max(1, args.steps)
+
+    def packs() -> float:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(pack_stream)
+        for _ in range(passes):
+            for j, mb in enumerate(mbs):
+                out, cu, pos = outs[j % len(outs)]
+                w.pack(mb, out, cu, pos, stream=pack_stream)
+        e1.record(pack_stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    torch.cuda.synchronize()
+    t_alone = packs()
+    stop = threading.Event()
+    stats = {"writes": 0, "bytes": 0, "error": None}
+
+    def producer():
+        window = collections.deque()
+        try:
+            with torch.cuda.stream(prod_stream):
+                i = 0
+                while not stop.is_set():
+                    s = pspecs[i % len(pspecs)]
+                    sid = fp.pool_write_sample(w.pool, s.text_ids, s.img_pos, s.img_ntok, pvis[i % len(pspecs)],
+                                               stream=prod_stream)
+                    window.append(sid)
+                    if len(window) > 16:
+                        fp.pool_free_sample(w.pool, window.popleft())
+                    stats["writes"] += 1
+                    stats["bytes"] += 2 * s.n_vis * cfg.row_bytes + 4 * s.n_text
+                    i += 1
+            prod_stream.synchronize()
+        except Exception as e:  # reported below
+            stats["error"] = repr(e)
+        finally:
+            for sid in window:
+                fp.pool_free_sample(w.pool, sid)
+
+    th = threading.Thread(target=producer)
+    th.start()
+    time.sleep(0.05)
+    wall0 = time.perf_counter()
+    w0, b0 = stats["writes"], stats["bytes"]
+    t_busy = packs()
+    wall = time.perf_counter() - wall0
+    w1, b1 = stats["writes"], stats["bytes"]
+    stop.set()
+    th.join()
+    torch.cuda.synchronize()
+    alone = mb_bytes * passes / t_alone / 1e9
+    busy = mb_bytes * passes / t_busy / 1e9
+    prod = (b1 - b0) / wall / 1e9
+    log(f"concurrent: pack alone {alone:.0f} GB/s, with producer {busy:.0f} GB/s, producer {prod:.0f} GB/s "
+        f"({w1 - w0} writes)")
+    return {"pack_alone_GBps": round(alone, 1), "pack_with_producer_GBps": round(busy, 1),
+            "producer_GBps": round(prod, 1), "producer_writes": w1 - w0,
+            "producer_writes_per_s": round((w1 - w0) / wall, 1), "passes": passes,
+            "pack_launches": passes * len(mbs), "producer_error": stats["error"],
+            "deferred_pages_after": fp.pool_reclaim(w.pool, True)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -267,6 +349,8 @@ def main() -> int:
     ap.add_argument("--sched-buckets", type=int, default=4)
     ap.add_argument("--sched-mb-per-rank", type=int, default=8)
     ap.add_argument("--sched-reps", type=int, default=50)
+    ap.add_argument("--concurrent", action="store_true",
+                    help="time the packs alone and under a concurrent producer on another stream")
     args = ap.parse_args()
 
     if args.scheduler:
@@ -329,6 +413,18 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"warmup done: {len(mbs)} microbatches, {step_tokens} tokens, {step_bytes / 1e6:.1f} MB per step, "
         f"{deferred} samples deferred")
+
+    if args.concurrent:
+        res = concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream)
+        print(json.dumps({
+            "metric": "pack_microbatch GB/s with a concurrent producer writing on another stream",
+            "value": res["pack_with_producer_GBps"], "unit": "GB/s", "higher_is_better": True,
+            "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{cfg.name}-h{cfg.hidden}-concurrent", "producer_window": 16,
+                       "producer_samples": 32, "seed": args.seed},
+            "concurrent": res}), flush=True)
+        w.close()
+        return 0 if res["producer_error"] is None else 1
 
     # Timed region: K whole steps back to back. One event pair on the pack
     # stream brackets every pack launch of the region (from the first pack of

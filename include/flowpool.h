@@ -21,13 +21,18 @@
  *    returns; "device" pointers must be readable/writable by the GPU (device
  *    memory, or pinned host memory mapped into the GPU address space).
  *  - `stream` is a hipStream_t cast to void* (NULL = the null stream). Work
- *    is enqueued on it; ordering against other streams is the caller's job.
+ *    is enqueued on it. The pool orders its own work across streams: a pack
+ *    or plan of a sample waits (on the GPU) for the sample's write if that
+ *    was enqueued on another stream and has not finished, and a free of a
+ *    sample still being read by an enqueued pack is deferred until that
+ *    pack completes (Sec. 3.1: producers and consumers run decoupled).
+ *    For that, a stream passed to pack_microbatch must stay valid until the
+ *    samples it packed are freed or the pool is destroyed.
  *  - Embeddings are bf16, row-major, H elements per row; the library moves
  *    them as raw 16-bit words (NaN payloads, signed zeros and denormals are
  *    preserved exactly).
- *  - A pool is not safe for concurrent calls from several threads; calls are
- *    serialised internally by a mutex, but stream ordering between a write,
- *    a free and a pack that touch the same sample is the caller's job.
+ *  - Calls from several threads are serialised internally by a mutex, so a
+ *    producer thread and a consumer thread may share one pool.
  */
 #ifndef FLOWPOOL_H
 #define FLOWPOOL_H
@@ -150,10 +155,22 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
                             const void* vis_emb, const uint8_t* page_tier_wish,
                             void* stream, uint64_t* out_sample_id);
 
-/* Release a sample: its pages, metadata and slot return to the free lists at
- * once. The caller guarantees no enqueued pack or plan still reads it.
- * Errors: ENOENT. */
+/* Release a sample; its id becomes invalid at once. Its pages, metadata and
+ * slot return to the free lists as soon as the work enqueued before this call
+ * on every stream that packed the sample has completed: at once if those
+ * streams are idle, otherwise later (an event recorded on each busy one;
+ * event-deferred reclamation, checked by the next write or by pool_reclaim).
+ * If the sample's own write has not finished, the call waits for it. Pages
+ * freed while no pack is pending return in free order.
+ * Errors: ENOENT, EHIP. */
 fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
+
+/* Returns the resources of deferred frees whose packs have completed (with
+ * wait != 0, first waits for all of them). *out_deferred_pages (host, may be
+ * NULL) receives the pages still deferred. pool_write_sample reclaims by
+ * itself and, when memory runs short, waits for the packs holding deferred
+ * pages. Errors: EHIP. */
+fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages);
 
 /* Planner (Sec. 3.4): evaluate each sample's cost K*l + l^2 (the per-sample
  * cost l + l^2/K scaled by K; l = text + visual rows) with a GPU kernel over

@@ -117,6 +117,62 @@ struct SampleRec {
   int64_t text_off, page_off;    // metadata-arena offsets of text ids and page GVAs
   std::vector<uint64_t> pages;   // GVAs in visual-row order
   std::vector<int32_t> img;      // (placeholder position, rows) per image
+  // Stream ordering with the GPU work that touches the sample:
+  int32_t written = -1;          // event after its write (metadata upload +
+                                 // k_write), -1 once seen complete
+  void* write_stream = nullptr;  // stream of that write
+  std::vector<void*> readers;    // streams that have packed it
+};
+
+// A freed sample whose pages, metadata and slot wait for packs still in
+// flight; they return to the allocators once all its events have completed.
+struct Deferred {
+  std::vector<uint64_t> pages;
+  int64_t meta_off = 0, meta_len = 0;
+  int32_t slot = -1;
+  std::vector<int32_t> events;
+};
+
+// Reference-counted, reusable HIP events (timing disabled).
+struct EventPool {
+  std::vector<hipEvent_t> ev;
+  std::vector<int32_t> refs;
+  std::vector<int32_t> idle;
+  hipError_t acquire(int32_t* out) {
+    if (idle.empty()) {
+      hipEvent_t e = nullptr;
+      hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+      if (r != hipSuccess) return r;
+      ev.push_back(e);
+      refs.push_back(0);
+      idle.push_back((int32_t)ev.size() - 1);
+    }
+    *out = idle.back();
+    idle.pop_back();
+    refs[(size_t)*out] = 1;
+    return hipSuccess;
+  }
+  void ref(int32_t i) { ++refs[(size_t)i]; }
+  void unref(int32_t i) {
+    if (--refs[(size_t)i] == 0) idle.push_back(i);
+  }
+  // Completed (or failed: a failure shows up again at the next synchronising call).
+  bool done(int32_t i) {
+    const hipError_t r = hipEventQuery(ev[(size_t)i]);
+    if (r == hipErrorNotReady) return false;
+    if (r != hipSuccess) (void)hipGetLastError();
+    return true;
+  }
+  // Drops the completed events of a list (waiting for each first if `wait`).
+  void prune(std::vector<int32_t>* list, bool wait) {
+    size_t k = 0;
+    for (int32_t i : *list) {
+      if (wait) (void)hipEventSynchronize(ev[(size_t)i]);
+      if (done(i)) unref(i);
+      else (*list)[k++] = i;
+    }
+    list->resize(k);
+  }
 };
 
 uint64_t splitmix64(uint64_t& s) {
@@ -155,6 +211,9 @@ struct fp_pool {
   RangeAlloc meta;
   std::unordered_map<uint64_t, SampleRec> samples;
   uint64_t next_id = 1;
+  EventPool events;
+  std::vector<Deferred> deferred;
+  int64_t deferred_pages = 0;
   // staging
   Stage ring[kRing];
   int ring_next = 0;
@@ -208,6 +267,11 @@ fp_status stage_release(Stage* s, hipStream_t stream) {
 }
 
 void free_all(fp_pool* p) {
+  for (hipEvent_t e : p->events.ev) {
+    (void)hipEventSynchronize(e);
+    (void)hipEventDestroy(e);
+  }
+  p->events = EventPool{};
   for (auto& s : p->ring) {
     if (s.ev) (void)hipEventSynchronize(s.ev);
     if (s.host) (void)hipHostFree(s.host);
@@ -278,6 +342,46 @@ void release_pages(fp_pool* p, const std::vector<uint64_t>& pages) {
     p->n_free[t] += 1;
     if (p->cfg.alloc_policy == FP_ALLOC_SCATTER) p->stack[t].push_back(i);
   }
+}
+
+// Returns what a deferred free holds to the allocators.
+void release_deferred(fp_pool* p, Deferred& d) {
+  release_pages(p, d.pages);
+  if (d.meta_len > 0) p->meta.release(d.meta_off, d.meta_len);
+  p->free_slots.push_back(d.slot);
+  p->deferred_pages -= (int64_t)d.pages.size();
+}
+
+// Completes the deferred frees whose packs have finished, oldest first
+// (waiting for all of them if `wait`).
+void reclaim(fp_pool* p, bool wait) {
+  size_t k = 0;
+  for (size_t i = 0; i < p->deferred.size(); ++i) {
+    Deferred& d = p->deferred[i];
+    p->events.prune(&d.events, wait);
+    if (d.events.empty()) {
+      release_deferred(p, d);
+    } else {
+      if (k != i) p->deferred[k] = std::move(d);   // never self-move: it would empty the record
+      ++k;
+    }
+  }
+  p->deferred.resize(k);
+}
+
+// Makes `stream` wait for the writes of the given samples that may still be
+// running on another stream (host-side check first: usually they are done).
+fp_status order_after_writes(fp_pool* p, const std::vector<SampleRec*>& recs, hipStream_t stream) {
+  for (SampleRec* r : recs) {
+    if (r->written < 0) continue;
+    if (p->events.done(r->written)) {
+      p->events.unref(r->written);
+      r->written = -1;
+    } else if (r->write_stream != (void*)stream) {
+      FP_HIP(hipStreamWaitEvent(stream, p->events.ev[(size_t)r->written], 0));
+    }
+  }
+  return FP_OK;
 }
 
 fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
@@ -498,18 +602,26 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
     }
     vis_dev = (const uint8_t*)(attr.devicePointer ? attr.devicePointer : vis_emb);
   }
-  if (p->free_slots.empty()) return fail(FP_ENOMEM, "all %lld sample slots in use", (long long)p->cfg.max_samples);
   const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);
   int64_t meta_off = 0;
-  if (meta_len > 0) {
-    meta_off = p->meta.alloc(meta_len);
-    if (meta_off < 0) return fail(FP_ENOMEM, "metadata arena full (%lld bytes wanted)", (long long)meta_len);
-  }
   SampleRec rec;
-  fp_status st = alloc_pages(p, n_pages, page_tier_wish, &rec.pages);
-  if (st != FP_OK) {
-    if (meta_len > 0) p->meta.release(meta_off, meta_len);
-    return st;
+  fp_status st = FP_OK;
+  // Frees deferred behind packs in flight come back first; if that is not
+  // enough, wait for those packs (the producer yields to the consumer).
+  reclaim(p, false);
+  for (int attempt = 0;; ++attempt) {
+    st = FP_OK;
+    if (p->free_slots.empty()) {
+      st = fail(FP_ENOMEM, "all %lld sample slots in use", (long long)p->cfg.max_samples);
+    } else if (meta_len > 0 && (meta_off = p->meta.alloc(meta_len)) < 0) {
+      st = fail(FP_ENOMEM, "metadata arena full (%lld bytes wanted)", (long long)meta_len);
+    } else {
+      st = alloc_pages(p, n_pages, page_tier_wish, &rec.pages);
+      if (st != FP_OK && meta_len > 0) p->meta.release(meta_off, meta_len);
+    }
+    if (st == FP_OK) break;
+    if (attempt > 0 || p->deferred.empty()) return st;
+    reclaim(p, true);
   }
   auto rollback = [&](fp_status s) {
     std::string keep = t_err;
@@ -560,6 +672,17 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   wa.tile_rows = p->tile_rows;
   hipError_t e = fp::launch_write(wa, hs);
   if (e != hipSuccess) return rollback(fail(FP_EHIP, "write kernel: %s", hipGetErrorString(e)));
+  int32_t ev = -1;
+  e = p->events.acquire(&ev);
+  if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
+  if (e != hipSuccess) {
+    // The write is already queued: wait for it rather than hand out its pages again.
+    (void)hipStreamSynchronize(hs);
+    if (ev >= 0) p->events.unref(ev);
+    return rollback(fail(FP_EHIP, "write event: %s", hipGetErrorString(e)));
+  }
+  rec.written = ev;
+  rec.write_stream = stream;
   p->free_slots.pop_back();
   rec.slot = slot;
   rec.len = (int32_t)len;
@@ -586,10 +709,57 @@ fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
   std::lock_guard<std::mutex> lock(p->mu);
   auto it = p->samples.find(sample_id);
   if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
-  release_pages(p, it->second.pages);
-  if (it->second.meta_len > 0) p->meta.release(it->second.meta_off, it->second.meta_len);
-  p->free_slots.push_back(it->second.slot);
+  SampleRec& r = it->second;
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  // The sample's own write is waited for here, so that reuse of its pages
+  // never races with it on another stream and, without packs in flight,
+  // pages return in free order. Packs still reading it defer the release.
+  if (r.written >= 0) {
+    FP_HIP(hipEventSynchronize(p->events.ev[(size_t)r.written]));
+    p->events.unref(r.written);
+    r.written = -1;
+  }
+  Deferred d;
+  // An event recorded now on every stream that packed the sample and still
+  // has work queued follows those packs; idle streams need none.
+  for (void* st : r.readers) {
+    const hipError_t q = hipStreamQuery((hipStream_t)st);
+    if (q == hipSuccess) continue;
+    if (q != hipErrorNotReady) return fail(FP_EHIP, "stream query: %s", hipGetErrorString(q));
+    int32_t ev = -1;
+    hipError_t e = p->events.acquire(&ev);
+    if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], (hipStream_t)st);
+    if (e != hipSuccess) {
+      if (ev >= 0) p->events.unref(ev);
+      for (int32_t x : d.events) p->events.unref(x);
+      return fail(FP_EHIP, "free event: %s", hipGetErrorString(e));
+    }
+    d.events.push_back(ev);
+  }
+  d.pages = std::move(r.pages);
+  d.meta_off = r.meta_off;
+  d.meta_len = r.meta_len;
+  d.slot = r.slot;
   p->samples.erase(it);
+  if (d.events.empty()) {
+    release_pages(p, d.pages);
+    if (d.meta_len > 0) p->meta.release(d.meta_off, d.meta_len);
+    p->free_slots.push_back(d.slot);
+  } else {
+    p->deferred_pages += (int64_t)d.pages.size();
+    p->deferred.push_back(std::move(d));
+  }
+  return FP_OK;
+}
+
+fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  reclaim(p, wait != 0);
+  if (out_deferred_pages) *out_deferred_pages = p->deferred_pages;
   return FP_OK;
 }
 
@@ -616,6 +786,7 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
     return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d, cost_k %d", n, n_mb, capacity, cost_k);
   if (n && (!sample_ids || !out_assign)) return fail(FP_EINVAL, "null array");
   std::vector<int32_t> slots((size_t)n), lens((size_t)n);
+  std::vector<SampleRec*> recs((size_t)n);
   std::unordered_set<uint64_t> seen;
   seen.reserve((size_t)n * 2);
   for (int32_t i = 0; i < n; ++i) {
@@ -625,6 +796,7 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
       return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
     slots[(size_t)i] = it->second.slot;
     lens[(size_t)i] = it->second.len;
+    recs[(size_t)i] = &it->second;
   }
   std::vector<int64_t> costs((size_t)n);
   if (n > 0) {
@@ -637,6 +809,8 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
     if (st != FP_OK) return st;
     std::memcpy(s->host, slots.data(), 4 * (size_t)n);
     FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
+    st = order_after_writes(p, recs, hs);   // the descriptors come from the writes
+    if (st != FP_OK) return st;
     FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->dev, n, cost_k, (int64_t*)(s->dev + slot_bytes), hs));
     FP_HIP(hipMemcpyAsync(s->host + slot_bytes, s->dev + slot_bytes, 8 * (size_t)n, hipMemcpyDeviceToHost, hs));
     FP_HIP(hipStreamSynchronize(hs));
@@ -733,13 +907,13 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
   if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
   if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
-  std::vector<const SampleRec*> recs((size_t)n);
+  std::vector<SampleRec*> recs((size_t)n);
   int64_t total = 0, n_text = 0, n_imgs = 0;
   int32_t mx = 0;
   for (int32_t i = 0; i < n; ++i) {
     auto it = p->samples.find(sample_ids[i]);
     if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-    const SampleRec& r = it->second;
+    SampleRec& r = it->second;
     recs[(size_t)i] = &r;
     total += r.len;
     n_text += r.n_text;
@@ -830,12 +1004,20 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
     a.samples_dev = (const fp::PackSample*)s->dev;
     a.imgs_dev = (const int2*)(s->dev + sb);
   }
+  {
+    fp_status st = order_after_writes(p, recs, hs);
+    if (st != FP_OK) return st;
+  }
   hipError_t e = fp::launch_pack(a, hs);
   if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
   if (s) {
     fp_status st = stage_release(s, hs);
     if (st != FP_OK) return st;
   }
+  // Remember the stream as a reader of each sample; a free records its event
+  // there (no event per pack: events between back-to-back packs slow them).
+  for (SampleRec* r : recs)
+    if (std::find(r->readers.begin(), r->readers.end(), stream) == r->readers.end()) r->readers.push_back(stream);
   if (out_n_tokens) *out_n_tokens = (int32_t)total;
   if (out_max_seqlen) *out_max_seqlen = mx;
   return FP_OK;

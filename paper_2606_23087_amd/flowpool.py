@@ -78,6 +78,7 @@ _SIGS = {
     "pool_sample_info": (C.c_int32, [_P, C.c_uint64, _i32p, _i32p, _i32p]),
     "pool_translate": (C.c_int32, [_P, C.c_uint64, _i32p, _u64p]),
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
+    "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
     "plan_dynamic_packing": (C.c_int32, [_i32p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
                                          _i32p, _i32p, _i64p, _i32p, _i32p, _i32p]),
     "plan_pool_packing": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
@@ -168,6 +169,14 @@ def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page
 
 def pool_free_sample(pool: int, sample_id: int) -> None:
     _check(_lib.pool_free_sample(pool, sample_id), "pool_free_sample")
+
+
+def pool_reclaim(pool: int, wait: bool = False) -> int:
+    """Complete deferred frees whose packs are done (all, after waiting, if ``wait``).
+    Returns the pages still deferred."""
+    n = C.c_int64()
+    _check(_lib.pool_reclaim(pool, 1 if wait else 0, C.byref(n)), "pool_reclaim")
+    return int(n.value)
 
 
 def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: int, stream=None):
