@@ -198,6 +198,43 @@ class OraclePool:
             if self.alloc == "scatter":
                 self.stack[t].append(i)
 
+    def migrate(self, sid: int, tier: int) -> int:
+        """Move every page of sample ``sid`` that is not in ``tier`` into a
+        page of ``tier`` (a tier promotion or demotion, Sec. 3.2: the pool
+        spans HBM and DRAM, and data moves between them by the transport the
+        pair of tiers calls for). Scatter pools only. The moving pages, in
+        visual-row order, each take the next page popped from the tier's
+        stack and keep their bytes; the pages they leave go back to their
+        stacks last-page-first, as in a free. All-or-nothing. Returns the
+        number of pages moved."""
+        s = self.samples.get(sid)
+        if s is None:
+            raise PoolError("ENOENT", f"sample {sid}")
+        if self.alloc != "scatter" or tier not in (TIER_HBM, TIER_HOST):
+            raise PoolError("EINVAL", "migration needs the scatter policy and a tier")
+        moving = [k for k, gva in enumerate(s.pages) if self._page_of(gva)[0] != tier]
+        if len(moving) > len(self.stack[tier]):
+            raise PoolError("ENOMEM", f"{len(moving)} pages do not fit in tier {tier}")
+        old = [s.pages[k] for k in moving]
+        pages = list(s.pages)
+        for k in moving:
+            i = self.stack[tier].pop()
+            self.used[tier][i] = True
+            new = self.page_gva(tier, i)
+            ot, of, _ = self.translate(pages[k])
+            nt, nf, _ = self.translate(new)
+            if of in self.frames[ot]:
+                self.frames[nt][nf] = self.frames[ot][of].copy()
+            else:
+                self.frames[nt].pop(nf, None)
+            pages[k] = new
+        for gva in reversed(old):
+            t, i = self._page_of(gva)
+            self.used[t][i] = False
+            self.stack[t].append(i)
+        s.pages = pages
+        return len(moving)
+
     # ------------------------------------------------------------ consumer
     def _rows_of(self, s: _Sample):
         """Row sources of one sample, token by token: before text token t come

@@ -33,7 +33,7 @@ def _golden_blocks():
     return blocks
 
 
-@pytest.mark.parametrize("block", range(4))
+@pytest.mark.parametrize("block", range(5))
 def test_allocator_worked_example(block):
     b = _golden_blocks()[block]
     kv = b["kv"]
@@ -44,6 +44,20 @@ def test_allocator_worked_example(block):
     for op in b["ops"]:
         if op[0] == "free":
             pool.free(names.pop(op[1]))
+            continue
+        if op[0] == "migrate":
+            expect = op[op.index("->") + 1:]
+            before = (pool.free_pages(), [list(s) for s in pool.stack], pool.sample_pages(names[op[1]]))
+            if expect == ["ENOMEM"]:
+                with pytest.raises(PoolError) as e:
+                    pool.migrate(names[op[1]], int(op[2]))
+                assert e.value.code == "ENOMEM"
+                assert (pool.free_pages(), [list(s) for s in pool.stack],
+                        pool.sample_pages(names[op[1]])) == before
+                continue
+            pool.migrate(names[op[1]], int(op[2]))
+            assert pool.sample_pages(names[op[1]]) == [int(x, 16) for x in expect]
+            assert sum(pool.free_pages()) == sum(before[0])
             continue
         arrow = op.index("->")
         nvis = int(op[3])
@@ -193,3 +207,36 @@ def test_churn_sequence_is_feasible():
             pool.free(keys.pop(op.key))
     assert cfg.hbm_pages - pool.free_pages()[0] <= 0.5 * cfg.hbm_pages
     assert sum(op.kind == "write" for op in ops) > 500
+
+
+def test_migration_keeps_bytes_and_conserves_pages():
+    """Moving samples between tiers changes where their rows live, never the
+    packed bytes (consumers read by GVA, Sec. 3.2), and conserves pages."""
+    cfg = scaled(CONFIGS["tiered"], hidden=64, hbm_pages=40, host_pages=40, vocab=200)
+    rng = np.random.default_rng(8)
+    pool = OraclePool(cfg.hidden, 8, cfg.hbm_pages, cfg.host_pages, "scatter", cfg.vocab)
+    table = tagged_table(cfg.vocab, cfg.hidden)
+    ids, vis = [], []
+    for i in range(8):
+        nv = int(rng.integers(0, 30))
+        v = tagged_vis(i, nv, cfg.hidden)
+        wish = [int(x) for x in rng.integers(0, 2, size=-(-nv // 8))]
+        ids.append(pool.write(rng.integers(0, cfg.vocab, size=5), [2] if nv else [], [nv] if nv else [], v,
+                              tier_wish=wish))
+        vis.append(v)
+    want = pool.pack(ids, table)[0]
+    total = sum(pool.free_pages())
+    for _ in range(30):
+        sid = ids[int(rng.integers(0, len(ids)))]
+        try:
+            pool.migrate(sid, int(rng.integers(0, 2)))
+        except PoolError as e:
+            assert e.code == "ENOMEM"
+        assert np.array_equal(pool.pack(ids, table)[0], want)
+        assert sum(pool.free_pages()) == total
+        pages = [g for i in ids for g in pool.sample_pages(i)]
+        assert len(pages) == len(set(pages))
+    for sid in ids:
+        pool.migrate(sid, 0)
+        assert all(pool.translate(g)[0] == 0 for g in pool.sample_pages(sid))
+    assert np.array_equal(pool.pack(ids, table)[0], want)
