@@ -331,6 +331,72 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
             "deferred_pages_after": fp.pool_reclaim(w.pool, True)}
 
 
+def prefetch_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
+    """Tiered pool: pack every microbatch reading host-tier pages zero-copy over
+    PCIe, then the same packs with each microbatch's host-tier pages first
+    promoted into HBM by DMA copies on a copy stream (pool_migrate), the
+    migration of microbatch j+1 overlapping the pack of microbatch j, then the
+    packs again once everything sits in HBM."""
+    import torch
+
+    from paper_2606_23087_amd import flowpool as fp
+
+    mb_bytes = sum(pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs)
+    host_rows = 0
+    for mb in mbs:
+        for sid in mb:
+            pages = fp.pool_sample_pages(w.pool, sid)
+            n_vis = spec_of[sid].n_vis
+            for k, g in enumerate(pages.tolist()):
+                if fp.pool_translate(w.pool, g)[0] == fp.FP_TIER_HOST:
+                    host_rows += min(cfg.page_tokens, n_vis - k * cfg.page_tokens)
+    host_bytes = host_rows * cfg.row_bytes
+
+    def packs() -> float:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(pack_stream)
+        for j, mb in enumerate(mbs):
+            out, cu, pos = outs[j % len(outs)]
+            w.pack(mb, out, cu, pos, stream=pack_stream)
+        e1.record(pack_stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    packs()
+    t_zero_copy = packs()
+    copy_stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    c0.record(copy_stream)
+    p0.record(pack_stream)
+    moved = fp.pool_migrate(w.pool, mbs[0], fp.FP_TIER_HBM, stream=copy_stream)
+    for j, mb in enumerate(mbs):
+        if j + 1 < len(mbs):
+            moved += fp.pool_migrate(w.pool, mbs[j + 1], fp.FP_TIER_HBM, stream=copy_stream)
+        out, cu, pos = outs[j % len(outs)]
+        w.pack(mb, out, cu, pos, stream=pack_stream)
+    c1.record(copy_stream)
+    p1.record(pack_stream)
+    torch.cuda.synchronize()
+    t_pipe = time.perf_counter() - t0
+    t_copy = c0.elapsed_time(c1) * 1e-3
+    t_pipe_gpu = p0.elapsed_time(p1) * 1e-3
+    fp.pool_reclaim(w.pool, True)
+    t_hbm = packs()
+    log(f"prefetch: zero-copy {t_zero_copy * 1e3:.2f} ms, pipelined {t_pipe_gpu * 1e3:.2f} ms "
+        f"(copies {t_copy * 1e3:.2f} ms, {moved} pages), all-HBM {t_hbm * 1e3:.3f} ms")
+    return {"microbatches": len(mbs), "pack_bytes": mb_bytes, "host_tier_bytes": host_bytes,
+            "zero_copy_ms": round(t_zero_copy * 1e3, 3),
+            "zero_copy_GBps": round(mb_bytes / t_zero_copy / 1e9, 1),
+            "pipelined_ms": round(t_pipe_gpu * 1e3, 3), "pipelined_wall_ms": round(t_pipe * 1e3, 3),
+            "pages_moved": moved, "copy_stream_ms": round(t_copy * 1e3, 3),
+            "copy_GBps": round(host_bytes / t_copy / 1e9, 1),
+            "all_hbm_ms": round(t_hbm * 1e3, 3), "all_hbm_GBps": round(mb_bytes / t_hbm / 1e9, 1),
+            "pcie_peak_GBps": PCIE_PEAK_GBPS}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -349,6 +415,8 @@ def main() -> int:
     ap.add_argument("--sched-buckets", type=int, default=4)
     ap.add_argument("--sched-mb-per-rank", type=int, default=8)
     ap.add_argument("--sched-reps", type=int, default=50)
+    ap.add_argument("--prefetch", action="store_true",
+                    help="tiered pool: zero-copy packs vs packs after promoting host-tier pages into HBM")
     ap.add_argument("--concurrent", action="store_true",
                     help="time the packs alone and under a concurrent producer on another stream")
     args = ap.parse_args()
@@ -413,6 +481,17 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"warmup done: {len(mbs)} microbatches, {step_tokens} tokens, {step_bytes / 1e6:.1f} MB per step, "
         f"{deferred} samples deferred")
+
+    if args.prefetch:
+        res = prefetch_bench(args, cfg, w, mbs, spec_of, outs, pack_stream)
+        print(json.dumps({
+            "metric": "tiered pack: zero-copy host-tier reads vs host-tier pages promoted into HBM first",
+            "value": res["pipelined_ms"], "unit": "ms per 16 microbatches (pipelined promote + pack)",
+            "higher_is_better": False, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{cfg.name}-h{cfg.hidden}-prefetch", "seed": args.seed},
+            "prefetch": res}), flush=True)
+        w.close()
+        return 0
 
     if args.concurrent:
         res = concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream)

@@ -172,6 +172,25 @@ fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
  * pages. Errors: EHIP. */
 fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages);
 
+/* Tier migration (Sec. 3.2: the pool spans HBM and host DRAM; data moves
+ * between tiers by the copy engine the pair of tiers calls for). Moves every
+ * page of the samples sample_ids[0..n) that is not in `tier` (FP_TIER_HBM or
+ * FP_TIER_HOST) into a free page of `tier`: pages in visual-row order, each
+ * taking the next page of the tier's free stack, so a sample's GVAs change
+ * and its bytes do not. The copies are asynchronous DMA copies on `stream`
+ * (host <-> device through the SDMA engines; device <-> device as a copy),
+ * followed by the upload of the samples' new page lists. Packs and plans
+ * enqueued later on other streams wait for them; packs enqueued earlier keep
+ * reading the old pages, which return to their tier's free stack
+ * (last-page-first) once the copies and those packs have completed. Used to
+ * prefetch host-tier pages into HBM ahead of their packs, or to demote
+ * samples to the host tier. SCATTER pools only; a sample may be listed once.
+ * All-or-nothing. *out_pages_moved (host, may be NULL) receives the number of
+ * pages moved. Errors: EINVAL, ENOENT, ENOMEM (not enough free pages in
+ * `tier`, or metadata arena full), EHIP. */
+fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t tier,
+                       void* stream, int64_t* out_pages_moved);
+
 /* Planner (Sec. 3.4): evaluate each sample's cost K*l + l^2 (the per-sample
  * cost l + l^2/K scaled by K; l = text + visual rows) with a GPU kernel over
  * the device sample table, then partition greedily into n_mb microbatches of

@@ -115,6 +115,7 @@ struct SampleRec {
   int32_t len, n_text, n_img, n_vis;
   int64_t meta_off, meta_len;
   int64_t text_off, page_off;    // metadata-arena offsets of text ids and page GVAs
+  int64_t pl_off = -1, pl_len = 0;  // page list moved out of the main block by a migration
   std::vector<uint64_t> pages;   // GVAs in visual-row order
   std::vector<int32_t> img;      // (placeholder position, rows) per image
   // Stream ordering with the GPU work that touches the sample:
@@ -128,8 +129,8 @@ struct SampleRec {
 // flight; they return to the allocators once all its events have completed.
 struct Deferred {
   std::vector<uint64_t> pages;
-  int64_t meta_off = 0, meta_len = 0;
-  int32_t slot = -1;
+  std::vector<std::pair<int64_t, int64_t>> meta;   // metadata ranges (offset, bytes)
+  int32_t slot = -1;                               // descriptor slot, or -1
   std::vector<int32_t> events;
 };
 
@@ -347,9 +348,38 @@ void release_pages(fp_pool* p, const std::vector<uint64_t>& pages) {
 // Returns what a deferred free holds to the allocators.
 void release_deferred(fp_pool* p, Deferred& d) {
   release_pages(p, d.pages);
-  if (d.meta_len > 0) p->meta.release(d.meta_off, d.meta_len);
-  p->free_slots.push_back(d.slot);
-  p->deferred_pages -= (int64_t)d.pages.size();
+  for (const auto& m : d.meta)
+    if (m.second > 0) p->meta.release(m.first, m.second);
+  if (d.slot >= 0) p->free_slots.push_back(d.slot);
+}
+
+// Releases at once what no pending event holds, else queues it.
+void defer_or_release(fp_pool* p, Deferred&& d) {
+  if (d.events.empty()) {
+    release_deferred(p, d);
+  } else {
+    p->deferred_pages += (int64_t)d.pages.size();
+    p->deferred.push_back(std::move(d));
+  }
+}
+
+// Records an event on every stream in `readers` that still has work queued
+// (the packs that read a sample) and appends it to `events`.
+fp_status mark_readers(fp_pool* p, const std::vector<void*>& readers, std::vector<int32_t>* events) {
+  for (void* st : readers) {
+    const hipError_t q = hipStreamQuery((hipStream_t)st);
+    if (q == hipSuccess) continue;
+    if (q != hipErrorNotReady) return fail(FP_EHIP, "stream query: %s", hipGetErrorString(q));
+    int32_t ev = -1;
+    hipError_t e = p->events.acquire(&ev);
+    if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], (hipStream_t)st);
+    if (e != hipSuccess) {
+      if (ev >= 0) p->events.unref(ev);
+      return fail(FP_EHIP, "reader event: %s", hipGetErrorString(e));
+    }
+    events->push_back(ev);
+  }
+  return FP_OK;
 }
 
 // Completes the deferred frees whose packs have finished, oldest first
@@ -360,6 +390,7 @@ void reclaim(fp_pool* p, bool wait) {
     Deferred& d = p->deferred[i];
     p->events.prune(&d.events, wait);
     if (d.events.empty()) {
+      p->deferred_pages -= (int64_t)d.pages.size();
       release_deferred(p, d);
     } else {
       if (k != i) p->deferred[k] = std::move(d);   // never self-move: it would empty the record
@@ -723,33 +754,17 @@ fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
   Deferred d;
   // An event recorded now on every stream that packed the sample and still
   // has work queued follows those packs; idle streams need none.
-  for (void* st : r.readers) {
-    const hipError_t q = hipStreamQuery((hipStream_t)st);
-    if (q == hipSuccess) continue;
-    if (q != hipErrorNotReady) return fail(FP_EHIP, "stream query: %s", hipGetErrorString(q));
-    int32_t ev = -1;
-    hipError_t e = p->events.acquire(&ev);
-    if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], (hipStream_t)st);
-    if (e != hipSuccess) {
-      if (ev >= 0) p->events.unref(ev);
-      for (int32_t x : d.events) p->events.unref(x);
-      return fail(FP_EHIP, "free event: %s", hipGetErrorString(e));
-    }
-    d.events.push_back(ev);
+  fp_status st = mark_readers(p, r.readers, &d.events);
+  if (st != FP_OK) {
+    for (int32_t x : d.events) p->events.unref(x);
+    return st;
   }
   d.pages = std::move(r.pages);
-  d.meta_off = r.meta_off;
-  d.meta_len = r.meta_len;
+  d.meta.emplace_back(r.meta_off, r.meta_len);
+  if (r.pl_off >= 0) d.meta.emplace_back(r.pl_off, r.pl_len);
   d.slot = r.slot;
   p->samples.erase(it);
-  if (d.events.empty()) {
-    release_pages(p, d.pages);
-    if (d.meta_len > 0) p->meta.release(d.meta_off, d.meta_len);
-    p->free_slots.push_back(d.slot);
-  } else {
-    p->deferred_pages += (int64_t)d.pages.size();
-    p->deferred.push_back(std::move(d));
-  }
+  defer_or_release(p, std::move(d));
   return FP_OK;
 }
 
@@ -761,6 +776,176 @@ fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
   reclaim(p, wait != 0);
   if (out_deferred_pages) *out_deferred_pages = p->deferred_pages;
   return FP_OK;
+}
+
+fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t tier, void* stream,
+                       int64_t* out_pages_moved) {
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "migration needs the scatter policy");
+  if (tier != FP_TIER_HBM && tier != FP_TIER_HOST) return fail(FP_EINVAL, "tier %d", tier);
+  if (n < 0 || (n > 0 && !sample_ids)) return fail(FP_EINVAL, "n %d / null sample_ids", n);
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  std::vector<SampleRec*> recs;
+  std::vector<std::vector<int32_t>> moving;   // per sample: indices of pages to move
+  std::unordered_set<uint64_t> seen;
+  int64_t need = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = p->samples.find(sample_ids[i]);
+    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+    if (!seen.insert(sample_ids[i]).second)
+      return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
+    std::vector<int32_t> mv;
+    for (size_t k = 0; k < it->second.pages.size(); ++k) {
+      int64_t idx = 0;
+      if (p->page_index(it->second.pages[k], &idx) != tier) mv.push_back((int32_t)k);
+    }
+    if (mv.empty()) continue;
+    need += (int64_t)mv.size();
+    recs.push_back(&it->second);
+    moving.push_back(std::move(mv));
+  }
+  if (out_pages_moved) *out_pages_moved = need;
+  if (need == 0) return FP_OK;
+  // All-or-nothing: target pages and the new page lists are reserved first.
+  reclaim(p, false);
+  std::vector<int64_t> pl_off(recs.size(), -1);
+  auto unreserve = [&]() {
+    for (size_t j = 0; j < recs.size(); ++j)
+      if (pl_off[j] >= 0) p->meta.release(pl_off[j], align16(8 * (int64_t)recs[j]->pages.size()));
+    std::fill(pl_off.begin(), pl_off.end(), -1);
+  };
+  for (int attempt = 0;; ++attempt) {
+    bool ok = (int64_t)p->stack[tier].size() >= need;
+    for (size_t j = 0; ok && j < recs.size(); ++j) {
+      pl_off[j] = p->meta.alloc(align16(8 * (int64_t)recs[j]->pages.size()));
+      ok = pl_off[j] >= 0;
+    }
+    if (ok) break;
+    unreserve();
+    if (attempt > 0 || p->deferred.empty())
+      return fail(FP_ENOMEM, "%lld pages (or their page lists) do not fit in tier %d", (long long)need, tier);
+    reclaim(p, true);
+  }
+  hipStream_t hs = (hipStream_t)stream;
+  fp_status st = order_after_writes(p, recs, hs);   // the copies read what the writes wrote
+  if (st != FP_OK) {
+    unreserve();
+    return st;
+  }
+  // Staging: the new page lists, then each sample's new page_off for its descriptor.
+  size_t stage_bytes = 0;
+  for (SampleRec* r : recs) stage_bytes += (size_t)align16(8 * (int64_t)r->pages.size()) + 16;
+  Stage* sg = nullptr;
+  st = stage_acquire(p, stage_bytes, 0, &sg);
+  if (st != FP_OK) {
+    unreserve();
+    return st;
+  }
+  // From here on nothing fails half-way but a HIP error: take the pages.
+  std::vector<std::vector<uint64_t>> new_pages(recs.size());
+  std::vector<std::vector<uint64_t>> old_pages(recs.size());
+  // Consecutive pages whose old and new frames are both adjacent inside one
+  // backing chunk are copied as one run.
+  struct Run { uint64_t src, dst, bytes; int src_chunk, dst_chunk; };
+  std::vector<Run> runs;
+  const int64_t P = p->cfg.page_tokens;
+  const uint64_t chunk_span = (uint64_t)p->frames_per_chunk * (uint64_t)p->pb;
+  auto chunk_of = [&](uint64_t addr) {
+    int id = 0;
+    for (int t = 0; t < 2; ++t)
+      for (void* c : p->chunks[t]) {
+        if (addr >= (uint64_t)c && addr < (uint64_t)c + chunk_span) return id;
+        ++id;
+      }
+    return -1;
+  };
+  for (size_t j = 0; j < recs.size(); ++j) {
+    SampleRec& r = *recs[j];
+    new_pages[j] = r.pages;
+    for (int32_t k : moving[j]) {
+      const int64_t i = p->stack[tier].back();
+      p->stack[tier].pop_back();
+      p->used[tier][i] = 1;
+      p->n_free[tier] -= 1;
+      const uint64_t gva = p->page_gva(tier, i);
+      const uint64_t src = p->pte[(size_t)((r.pages[(size_t)k] - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
+      const uint64_t dst = p->pte[(size_t)((gva - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
+      const int64_t rows = std::min<int64_t>(P, r.n_vis - (int64_t)k * P);
+      const uint64_t bytes = (uint64_t)(rows * p->rb);
+      const int sc = chunk_of(src), dc = chunk_of(dst);
+      if (!runs.empty() && runs.back().src + runs.back().bytes == src && runs.back().dst + runs.back().bytes == dst &&
+          runs.back().bytes % (uint64_t)p->pb == 0 && runs.back().src_chunk == sc && runs.back().dst_chunk == dc)
+        runs.back().bytes += bytes;
+      else
+        runs.push_back(Run{src, dst, bytes, sc, dc});
+      old_pages[j].push_back(r.pages[(size_t)k]);
+      new_pages[j][(size_t)k] = gva;
+    }
+  }
+  hipError_t e = hipSuccess;
+  for (const Run& run : runs) {
+    e = hipMemcpyAsync((void*)run.dst, (const void*)run.src, run.bytes, hipMemcpyDefault, hs);
+    if (e != hipSuccess) break;
+  }
+  size_t at = 0;
+  for (size_t j = 0; e == hipSuccess && j < recs.size(); ++j) {
+    const size_t nb = 8 * new_pages[j].size();
+    std::memcpy(sg->host + at, new_pages[j].data(), nb);
+    e = hipMemcpyAsync(p->meta_dev + pl_off[j], sg->host + at, nb, hipMemcpyHostToDevice, hs);
+    at += (size_t)align16((int64_t)nb);
+    if (e != hipSuccess) break;
+    std::memcpy(sg->host + at, &pl_off[j], 8);
+    e = hipMemcpyAsync(&p->desc_dev[recs[j]->slot].page_off, sg->host + at, 8, hipMemcpyHostToDevice, hs);
+    at += 16;
+  }
+  int32_t ev = -1;
+  if (e == hipSuccess) e = p->events.acquire(&ev);
+  if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
+  if (e != hipSuccess) {
+    // Queued copies may still run: wait for them, then put everything back.
+    (void)hipStreamSynchronize(hs);
+    if (ev >= 0) p->events.unref(ev);
+    for (size_t j = 0; j < recs.size(); ++j) {
+      std::vector<uint64_t> taken;
+      for (int32_t k : moving[j]) taken.push_back(new_pages[j][(size_t)k]);
+      release_pages(p, taken);
+    }
+    unreserve();
+    return fail(FP_EHIP, "migration copies: %s", hipGetErrorString(e));
+  }
+  st = stage_release(sg, hs);
+  // The pages left behind and the old page lists wait for the copies and for
+  // every pack that may still read them.
+  for (size_t j = 0; j < recs.size(); ++j) {
+    SampleRec& r = *recs[j];
+    Deferred d;
+    d.pages = std::move(old_pages[j]);
+    const int64_t pl_bytes = align16(8 * (int64_t)r.pages.size());
+    if (r.pl_off >= 0) {
+      d.meta.emplace_back(r.pl_off, r.pl_len);
+    } else {
+      d.meta.emplace_back(r.meta_off, pl_bytes);     // the head of the main block
+      r.meta_off += pl_bytes;
+      r.meta_len -= pl_bytes;
+    }
+    r.pl_off = pl_off[j];
+    r.pl_len = pl_bytes;
+    r.page_off = pl_off[j];
+    r.pages = std::move(new_pages[j]);
+    fp_status ms = mark_readers(p, r.readers, &d.events);
+    if (ms != FP_OK && st == FP_OK) st = ms;
+    p->events.ref(ev);
+    d.events.push_back(ev);
+    if (r.written >= 0) p->events.unref(r.written);
+    p->events.ref(ev);
+    r.written = ev;
+    r.write_stream = stream;
+    defer_or_release(p, std::move(d));
+  }
+  p->events.unref(ev);
+  return st;
 }
 
 fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,

@@ -79,6 +79,7 @@ _SIGS = {
     "pool_translate": (C.c_int32, [_P, C.c_uint64, _i32p, _u64p]),
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
     "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
+    "pool_migrate": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, _P, _i64p]),
     "plan_dynamic_packing": (C.c_int32, [_i32p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
                                          _i32p, _i32p, _i64p, _i32p, _i32p, _i32p]),
     "plan_pool_packing": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
@@ -177,6 +178,14 @@ def pool_reclaim(pool: int, wait: bool = False) -> int:
     n = C.c_int64()
     _check(_lib.pool_reclaim(pool, 1 if wait else 0, C.byref(n)), "pool_reclaim")
     return int(n.value)
+
+
+def pool_migrate(pool: int, sample_ids, tier: int, stream=None) -> int:
+    """Move the samples' pages into ``tier`` (FP_TIER_HBM / FP_TIER_HOST). Returns pages moved."""
+    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    moved = C.c_int64()
+    _check(_lib.pool_migrate(pool, idp, len(ids), tier, _stream(stream), C.byref(moved)), "pool_migrate")
+    return int(moved.value)
 
 
 def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: int, stream=None):
