@@ -19,6 +19,9 @@ Plain, slow, obviously correct Python + numpy:
   visual row through the page table.
 - ``oracle.plan``   the per-sample cost l + l^2/K, the per-microbatch cost of
   Eq. 3, the greedy balanced partition, and brute-force optimal partitions.
+- ``oracle.allocate`` the heterogeneous parallel allocator of Eq. 1-2:
+  pruned candidate configurations and the lexmax (G, -F) flow matching,
+  solved by enumerating every combination.
 - ``oracle.schedule`` the dynamic packing scheduler of Alg. 1: best-fit
   packing by a plain scan of the open microbatches, Eq. 3 costs, buckets by
   exact one-dimensional k-means, and zig-zag dispatch to ranks.
@@ -27,4 +30,4 @@ All arithmetic is on Python ints or numpy integer arrays; embeddings are
 moved as raw 16-bit words and never pass through floating point.
 """
 
-from . import pack, plan, pool, schedule  # noqa: F401
+from . import allocate, pack, plan, pool, schedule  # noqa: F401
