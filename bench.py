@@ -397,6 +397,57 @@ def prefetch_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
             "pcie_peak_GBps": PCIE_PEAK_GBPS}
 
 
+ALLOC_DEVICES = (64, 128, 256, 512, 1024)
+
+
+def allocator_bench(args) -> int:
+    """Time of the allocator's flow matching (Eq. 2) on the host for clusters
+    of 8-device nodes (global batch 512, a 28-layer backbone, two encoders),
+    on synthetic throughput surrogates over the pruned candidates. The
+    oracle's enumeration is timed beside it where it finishes in seconds and
+    must give the same answer."""
+    import statistics
+
+    from oracle.allocate import solve
+    from paper_2606_23087_amd import flowpool as fp
+    from paper_2606_23087_amd.workloads import allocator_tables
+
+    rows = []
+    for dev in ALLOC_DEVICES:
+        mods = allocator_tables(args.seed, dev, candidates_fn=fp.alloc_candidates)
+        combos = 1
+        for m in mods:
+            combos *= len(m)
+        r = fp.plan_allocation(mods, dev)
+        ts = []
+        for _ in range(args.sched_reps):
+            t0 = time.perf_counter()
+            r = fp.plan_allocation(mods, dev)
+            ts.append(time.perf_counter() - t0)
+        row = dict(devices=dev, configs=[len(m) for m in mods], combinations=combos,
+                   ms_median=round(statistics.median(ts) * 1e3, 4), G=r["G"], F=r["F"], devices_used=r["devices"],
+                   choice=r["choice"])
+        if combos <= 300_000:
+            t0 = time.perf_counter()
+            want = solve(mods, dev)
+            row["oracle_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+            row["same_as_oracle"] = (list(want) == [r["choice"], r["G"], r["F"], r["devices"]])
+        rows.append(row)
+        log(f"allocator {dev} devices: {row}")
+    at256 = [x for x in rows if x["devices"] == 256][0]
+    print(json.dumps({
+        "metric": "allocator flow matching (Eq. 2) time per solve",
+        "value": at256["ms_median"], "unit": "ms", "higher_is_better": False,
+        "data": "synthetic throughput surrogates over pruned candidates",
+        "config": {"workload": "allocator", "per_node": 8, "global_batch": 512, "layers": 28, "encoders": 2,
+                   "reps": args.sched_reps, "seed": args.seed},
+        "per_cluster": rows,
+        "cpu_baseline": {"value": at256.get("oracle_ms"), "unit": "ms", "cores": 1, "kind": "oracle",
+                         "sample": "enumeration of every combination at 256 devices, once"},
+    }), flush=True)
+    return 0 if all(x.get("same_as_oracle", True) for x in rows) else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -415,6 +466,8 @@ def main() -> int:
     ap.add_argument("--sched-buckets", type=int, default=4)
     ap.add_argument("--sched-mb-per-rank", type=int, default=8)
     ap.add_argument("--sched-reps", type=int, default=50)
+    ap.add_argument("--allocator", action="store_true",
+                    help="time the allocator's flow matching (Eq. 2) on the host instead of the pack")
     ap.add_argument("--prefetch", action="store_true",
                     help="tiered pool: zero-copy packs vs packs after promoting host-tier pages into HBM")
     ap.add_argument("--concurrent", action="store_true",
@@ -423,6 +476,8 @@ def main() -> int:
 
     if args.scheduler:
         return scheduler_bench(args)
+    if args.allocator:
+        return allocator_bench(args)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this build "
               "(run with --gpus 1)", file=sys.stderr)

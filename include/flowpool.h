@@ -221,6 +221,37 @@ fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, in
                          int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
                          int32_t* out_mb_max_len);
 
+/* Heterogeneous parallel allocator, first step (Sec. 3.3): the pruned
+ * parallelism configurations of one module. Encoders (backbone = 0) use data
+ * and tensor parallelism, DP x TP devices; the backbone (backbone != 0) also
+ * pipeline parallelism, DP x TP x PP devices. Kept: DP divides global_batch,
+ * TP divides per_node (no tensor parallelism across nodes), PP divides
+ * layers (backbone only; PP = 1 for encoders), DP*TP*PP <= devices. Listed in
+ * increasing (DP, TP, PP) order into host int32 out_dp/out_tp/out_pp[cap]
+ * (any may be NULL); *out_n (host) receives the count even when it exceeds
+ * cap (then EINVAL). Host only. Errors: EINVAL. */
+fp_status alloc_candidates(int32_t backbone, int32_t devices, int32_t per_node, int32_t global_batch,
+                           int32_t layers, int32_t* out_dp, int32_t* out_tp, int32_t* out_pp,
+                           int32_t cap, int32_t* out_n);
+
+/* Heterogeneous parallel allocator, flow matching (Eq. 1-2): pick one
+ * configuration per module so that the devices used fit `budget` and
+ * lexmax (G, -F), G = min(T_enc, T_bb), F = |T_enc - T_bb|, T_enc the sum of
+ * the chosen encoder throughputs and T_bb the backbone's. Exact, on integer
+ * throughputs (e.g. tokens/s from profiling); ties go to fewer devices, then
+ * the smallest choice vector.
+ *  n_modules   encoders followed by the backbone (>= 2)
+ *  n_configs   host int32[n_modules], configurations per module (>= 1)
+ *  tau, cost   host int64[sum(n_configs)], module by module: throughput and
+ *              devices of each configuration
+ * Outputs (host, may be NULL): out_choice int32[n_modules] configuration
+ * index per module; out_G, out_F; out_devices (devices used).
+ * Host only. Errors: EINVAL (also more than 2^22 encoder combinations),
+ * ECAPACITY (no choice fits the budget). */
+fp_status plan_allocation(int32_t n_modules, const int32_t* n_configs, const int64_t* tau,
+                          const int64_t* cost, int64_t budget, int32_t* out_choice,
+                          int64_t* out_G, int64_t* out_F, int64_t* out_devices);
+
 /* Dynamic packing scheduler (Alg. 1, Sec. 3.4), host only (no pool, no GPU).
  * Phase 1, best fit: sequences are taken in input order; each goes to the open
  * microbatch whose residual capacity is the smallest that still holds it

@@ -7,7 +7,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libflowpool.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("pool.hip", "kernels.hip", "schedule.cpp")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("pool.hip", "kernels.hip", "schedule.cpp", "allocate.cpp")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

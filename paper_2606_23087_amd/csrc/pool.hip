@@ -23,6 +23,7 @@
 #include "flowpool.h"
 #include "fp_internal.h"
 #include "schedule.h"
+#include "allocate.h"
 
 using fp::SampleDesc;
 
@@ -1037,6 +1038,56 @@ fp_status check_packing_args(int32_t n, int32_t capacity, int32_t n_ranks, int32
 }
 
 }  // namespace
+
+fp_status alloc_candidates(int32_t backbone, int32_t devices, int32_t per_node, int32_t global_batch,
+                           int32_t layers, int32_t* out_dp, int32_t* out_tp, int32_t* out_pp, int32_t cap,
+                           int32_t* out_n) {
+  if (devices < 1 || per_node < 1 || global_batch < 1 || layers < 1 || devices > (1 << 20) ||
+      per_node > 4096 || global_batch > (1 << 24) || layers > 65536)
+    return fail(FP_EINVAL, "devices %d, per_node %d, global_batch %d, layers %d", devices, per_node,
+                global_batch, layers);
+  if (!out_n) return fail(FP_EINVAL, "null out_n");
+  const std::vector<fp::Config> c = fp::prune_candidates(backbone != 0, devices, per_node, global_batch, layers);
+  *out_n = (int32_t)c.size();
+  if ((int64_t)c.size() > cap) return fail(FP_EINVAL, "%zu candidates, room for %d", c.size(), cap);
+  for (size_t i = 0; i < c.size(); ++i) {
+    if (out_dp) out_dp[i] = c[i].dp;
+    if (out_tp) out_tp[i] = c[i].tp;
+    if (out_pp) out_pp[i] = c[i].pp;
+  }
+  return FP_OK;
+}
+
+fp_status plan_allocation(int32_t n_modules, const int32_t* n_configs, const int64_t* tau, const int64_t* cost,
+                          int64_t budget, int32_t* out_choice, int64_t* out_G, int64_t* out_F,
+                          int64_t* out_devices) {
+  if (n_modules < 2 || n_modules > 64) return fail(FP_EINVAL, "n_modules %d (encoders + 1 backbone)", n_modules);
+  if (!n_configs || !tau || !cost) return fail(FP_EINVAL, "null array");
+  if (budget < 0) return fail(FP_EINVAL, "budget %lld", (long long)budget);
+  std::vector<std::vector<int64_t>> t((size_t)n_modules), c((size_t)n_modules);
+  double combos = 1;
+  size_t at = 0;
+  for (int32_t i = 0; i < n_modules; ++i) {
+    if (n_configs[i] < 1) return fail(FP_EINVAL, "module %d has %d configurations", i, n_configs[i]);
+    if (i < n_modules - 1) combos *= n_configs[i];
+    for (int32_t k = 0; k < n_configs[i]; ++k, ++at) {
+      if (tau[at] < 0 || tau[at] > (1ll << 50) || cost[at] < 0 || cost[at] > (1ll << 40))
+        return fail(FP_EINVAL, "module %d configuration %d: tau %lld, cost %lld", i, k, (long long)tau[at],
+                    (long long)cost[at]);
+      t[(size_t)i].push_back(tau[at]);
+      c[(size_t)i].push_back(cost[at]);
+    }
+  }
+  if (combos > (double)(1 << 22)) return fail(FP_EINVAL, "%.0f encoder combinations (at most 2^22)", combos);
+  fp::FlowChoice best;
+  if (!fp::flow_match(t, c, budget, &best))
+    return fail(FP_ECAPACITY, "no choice of configurations fits %lld devices", (long long)budget);
+  if (out_choice) std::copy(best.choice.begin(), best.choice.end(), out_choice);
+  if (out_G) *out_G = best.G;
+  if (out_F) *out_F = best.F;
+  if (out_devices) *out_devices = best.devices;
+  return FP_OK;
+}
 
 fp_status plan_dynamic_packing(const int32_t* lengths, int32_t n, int32_t capacity, int32_t n_ranks,
                                int32_t n_buckets, int32_t* out_mb_of_seq, int32_t* out_n_mb,

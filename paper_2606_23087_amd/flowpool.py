@@ -80,6 +80,9 @@ _SIGS = {
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
     "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
     "pool_migrate": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, _P, _i64p]),
+    "alloc_candidates": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i32p,
+                                     C.c_int32, _i32p]),
+    "plan_allocation": (C.c_int32, [C.c_int32, _i32p, _i64p, _i64p, C.c_int64, _i32p, _i64p, _i64p, _i64p]),
     "plan_dynamic_packing": (C.c_int32, [_i32p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
                                          _i32p, _i32p, _i64p, _i32p, _i32p, _i32p]),
     "plan_pool_packing": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p,
@@ -231,6 +234,35 @@ def _packing_call(fn, name, head, n, capacity, n_ranks, n_buckets):
     out = dict(mb_of_seq=mb_of_seq, n_mb=m)
     out.update({k: a[:m].copy() for k, a in zip(keys, per)})
     return out
+
+
+def alloc_candidates(backbone: bool, devices: int, per_node: int, global_batch: int, layers: int):
+    """Pruned (DP, TP, PP) configurations of one module, as a list of tuples."""
+    n = C.c_int32()
+    st = _lib.alloc_candidates(int(backbone), devices, per_node, global_batch, layers, None, None, None, 0,
+                               C.byref(n))
+    if st != FP_OK and n.value <= 0:
+        _check(st, "alloc_candidates")
+    cap = max(n.value, 1)
+    dp, tp, pp = (np.empty(cap, np.int32) for _ in range(3))
+    _check(_lib.alloc_candidates(int(backbone), devices, per_node, global_batch, layers,
+                                 dp.ctypes.data_as(_i32p), tp.ctypes.data_as(_i32p), pp.ctypes.data_as(_i32p),
+                                 cap, C.byref(n)), "alloc_candidates")
+    return [(int(a), int(b), int(c)) for a, b, c in zip(dp[:n.value], tp[:n.value], pp[:n.value])]
+
+
+def plan_allocation(modules, budget: int):
+    """modules: encoders then the backbone, each a list of (tau, devices).
+    Returns dict(choice, G, F, devices)."""
+    nc = np.array([len(m) for m in modules], np.int32)
+    tau = np.array([t for m in modules for t, _ in m], np.int64)
+    cost = np.array([r for m in modules for _, r in m], np.int64)
+    choice = np.empty(len(modules), np.int32)
+    g, f, d = C.c_int64(), C.c_int64(), C.c_int64()
+    _check(_lib.plan_allocation(len(modules), nc.ctypes.data_as(_i32p), tau.ctypes.data_as(_i64p),
+                                cost.ctypes.data_as(_i64p), budget, choice.ctypes.data_as(_i32p),
+                                C.byref(g), C.byref(f), C.byref(d)), "plan_allocation")
+    return dict(choice=choice.tolist(), G=g.value, F=f.value, devices=d.value)
 
 
 def plan_dynamic_packing(lengths, capacity: int, n_ranks: int, n_buckets: int):

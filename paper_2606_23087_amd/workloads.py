@@ -216,6 +216,31 @@ def schedule_lengths(seed: int, capacity: int, tokens: int, cfg_name: str = "qwe
     return np.array(out, dtype=np.int32)
 
 
+def allocator_tables(seed: int, devices: int, per_node: int = 8, global_batch: int = 512, layers: int = 28,
+                     n_encoders: int = 2, candidates_fn=None):
+    """Stand-in for the allocator's profiled throughput surrogates: for each
+    module (the encoders, then the backbone) a list of (tau, devices) over its
+    candidate configurations. tau (integer tokens/s) grows with data
+    parallelism, sublinearly with tensor parallelism, and with pipeline
+    parallelism less a pipeline bubble, times a seeded +-10 % perturbation.
+    ``candidates_fn(backbone, devices, per_node, global_batch, layers)`` lists
+    the configurations."""
+    rng = np.random.default_rng([seed, 0xA11C])
+    mods = []
+    for m in range(n_encoders + 1):
+        backbone = m == n_encoders
+        base = 9000.0 if backbone else 40000.0 / (m + 1)
+        out = []
+        for dp, tp, pp in candidates_fn(backbone, devices, per_node, global_batch, layers):
+            t = base * dp * tp ** 0.82
+            if backbone:
+                t *= pp ** 0.92 / (1.0 + (pp - 1) / 16.0)
+            t *= 1.0 + 0.1 * (2.0 * rng.random() - 1.0)
+            out.append((int(round(t)), dp * tp * pp))
+        mods.append(out)
+    return mods
+
+
 # ---------------------------------------------------------------- embeddings
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:

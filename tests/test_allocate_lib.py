@@ -1,0 +1,58 @@
+"""The library's allocator (Sec. 3.3, Eq. 1-2) against the oracle, CPU only
+(host code, no GPU needed).
+
+Bar: identical candidate lists, and identical choice, G, F and device count
+(all integers) on seeded random tables and on the synthetic throughput
+surrogates of small clusters; ECAPACITY when nothing fits.
+"""
+
+import numpy as np
+import pytest
+
+from oracle.allocate import candidates, solve
+from paper_2606_23087_amd.workloads import allocator_tables
+
+fp = pytest.importorskip("paper_2606_23087_amd.flowpool")
+
+
+@pytest.mark.parametrize("cluster", [(8, 4, 8, 4), (24, 8, 48, 12), (64, 8, 256, 28), (3, 2, 5, 7)])
+def test_candidates_match(cluster):
+    for bb in (False, True):
+        assert fp.alloc_candidates(bb, *cluster) == candidates(bb, *cluster)
+
+
+def _check(mods, budget):
+    want = solve(mods, budget)
+    if want is None:
+        with pytest.raises(fp.FlowPoolError, match="ECAPACITY"):
+            fp.plan_allocation(mods, budget)
+        return
+    got = fp.plan_allocation(mods, budget)
+    assert (got["choice"], got["G"], got["F"], got["devices"]) == tuple(want)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_tables_match(seed):
+    rng = np.random.default_rng([seed, 77])
+    n_mod = int(rng.integers(2, 5))
+    mods = [[(int(rng.integers(0, 60)), int(rng.integers(1, 8))) for _ in range(int(rng.integers(1, 6)))]
+            for _ in range(n_mod)]
+    for budget in (0, 3, 8, 15, 40):
+        _check(mods, budget)
+
+
+@pytest.mark.parametrize("devices", [16, 32])
+def test_surrogate_tables_match(devices):
+    mods = allocator_tables(devices, devices, per_node=8, global_batch=64, layers=12, n_encoders=2,
+                            candidates_fn=candidates)
+    for budget in (devices // 2, devices):
+        _check(mods, budget)
+
+
+def test_errors():
+    with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+        fp.plan_allocation([[(1, 1)]], 5)
+    with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+        fp.plan_allocation([[(1, 1)], []], 5)
+    with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+        fp.alloc_candidates(True, 0, 8, 8, 8)
