@@ -23,6 +23,15 @@ LIB_PATH = os.path.join(_HERE, "libflowpool.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run paper_2606_23087_amd/build.py first")
 
+# torch (when installed) ships its own HIP and HSA runtimes. Loading torch
+# first lets the library bind to that already-loaded runtime; loaded the
+# other way round, the process ends up with two HSA runtimes, and the second
+# one to start finds no device.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
+
 _lib = C.CDLL(LIB_PATH)
 
 FP_OK, FP_EINVAL, FP_ENOMEM, FP_ENOENT, FP_ECAPACITY, FP_EALIGN, FP_EHIP, FP_ESTATE = 0, -1, -2, -3, -4, -5, -6, -7
