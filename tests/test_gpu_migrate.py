@@ -141,3 +141,41 @@ def test_migration_racing_a_queued_pack(fp):
     finally:
         torch.cuda.synchronize()
         fp.pool_destroy(pool)
+
+
+def test_migration_errors_leave_the_pool_unchanged(fp):
+    say("case migration errors")
+    rng = np.random.default_rng(9)
+    pool = fp.pool_create(hidden=H, page_tokens=P, hbm_pages=6, host_pages=6, vocab=VOCAB, alloc="scatter")
+    contig = fp.pool_create(hidden=H, page_tokens=P, hbm_pages=6, vocab=VOCAB, alloc="contig")
+    try:
+        sp = SampleSpec(rng.integers(0, VOCAB, size=5).astype(np.int32), np.array([2], np.int32),
+                        np.array([4 * P], np.int32))
+        v = to_dev(tagged_vis(0, sp.n_vis, H))
+        torch.cuda.synchronize()
+        a = fp.pool_write_sample(pool, sp.text_ids, sp.img_pos, sp.img_ntok, v, np.ones(4, np.uint8))
+        b = fp.pool_write_sample(pool, sp.text_ids, sp.img_pos, sp.img_ntok, v, np.zeros(4, np.uint8))
+        c = fp.pool_write_sample(contig, sp.text_ids, sp.img_pos, sp.img_ntok, v)
+        torch.cuda.synchronize()
+        before = (fp.pool_sample_pages(pool, a).tolist(), fp.pool_sample_pages(pool, b).tolist(), fp.pool_stats(pool))
+        cases = [
+            (lambda: fp.pool_migrate(contig, [c], fp.FP_TIER_HOST), "EINVAL"),     # contig pools do not migrate
+            (lambda: fp.pool_migrate(pool, [a], 7), "EINVAL"),                     # no such tier
+            (lambda: fp.pool_migrate(pool, [a, a], fp.FP_TIER_HBM), "EINVAL"),     # listed twice
+            (lambda: fp.pool_migrate(pool, [a, 999], fp.FP_TIER_HBM), "ENOENT"),
+            (lambda: fp.pool_migrate(pool, [a], fp.FP_TIER_HBM), "ENOMEM"),         # 4 pages, 2 free in HBM
+        ]
+        for call, code in cases:
+            with pytest.raises(fp.FlowPoolError, match=code):
+                call()
+        assert (fp.pool_sample_pages(pool, a).tolist(), fp.pool_sample_pages(pool, b).tolist(),
+                fp.pool_stats(pool)) == before
+        assert fp.pool_migrate(pool, [b], fp.FP_TIER_HBM) == 0                   # already there
+        with pytest.raises(fp.FlowPoolError, match="ENOENT"):
+            fp.plan_pool_packing(pool, [a, 12345], 1000, 2, 2)
+        with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+            fp.plan_pool_packing(pool, [a], 10, 2, 2)                            # longer than the capacity
+    finally:
+        torch.cuda.synchronize()
+        fp.pool_destroy(pool)
+        fp.pool_destroy(contig)

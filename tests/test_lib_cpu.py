@@ -75,3 +75,24 @@ def test_pool_create_rejects_bad_config_without_gpu():
         with pytest.raises(fp.FlowPoolError) as e:
             fp.pool_create(**args)
         assert e.value.code == "EINVAL"
+
+
+def test_null_pool_is_rejected_by_every_pool_call():
+    """Every call taking a pool answers EINVAL for a null pool (no device use)."""
+    lib = ctypes.CDLL(fp.LIB_PATH)
+    n = ctypes.c_int64()
+    assert lib.pool_reclaim(None, 0, ctypes.byref(n)) == fp.FP_EINVAL
+    assert lib.pool_migrate(None, None, 0, 0, None, None) == fp.FP_EINVAL
+    assert lib.plan_pool_packing(None, None, 0, 10, 1, 1, None, None, None, None, None, None, None,
+                                 None) == fp.FP_EINVAL
+    assert lib.pool_free_sample(None, ctypes.c_uint64(1)) == fp.FP_EINVAL
+    assert lib.pack_microbatch(None, None, 0, None, ctypes.c_int64(0), None, ctypes.c_int64(0), None, None,
+                               None, None, 3, None) == fp.FP_EINVAL
+    assert "null" in fp.fp_last_error()
+    assert fp.pool_destroy(0) is None                          # NULL is accepted
+
+
+def test_pool_create_rejects_gva_span_beyond_2_52():
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.pool_create(hidden=1 << 20, page_tokens=1 << 20, hbm_pages=1 << 20)
+    assert e.value.code == "EINVAL"
