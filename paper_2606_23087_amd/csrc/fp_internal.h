@@ -39,7 +39,7 @@ constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per 
 constexpr int kInlineSamples = 64;   // sample headers passed by value to k_pack
 constexpr int kInlineImages = 128;   // image pairs passed by value to k_pack
 constexpr int kImgGroup = 8;       // image pairs read per scalar load group in k_pack
-constexpr int kLenGroup = 16;      // sample lengths read per scalar load group in k_pack
+constexpr int kLenGroup = 8;       // sample lengths read per scalar load group in k_pack
 constexpr int kWaveRows = 16;      // rows per wave resolved with scalar loads in k_pack
 static_assert(kInlineSamples % kLenGroup == 0, "length groups tile the inline headers");
 constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds k_pack's LDS use)

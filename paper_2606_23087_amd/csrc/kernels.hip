@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
       // Sample k holding the row: running sum of the lengths, a group of
-      // sixteen per scalar load.
+      // kLenGroup per scalar load (a short group ends the search sooner).
       int k = -1, start = 0;
       for (int b = 0; k < 0 && b < kInlineSamples; b += kLenGroup) {
         u32x4 g[kLenGroup / 4];
