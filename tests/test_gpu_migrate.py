@@ -83,7 +83,7 @@ def test_migration_matches_oracle(fp):
         for rnd in range(6):
             pick = sorted(set(int(i) for i in rng.integers(0, len(gids), size=3)))
             tier = rnd % 2
-            say(f"  round {rnd}: samples {pick} -> tier {tier}")
+            say(f"  step {rnd}: samples {pick} -> tier {tier}")
             need = sum(1 for i in pick for g in orc.sample_pages(oids[i]) if orc.translate(g)[0] != tier)
             if need <= len(orc.stack[tier]):
                 want = sum(orc.migrate(oids[i], tier) for i in pick)
