@@ -936,7 +936,11 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
     r.page_off = pl_off[j];
     r.pages = std::move(new_pages[j]);
     fp_status ms = mark_readers(p, r.readers, &d.events);
-    if (ms != FP_OK && st == FP_OK) st = ms;
+    if (ms != FP_OK) {
+      // Without an event on every reader, wait for the whole device instead.
+      (void)hipDeviceSynchronize();
+      if (st == FP_OK) st = ms;
+    }
     p->events.ref(ev);
     d.events.push_back(ev);
     if (r.written >= 0) p->events.unref(r.written);
