@@ -470,6 +470,8 @@ def main() -> int:
                     help="time the allocator's flow matching (Eq. 2) on the host instead of the pack")
     ap.add_argument("--prefetch", action="store_true",
                     help="tiered pool: zero-copy packs vs packs after promoting host-tier pages into HBM")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time one step's packs captured into a HIP graph and replayed")
     ap.add_argument("--concurrent", action="store_true",
                     help="time the packs alone and under a concurrent producer on another stream")
     args = ap.parse_args()
@@ -588,6 +590,29 @@ def main() -> int:
     torch.cuda.synchronize()
     durs = np.array([s_.elapsed_time(e_) * 1e-3 for s_, e_ in events])   # seconds
 
+    graph_s = None
+    if args.graph:
+        # One step's packs captured into a HIP graph and replayed: no host
+        # work per pack (matters when the packs are small and host-bound).
+        fp.pool_reclaim(w.pool, True)
+        gouts = [w.alloc_outputs() for _ in range(len(mbs))]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(pack_stream):
+            with torch.cuda.graph(g, stream=pack_stream):
+                for mb, (o, c, q) in zip(mbs, gouts):
+                    w.pack(mb, o, c, q, stream=pack_stream)
+        g.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(pack_stream)
+        with torch.cuda.stream(pack_stream):
+            for _ in range(args.steps):
+                g.replay()
+        g1.record(pack_stream)
+        torch.cuda.synchronize()
+        graph_s = g0.elapsed_time(g1) * 1e-3 / args.steps
+        del g, gouts
+
     value = step_bytes * args.steps / wall / 1e9
     kernel_gbps = float(mb_bytes.mean()) / launch_s / 1e9
     per_call = mb_bytes / durs / 1e9
@@ -626,6 +651,10 @@ def main() -> int:
                      "traffic": (round(traffic) if traffic else None),
                      "traffic_over_algorithmic": (round(traffic / mean_bytes, 4) if traffic else None)},
     }
+    if graph_s is not None:
+        result["graph_pack"] = {"packs_per_replay": n_packs, "replay_ms": round(graph_s * 1e3, 4),
+                                "GBps": round(step_bytes / graph_s / 1e9, 2),
+                                "per_call_GBps_same_packs": round(step_bytes / (launch_s * n_packs) / 1e9, 2)}
     imb = plan["mb_cost_scaled"].max() / plan["mb_cost_scaled"].mean()
     result["plan"] = {"max_over_mean_cost": round(float(imb), 5),
                       "eq3_max": round(float(max((t / cfg.capacity) + (m / cfg.capacity) ** 2

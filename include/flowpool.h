@@ -33,6 +33,15 @@
  *    preserved exactly).
  *  - Calls from several threads are serialised internally by a mutex, so a
  *    producer thread and a consumer thread may share one pool.
+ *  - HIP graphs: pack_microbatch may be captured on a capturing stream when
+ *    its headers travel in the kernel arguments (at most 64 samples and 128
+ *    images) and its samples' writes are known complete (a pack, plan or
+ *    pool_reclaim after they finished has seen them; the capture makes no
+ *    event queries); each replay packs the same samples into the same
+ *    buffers. The samples must stay resident
+ *    while the graph may be replayed. pool_write_sample, pool_migrate and
+ *    plan_microbatches return ESTATE on a capturing stream, as does a pack
+ *    that cannot be captured.
  */
 #ifndef FLOWPOOL_H
 #define FLOWPOOL_H
@@ -166,8 +175,9 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
 fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
 
 /* Returns the resources of deferred frees whose packs have completed (with
- * wait != 0, first waits for all of them). *out_deferred_pages (host, may be
- * NULL) receives the pages still deferred. pool_write_sample reclaims by
+ * wait != 0, first waits for all of them), and forgets the events of writes
+ * that have completed (all of them with wait != 0). *out_deferred_pages
+ * (host, may be NULL) receives the pages still deferred. pool_write_sample reclaims by
  * itself and, when memory runs short, waits for the packs holding deferred
  * pages. Errors: EHIP. */
 fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages);

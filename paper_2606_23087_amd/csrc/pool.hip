@@ -416,6 +416,16 @@ fp_status order_after_writes(fp_pool* p, const std::vector<SampleRec*>& recs, hi
   return FP_OK;
 }
 
+// True while `stream` is being captured into a HIP graph.
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return cs != hipStreamCaptureStatusNone;
+}
+
 fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
                  int32_t n_mb, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
                  int32_t* mb_max) {
@@ -624,6 +634,8 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   }
   DeviceGuard guard(p->cfg.device);
   if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  if (capturing((hipStream_t)stream))
+    return fail(FP_ESTATE, "pool_write_sample cannot be captured into a graph (its staging buffers are reused)");
   const uint8_t* vis_dev = nullptr;
   if (vis_emb && n_vis > 0) {
     if ((uintptr_t)vis_emb % 16) return fail(FP_EALIGN, "vis_emb must be 16-byte aligned");
@@ -775,6 +787,16 @@ fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
   DeviceGuard guard(p->cfg.device);
   if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
   reclaim(p, wait != 0);
+  // Forget the write events that have completed (or, with wait, all of them).
+  for (auto& kv : p->samples) {
+    SampleRec& r = kv.second;
+    if (r.written < 0) continue;
+    if (wait) (void)hipEventSynchronize(p->events.ev[(size_t)r.written]);
+    if (p->events.done(r.written)) {
+      p->events.unref(r.written);
+      r.written = -1;
+    }
+  }
   if (out_deferred_pages) *out_deferred_pages = p->deferred_pages;
   return FP_OK;
 }
@@ -830,6 +852,10 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
     reclaim(p, true);
   }
   hipStream_t hs = (hipStream_t)stream;
+  if (capturing(hs)) {
+    unreserve();
+    return fail(FP_ESTATE, "pool_migrate cannot be captured into a graph (it moves pages now)");
+  }
   fp_status st = order_after_writes(p, recs, hs);   // the copies read what the writes wrote
   if (st != FP_OK) {
     unreserve();
@@ -993,6 +1019,7 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
     DeviceGuard guard(p->cfg.device);
     if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
     hipStream_t hs = (hipStream_t)stream;
+    if (capturing(hs)) return fail(FP_ESTATE, "plan_microbatches waits for its result and cannot be captured");
     const size_t slot_bytes = align16(4ll * n);
     Stage* s = nullptr;
     fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, slot_bytes + 8 * (size_t)n, &s);
@@ -1215,6 +1242,18 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
     a.pb_shift = sh - 64;
   }
   const bool staged = n > fp::kInlineSamples || n_imgs > fp::kInlineImages;
+  if (capturing(hs)) {
+    // A captured pack is one kernel whose arguments hold the whole
+    // microbatch, so a replay packs the same samples again.
+    if (staged)
+      return fail(FP_ESTATE, "a pack of more than %d samples or %d images cannot be captured into a graph",
+                  fp::kInlineSamples, fp::kInlineImages);
+    // No event queries during capture: the writes must already be known complete.
+    for (SampleRec* r : recs)
+      if (r->written >= 0)
+        return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
+                               "before capturing its pack");
+  }
   std::vector<fp::PackSample> big_s;
   std::vector<int2> big_i;
   fp::PackSample* smp = a.samples;
