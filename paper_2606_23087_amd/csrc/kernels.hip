@@ -145,8 +145,8 @@ __device__ __forceinline__ int div_vpr(const PackArgs& a, int e) {
 //
 // Headers passed by value and at most kWaveRows rows per wave (the usual
 // case): each row is resolved by one wave with scalar loads, so the only
-// vector memory operations are the copies. Otherwise the headers are staged
-// in LDS and scanned there.
+// vector memory loads are the copies. Otherwise the headers are staged in
+// LDS and scanned there.
 __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   extern __shared__ __align__(16) uint8_t s_dyn[];
   __shared__ int32_t s_wsum[kPackBlock / 64];
