@@ -34,8 +34,10 @@
  *  - Calls from several threads are serialised internally by a mutex, so a
  *    producer thread and a consumer thread may share one pool.
  *  - HIP graphs: pack_microbatch may be captured on a capturing stream when
- *    its headers travel in the kernel arguments (at most 64 samples and 128
- *    images) and its samples' writes are known complete (a pack, plan or
+ *    its row table travels in the kernel arguments (at most 64 samples whose
+ *    rows form at most 160 runs, a run being a stretch of one sample's text
+ *    rows, or of its image rows with no text row between them) and its
+ *    samples' writes are known complete (a pack, plan or
  *    pool_reclaim after they finished has seen them; the capture makes no
  *    event queries); each replay packs the same samples into the same
  *    buffers. The samples must stay resident
@@ -92,7 +94,7 @@ enum { FP_TIER_MASK_HBM = 1, FP_TIER_MASK_HOST = 2, FP_TIER_MASK_ALL = 3 };
  *  world_size, rank   must be 1 and 0 in this library (single process).
  *  max_samples   resident sample slots; 0 = 65536.
  *  meta_bytes    device metadata arena (text ids, image positions, page
- *                lists); 0 = 64 MiB.
+ *                lists); 0 = 64 MiB, at most 8 GiB.
  *  frame_shuffle_seed  0 = physical frames bound to GVA pages in order; else
  *                a seeded permutation of frames (placement-independence tests).
  *  chunk_bytes   the library allocates tier backing in chunks of this many

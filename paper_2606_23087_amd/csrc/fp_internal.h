@@ -36,31 +36,37 @@ constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
 constexpr int kPackBlock = 256;      // threads per k_pack workgroup
 constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves (12 KiB chunks)
 constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
-constexpr int kInlineSamples = 64;   // sample headers passed by value to k_pack
-constexpr int kInlineImages = 128;   // image pairs passed by value to k_pack
-constexpr int kImgGroup = 8;       // image pairs read per scalar load group in k_pack
-constexpr int kLenGroup = 8;       // sample lengths read per scalar load group in k_pack
-constexpr int kWaveRows = 16;      // rows per wave resolved with scalar loads in k_pack
-static_assert(kInlineSamples % kLenGroup == 0, "length groups tile the inline headers");
-constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds k_pack's LDS use)
+constexpr int kInlineSamples = 64;   // sample lengths passed by value to k_pack
+constexpr int kInlineRuns = 160;     // runs passed by value to k_pack
+constexpr int kBuckets = 256;        // row buckets of the run index
+constexpr int kWaveRows = 16;        // rows per wave resolved with scalar loads in k_pack
+constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds the staged run table)
 constexpr int kMaxPackImages = 1024;
 
-// Per-sample header of a microbatch, taken from the pool's host mirror of
-// the sample metadata (the variable-length parts stay in device memory).
-struct alignas(16) PackSample {
-  int32_t len;        // rows = text + visual
-  int32_t n_img;
-  int32_t img_base;   // index of the sample's first (position, rows) pair
-  int32_t n_text;
-  int64_t text_off;   // metadata-arena byte offset of the text ids
-  int64_t page_off;   // metadata-arena byte offset of the page GVAs
+// A run is a maximal stretch of packed rows of one sample that come from one
+// place: text rows (ids read from the sample's text list) or image rows (the
+// images between two text rows, which are consecutive in the sample's page
+// list). The host lists a microbatch's runs in row order, so resolving a row
+// is finding its run and one or two indexed loads. Metadata-arena offsets are
+// kept as word indexes, so the arena is limited to kMaxMetaBytes.
+struct alignas(16) PackRun {
+  int32_t end;        // one past the run's last row
+  int32_t head;       // first row of the run's sample; bit 31 set for a text run
+  int32_t vdelta;     // image run: visual index of row r is r + vdelta
+  int32_t word;       // text run: the id of row r is 32-bit word word + r of the
+                      // arena; image run: the sample's page GVAs start at
+                      // 64-bit word `word`
 };
-static_assert(sizeof(PackSample) == 32, "PackSample layout");
+static_assert(sizeof(PackRun) == 16, "PackRun layout");
+constexpr int32_t kTextRun = INT32_MIN;
+constexpr int64_t kMaxMetaBytes = 1ll << 33;
 
-// Everything one pack launch needs, passed by value. Kernel arguments are
-// captured at launch, so microbatches of up to kInlineSamples samples and
-// kInlineImages images need no staging copy; larger ones point at a staged
-// device copy of the same arrays.
+// Everything one pack launch needs, passed by value. The run table (sample
+// lengths, runs, bucket index) follows the scalar fields; kernel arguments are
+// captured at launch, so a microbatch of up to kInlineSamples samples and
+// kInlineRuns runs needs no staging copy. A larger one points `staged` at a
+// device copy of the table laid out at the given offsets. bucket[b] is the
+// last run starting at or before row b << bucket_shift.
 struct PackArgs {
   const uint8_t* meta;        // device metadata arena
   const uint64_t* pte;        // device page table, index = (gva - gva_start) / page_bytes
@@ -70,25 +76,28 @@ struct PackArgs {
   uint8_t* out;               // packed rows
   int32_t* cu;                // cu_seqlens or null
   int32_t* pos;               // position ids or null
-  const PackSample* samples_dev;   // staged headers, or null = samples[]
-  const int2* imgs_dev;            // staged image pairs, or null = imgs[]
+  const uint8_t* staged;      // staged run table, or null = the arrays below
+  int32_t off_runs;           // byte offsets of the arrays from the table's start
+  int32_t off_bucket;
   int32_t n;                  // samples
-  int32_t n_imgs;             // image pairs
+  int32_t n_runs;
   int32_t n_tokens;           // total rows
   int32_t row_bytes;
   int32_t page_tokens;
   int32_t tier_mask;
   int32_t max_chunk_rows;     // rows one chunk can touch
+  int32_t bucket_shift;
   uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
-  int32_t div_shift;
-  int32_t pt_shift;           // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
-  uint64_t pt_mul;
+  uint64_t pt_mul;            // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
   uint64_t pb_mul;            // d / page_bytes == umulhi64(d, pb_mul) >> pb_shift for d < 2^52
+  int32_t div_shift;
+  int32_t pt_shift;
   int32_t pb_shift;
-  alignas(16) int32_t lens[kInlineSamples];   // sample lengths, zero past n
-  PackSample samples[kInlineSamples];
-  int2 imgs[kInlineImages + kImgGroup];       // zero past n_imgs, so a group may overrun
+  alignas(16) int32_t lens[kInlineSamples];   // sample lengths (rows), in pack order
+  alignas(16) PackRun runs[kInlineRuns];
+  uint16_t bucket[kBuckets];
 };
+static_assert(sizeof(PackArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
 struct WriteArgs {
   SampleDesc desc;            // descriptor to publish into the table

@@ -1,11 +1,12 @@
 // HIP kernels of libflowpool for gfx950 (CDNA4).
 //
 // k_pack  : the consumer's translate-gather-pack of one microbatch
-//           (paper Sec. 3.1 / Sec. 3.2): prefix sum of sample lengths ->
-//           cu_seqlens; per row, the sample and its text/image segment; for
-//           image rows the GVA page walk through the page table; then 16-byte
-//           vector copies of every row from its page or embedding-table row
-//           into the packed output, plus position ids.
+//           (paper Sec. 3.1 / Sec. 3.2): per row, its run (a stretch of one
+//           sample's text rows or image rows, listed by the host in row
+//           order); for image rows the GVA page walk through the page table;
+//           then 16-byte vector copies of every row from its page or
+//           embedding-table row into the packed output; cu_seqlens as a
+//           wave-wide prefix sum of the sample lengths, and position ids.
 // k_write : the producer's write of one sample's image rows into its pages,
 //           through the same page table (Sec. 3.2, producer side), and
 //           publication of the sample descriptor.
@@ -36,130 +37,93 @@ __device__ __forceinline__ void store16(uint8_t* p, u32x4 v) {
   asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" : : "v"(p), "v"(v) : "memory");
 }
 
-template <typename T>
-__device__ __forceinline__ T ld_global(const T* p) {
-  return *(const __attribute__((address_space(1))) T*)p;
-}
-
-__device__ __forceinline__ PackSample ld_sample(const PackSample* p) {
-  const g_u32x4_c* q = (const g_u32x4_c*)p;
-  const u32x4 lo = q[0], hi = q[1];
-  PackSample s;
-  __builtin_memcpy(&s, &lo, 16);
-  __builtin_memcpy(reinterpret_cast<uint8_t*>(&s) + 16, &hi, 16);
-  return s;
-}
-
-__device__ __forceinline__ int2 ld_pair(const int2* p) {
-  const uint64_t v = ld_global(reinterpret_cast<const uint64_t*>(p));
-  int2 r;
-  r.x = (int)(uint32_t)v;
-  r.y = (int)(uint32_t)(v >> 32);
-  return r;
-}
-
-// Block-wide exclusive prefix sum of len[0..n) into cu[0..n] (cu[0] = 0).
-__device__ __forceinline__ void block_scan_lengths(const PackSample* smp, int n, int32_t* cu,
-                                                   int32_t* wsum) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) cu[0] = 0;
-  int carry = 0;
-  for (int base = 0; base < n; base += kPackBlock) {
-    const int i = base + tid;
-    int v = (i < n) ? smp[i].len : 0;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int t = __shfl_up(v, d, 64);
-      if (lane >= d) v += t;
-    }
-    if (lane == 63) wsum[wave] = v;
-    __syncthreads();
-    int before = 0, all = 0;
-#pragma unroll
-    for (int w = 0; w < kPackBlock / 64; ++w) {
-      before += (w < wave) ? wsum[w] : 0;
-      all += wsum[w];
-    }
-    if (i < n) cu[i + 1] = carry + before + v;
-    carry += all;
-    __syncthreads();
-  }
-}
-
-// Index of the sample holding packed row `row`: last k with cu[k] <= row.
-__device__ __forceinline__ int sample_of(const int32_t* cu, int n, int row) {
-  int lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (cu[mid] <= row) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
-// Source address of row r of sample sp (null if the tier mask skips it).
-__device__ __forceinline__ const uint8_t* resolve_row(const PackArgs& a, const PackSample& sp,
-                                                      const int2* img, int r) {
-  // Image j of the sample starts after img.x of its text rows and all rows
-  // of the images before it; text rows fill the gaps.
-  int vis_before = 0, vis_idx = -1;
-  for (int j = 0; j < sp.n_img; ++j) {
-    const int2 pr = img[sp.img_base + j];
-    const int start = pr.x + vis_before;
-    if (r < start) break;
-    if (r < start + pr.y) { vis_idx = vis_before + (r - start); break; }
-    vis_before += pr.y;
-  }
-  if (vis_idx < 0) {
-    if (!(a.tier_mask & 1)) return nullptr;
-    const int32_t id = ld_global(reinterpret_cast<const int32_t*>(a.meta + sp.text_off) + (r - vis_before));
-    return a.table + (size_t)id * a.row_bytes;
-  }
-  // Page walk: visual row -> page GVA -> page-table entry -> physical row.
-  const int lp = vis_idx / a.page_tokens;
-  const int off = vis_idx - lp * a.page_tokens;
-  const uint64_t gva = ld_global(reinterpret_cast<const uint64_t*>(a.meta + sp.page_off) + lp);
-  const uint64_t pte = ld_global(a.pte + (gva - a.gva_start) / a.page_bytes);
-  if (!(a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))) return nullptr;
-  return reinterpret_cast<const uint8_t*>(pte & PTE_ADDR_MASK) + (size_t)off * a.row_bytes;
-}
-
 // Reads through constant-address-space views of uniform addresses compile to
 // scalar loads (scalar cache), which do not queue behind the vector memory
-// traffic of the copies.
-typedef __attribute__((address_space(4))) const int32_t k_i32;
-typedef __attribute__((address_space(4))) const int64_t k_i64;
-typedef __attribute__((address_space(4))) const uint64_t k_u64;
-typedef __attribute__((address_space(4))) const u32x4 k_u32x4;
+// traffic of the copies; the per-lane path reads through global views.
+// Loads for the two ways rows are resolved: kScalar (one row per wave,
+// wave-uniform addresses) or per lane.
+template <bool kScalar, typename T>
+__device__ __forceinline__ T ld(const void* p) {
+  if constexpr (kScalar) {
+    return *(const __attribute__((address_space(4))) T*)p;
+  } else {
+    return *(const __attribute__((address_space(1))) T*)p;
+  }
+}
 
 // e / (row_bytes / 16) as a multiply and a shift (host-computed constants).
 __device__ __forceinline__ int div_vpr(const PackArgs& a, int e) {
   return (int)(((uint64_t)(uint32_t)e * a.div_mul) >> a.div_shift);
 }
 
+// One run, as a single 16-byte load.
+template <bool kScalar>
+__device__ __forceinline__ PackRun ld_run(const PackRun* rp) {
+  const u32x4 d = ld<kScalar, u32x4>(rp);
+  return PackRun{(int32_t)d.x, (int32_t)d.y, (int32_t)d.z, (int32_t)d.w};
+}
+
+// Run holding packed row `row`: the bucket of the row names a run starting
+// at or before it; runs that end at or before the row are stepped over.
+template <bool kScalar>
+__device__ __forceinline__ PackRun run_of(const PackArgs& a, const uint8_t* tb, int row, int* s_out = nullptr) {
+  const int b = row >> a.bucket_shift;
+  const uint32_t w = ld<kScalar, uint32_t>(tb + a.off_bucket + 4 * (b >> 1));
+  int s = (int)((b & 1) ? (w >> 16) : (w & 0xffffu));
+  const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
+  PackRun r = ld_run<kScalar>(runs + s);
+  while (r.end <= row) r = ld_run<kScalar>(runs + ++s);
+  if (s_out) *s_out = s;
+  return r;
+}
+
+// Source address of packed row `row` of run r, or 0 when the tier mask
+// leaves the row out. A text row's id selects an embedding-table row; an
+// image row walks the page table: visual index -> page GVA (the sample's page
+// list) -> page-table entry (the GVA's page number) -> row in the physical page.
+template <bool kScalar>
+__device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun& run, int row) {
+  if (run.head < 0) {
+    if (!(a.tier_mask & 1)) return 0;
+    const int32_t id = ld<kScalar, int32_t>(a.meta + 4 * ((int64_t)run.word + row));
+    return reinterpret_cast<uint64_t>(a.table) + (uint64_t)(uint32_t)id * (uint64_t)a.row_bytes;
+  }
+  const uint32_t vidx = (uint32_t)(row + run.vdelta);
+  const int lp = (int)(((uint64_t)vidx * a.pt_mul) >> a.pt_shift);
+  const int in_page = (int)vidx - lp * a.page_tokens;
+  const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)run.word + lp));
+  const uint64_t vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
+  const uint64_t pte = ld<kScalar, uint64_t>(a.pte + vpn);
+  if (!(a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))) return 0;
+  return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
+}
+
 // One workgroup packs one chunk of kChunkVecs 16-byte vectors of the output
 // (rows are contiguous in the output, so a chunk is a contiguous byte range
-// that may start and end inside rows): it finds, for every row the chunk
-// touches, the row's sample (prefix sum of sample lengths) and segment, walks
-// the page table for image rows, and then moves kVecsPerThread vectors per
-// thread with all loads in flight before the stores.
+// that may start and end inside rows): it resolves the source of every row
+// the chunk touches, then moves kVecsPerThread vectors per thread with all
+// loads in flight before the stores.
 //
-// Headers passed by value and at most kWaveRows rows per wave (the usual
-// case): each row is resolved by one wave with scalar loads, so the only
-// vector memory loads are the copies. Otherwise the headers are staged in
-// LDS and scanned there.
+// Up to kWaveRows rows per wave (the usual case: a chunk touches two or three
+// rows at realistic hidden sizes), each row is resolved by one wave with
+// scalar loads, so the only vector memory loads are the copies. Chunks of
+// many short rows resolve one row per lane.
 __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
-  extern __shared__ __align__(16) uint8_t s_dyn[];
-  __shared__ int32_t s_wsum[kPackBlock / 64];
+  extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
-  PackSample* s_smp = reinterpret_cast<PackSample*>(s_dyn);
-  int2* s_img = reinterpret_cast<int2*>(s_smp + a.n);
-  uint64_t* s_src = reinterpret_cast<uint64_t*>(s_img + a.n_imgs);
-  int32_t* s_cu = reinterpret_cast<int32_t*>(s_src + a.max_chunk_rows);
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  // Every kernel argument the row resolution uses, read in one batch of
+  // scalar loads instead of in several batches on the way.
+  asm volatile("" : : "s"(a.staged), "s"(a.off_runs), "s"(a.off_bucket), "s"(a.bucket_shift),
+               "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start), "s"(a.pt_mul),
+               "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
+               "s"(a.tier_mask), "s"(a.row_bytes), "s"(a.n_tokens), "s"(a.div_mul),
+               "s"(a.div_shift));
+  const uint8_t* tb = a.staged ? a.staged : reinterpret_cast<const uint8_t*>(a.lens);
   int my_skip = 0;                                  // a row of this chunk is not copied
 
   const bool write_meta = (a.tier_mask & 1) != 0;
-  const bool write_cu = blockIdx.x == 0 && a.cu && write_meta;
   const int vpr = a.row_bytes >> 4;
   const int total = a.n_tokens * vpr;                 // the host keeps this below 2^31
   const int v0 = blockIdx.x * kChunkVecs;
@@ -167,119 +131,29 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   const int r0 = div_vpr(a, v0);
   const int rows = v1 > v0 ? div_vpr(a, v1 - 1) - r0 + 1 : 0;
 
-  if (!a.samples_dev && rows <= kWaveRows * (kPackBlock / 64)) {
-    // Each wave resolves rows wave, wave + 4, ... of the chunk on its own,
-    // so the dependent load chains of different rows overlap. All of it is
-    // wave-uniform and runs on scalar loads.
-    const int lane = tid & 63;
+  if (rows <= kWaveRows * (kPackBlock / 64)) {
+    // Wave w resolves rows w, w + 4, ... of the chunk, so the dependent load
+    // chains of different rows overlap.
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (write_cu && tid == kPackBlock - 1) {
-      int start = 0;
-      for (int i = 0; i < a.n; ++i) {
-        a.cu[i] = start;
-        start += *(const k_i32*)(a.lens + i);
-      }
-      a.cu[a.n] = start;
-    }
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
-      // Sample k holding the row: running sum of the lengths, a group of
-      // kLenGroup per scalar load (a short group ends the search sooner).
-      int k = -1, start = 0;
-      for (int b = 0; k < 0 && b < kInlineSamples; b += kLenGroup) {
-        u32x4 g[kLenGroup / 4];
-#pragma unroll
-        for (int q = 0; q < kLenGroup / 4; ++q) g[q] = ((const k_u32x4*)(a.lens + b))[q];
-#pragma unroll
-        for (int q = 0; q < kLenGroup; ++q) {
-          const int len = (int)g[q >> 2][q & 3];
-          if (k < 0) {
-            if (row < start + len) k = b + q;
-            else start += len;
-          }
-        }
-      }
-      uint64_t src = 0;
-      const int r = row - start;
-      if (k >= 0) {
-        const u32x4 h0 = ((const k_u32x4*)(a.samples + k))[0];
-        const u32x4 h1 = ((const k_u32x4*)(a.samples + k))[1];
-        const int n_img = (int)h0.y, img_base = (int)h0.z;
-        const int64_t text_off = (int64_t)(((uint64_t)h1.y << 32) | h1.x);
-        const int64_t page_off = (int64_t)(((uint64_t)h1.w << 32) | h1.z);
-        // Segment of row r: image j starts after pos_j of the sample's text
-        // rows and all rows of the images before it; text rows fill the gaps.
-        int vis_before = 0, vidx = -1;
-        bool done = false;
-        for (int jb = 0; jb < n_img && !done; jb += kImgGroup) {
-          const k_i32* pr = (const k_i32*)(a.imgs + img_base + jb);
-          int pos_j[kImgGroup], ntok_j[kImgGroup];
-#pragma unroll
-          for (int j = 0; j < kImgGroup; ++j) {
-            pos_j[j] = pr[2 * j];
-            ntok_j[j] = pr[2 * j + 1];
-          }
-#pragma unroll
-          for (int j = 0; j < kImgGroup; ++j) {
-            if (!done && jb + j < n_img) {
-              const int s0 = pos_j[j] + vis_before;
-              if (r < s0) {
-                done = true;
-              } else if (r < s0 + ntok_j[j]) {
-                vidx = vis_before + (r - s0);
-                done = true;
-              } else {
-                vis_before += ntok_j[j];
-              }
-            }
-          }
-        }
-        if (vidx < 0) {
-          // Text row: its token id selects the embedding-table row.
-          if (a.tier_mask & 1) {
-            const int32_t id = *(const k_i32*)(a.meta + text_off + 4 * (int64_t)(r - vis_before));
-            src = reinterpret_cast<uint64_t>(a.table) + (uint64_t)(uint32_t)id * (uint64_t)a.row_bytes;
-          }
-        } else {
-          // Image row: page GVA from the sample's page list, page-table entry
-          // from the GVA's page number, row inside the physical page.
-          const int lp = (int)(((uint64_t)(uint32_t)vidx * a.pt_mul) >> a.pt_shift);
-          const int off = vidx - lp * a.page_tokens;
-          const uint64_t gva = *(const k_u64*)(a.meta + page_off + 8 * (int64_t)lp);
-          const uint64_t vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
-          const uint64_t pte = *(const k_u64*)(a.pte + vpn);
-          if (a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))
-            src = (pte & PTE_ADDR_MASK) + (uint64_t)off * (uint64_t)a.row_bytes;
-        }
-      }
+      const uint64_t src = row_source<true>(a, run_of<true>(a, tb, row), row);
       if (lane == 0) {
         s_src[t] = src;
         if (!src) my_skip = 1;
       }
     }
   } else {
-    const PackSample* gs = a.samples_dev ? a.samples_dev : a.samples;
-    const int2* gi = a.imgs_dev ? a.imgs_dev : a.imgs;
-    for (int i = tid; i < a.n; i += kPackBlock) s_smp[i] = ld_sample(gs + i);
-    for (int i = tid; i < a.n_imgs; i += kPackBlock) s_img[i] = ld_pair(gi + i);
-    __syncthreads();
-    block_scan_lengths(s_smp, a.n, s_cu, s_wsum);
-    if (write_cu) {
-      for (int i = tid; i <= a.n; i += kPackBlock) a.cu[i] = s_cu[i];
-    }
     for (int t = tid; t < rows; t += kPackBlock) {
       const int row = r0 + t;
-      const int k = sample_of(s_cu, a.n, row);
-      const int r = row - s_cu[k];
-      const uint8_t* src = resolve_row(a, s_smp[k], s_img, r);
-      s_src[t] = reinterpret_cast<uint64_t>(src);
+      const uint64_t src = row_source<false>(a, run_of<false>(a, tb, row), row);
+      s_src[t] = src;
       if (!src) my_skip = 1;
-      if (a.samples_dev && a.pos && write_meta && row * vpr >= v0) a.pos[row] = r;
     }
   }
   // One flag per wave, written before and read after the only barrier.
   const bool wave_skip = __any(my_skip);
-  if ((tid & 63) == 0) s_skip[tid >> 6] = wave_skip ? 1 : 0;
+  if (lane == 0) s_skip[tid >> 6] = wave_skip ? 1 : 0;
   __syncthreads();
   int skip = 0;
 #pragma unroll
@@ -320,28 +194,44 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
       if (live[u]) store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
   }
 
-  // Position ids (headers passed by value): the last wave of workgroup b
-  // writes the ids of rows [64 p, 64 p + 64) for blocks p = b, b + grid, ...,
-  // so every cache line of them is written whole by one store instruction.
-  // A lane's id is its row minus the first row of its sample, the largest
-  // prefix sum of lengths not above the row.
-  if (!a.samples_dev && a.pos && write_meta && tid >= kPackBlock - 64) {
-    const int lane = tid & 63;
-    for (int blk = blockIdx.x; blk * 64 < a.n_tokens; blk += gridDim.x) {
-      const int row = blk * 64 + lane;
-      const int last = min(blk * 64 + 63, a.n_tokens - 1);
-      int start = 0, first = 0;
-      for (int b = 0; b < kInlineSamples && start <= last; b += kLenGroup) {
-        u32x4 g[kLenGroup / 4];
+  // cu_seqlens and position ids, by the last wave after its copies.
+  // Workgroup 0 writes cu_seqlens: an exclusive prefix sum of the sample
+  // lengths, 64 samples per step of a wave-wide scan. Workgroup b writes the
+  // position ids of rows [64 p, 64 p + 64) for blocks p = b, b + grid, ...,
+  // so every cache line of them is written whole by one store instruction:
+  // a row's id is the row minus the first row of its sample, taken from the
+  // runs that start inside the block.
+  if (write_meta && tid >= kPackBlock - 64) {
+    if (blockIdx.x == 0 && a.cu) {
+      if (lane == 0) a.cu[0] = 0;
+      int carry = 0;
+      for (int base = 0; base < a.n; base += 64) {
+        const int i = base + lane;
+        int v = i < a.n ? ld<false, int32_t>(tb + 4 * i) : 0;
 #pragma unroll
-        for (int q = 0; q < kLenGroup / 4; ++q) g[q] = ((const k_u32x4*)(a.lens + b))[q];
-#pragma unroll
-        for (int q = 0; q < kLenGroup; ++q) {
-          if (row >= start) first = start;
-          start += (int)g[q >> 2][q & 3];
+        for (int d = 1; d < 64; d <<= 1) {
+          const int t = __shfl_up(v, d, 64);
+          if (lane >= d) v += t;
         }
+        if (i < a.n) a.cu[i + 1] = carry + v;
+        carry += __shfl(v, 63, 64);
       }
-      if (row < a.n_tokens) a.pos[row] = row - first;
+    }
+    if (a.pos) {
+      const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
+      for (int blk = blockIdx.x; blk * 64 < a.n_tokens; blk += gridDim.x) {
+        const int first = blk * 64, row = first + lane;
+        const int last = min(first + 63, a.n_tokens - 1);
+        int s;
+        PackRun r = run_of<true>(a, tb, first, &s);
+        int start = r.head & 0x7fffffff;
+        while (r.end <= last) {
+          const int next = r.end;
+          r = ld_run<true>(runs + ++s);
+          if (row >= next) start = r.head & 0x7fffffff;
+        }
+        if (row < a.n_tokens) a.pos[row] = row - start;
+      }
     }
   }
 }
@@ -395,10 +285,7 @@ __global__ __launch_bounds__(kBlock) void k_cost(const SampleDesc* __restrict__ 
 
 constexpr int kUnroll = 8;
 
-size_t pack_lds_bytes(const PackArgs& a) {
-  return sizeof(PackSample) * (size_t)a.n + sizeof(int2) * (size_t)a.n_imgs +
-         sizeof(void*) * (size_t)a.max_chunk_rows + sizeof(int32_t) * (size_t)(a.n + 1);
-}
+size_t pack_lds_bytes(const PackArgs& a) { return sizeof(uint64_t) * (size_t)a.max_chunk_rows; }
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);

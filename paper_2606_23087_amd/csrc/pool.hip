@@ -9,7 +9,9 @@
 // asynchronous metadata uploads.
 
 #include <algorithm>
+#include <climits>
 #include <cstdarg>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -501,7 +503,7 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
   if (c.max_samples == 0) c.max_samples = kDefaultMaxSamples;
   if (c.max_samples < 1 || c.max_samples > (1ll << 31) - 1) return fail(FP_EINVAL, "max_samples");
   if (c.meta_bytes == 0) c.meta_bytes = kDefaultMetaBytes;
-  if (c.meta_bytes < 16) return fail(FP_EINVAL, "meta_bytes");
+  if (c.meta_bytes < 16 || c.meta_bytes > fp::kMaxMetaBytes) return fail(FP_EINVAL, "meta_bytes");
   if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunkBytes;
   if (c.chunk_bytes < 0) return fail(FP_EINVAL, "chunk_bytes");
   int ndev = 0;
@@ -1210,7 +1212,6 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   a.cu = out_cu_seqlens;
   a.pos = out_position_ids;
   a.n = n;
-  a.n_imgs = (int32_t)n_imgs;
   a.n_tokens = (int32_t)total;
   a.row_bytes = (int32_t)p->rb;
   a.page_tokens = p->cfg.page_tokens;
@@ -1241,47 +1242,94 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
     a.pb_mul = (uint64_t)m;
     a.pb_shift = sh - 64;
   }
-  const bool staged = n > fp::kInlineSamples || n_imgs > fp::kInlineImages;
+  // The run table: sample lengths, then the runs of every sample in row
+  // order (a text run per nonempty stretch of text rows, an image run per
+  // stretch of images with no text row between them), then the bucket index.
+  std::vector<int32_t> lens((size_t)n), run_start;
+  std::vector<fp::PackRun> runs;
+  {
+    int32_t row = 0;
+    auto close_run = [&]() {
+      if (!runs.empty()) runs.back().end = row;
+    };
+    for (int32_t i = 0; i < n; ++i) {
+      const SampleRec& r = *recs[(size_t)i];
+      const int32_t s0 = row;
+      lens[(size_t)i] = r.len;
+      int32_t ti = 0, vis = 0;
+      bool in_image = false;
+      auto text_to = [&](int32_t upto) {
+        if (upto <= ti) return;
+        close_run();
+        run_start.push_back(row);
+        runs.push_back(fp::PackRun{0, s0 | fp::kTextRun, 0, (int32_t)(r.text_off / 4 + ti - row)});
+        row += upto - ti;
+        ti = upto;
+        in_image = false;
+      };
+      for (int32_t j = 0; j < r.n_img; ++j) {
+        text_to(r.img[2 * (size_t)j]);
+        const int32_t nt = r.img[2 * (size_t)j + 1];
+        if (nt <= 0) continue;
+        if (!in_image) {
+          close_run();
+          run_start.push_back(row);
+          runs.push_back(fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)});
+          in_image = true;
+        }
+        row += nt;
+        vis += nt;
+      }
+      text_to(r.n_text);
+    }
+    close_run();
+  }
+  const int32_t n_runs = (int32_t)runs.size();
+  int32_t shift = 0;
+  while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
+  const int32_t n_buckets = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
+  std::vector<uint16_t> bucket((size_t)(n_buckets + (n_buckets & 1)), 0);
+  for (int32_t b = 0, sidx = 0; b < n_buckets; ++b) {
+    const int64_t first = (int64_t)b << shift;
+    while (sidx + 1 < n_runs && run_start[(size_t)sidx + 1] <= first) ++sidx;
+    bucket[(size_t)b] = (uint16_t)sidx;
+  }
+  a.n_runs = n_runs;
+  a.bucket_shift = shift;
+  const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;
   if (capturing(hs)) {
     // A captured pack is one kernel whose arguments hold the whole
     // microbatch, so a replay packs the same samples again.
     if (staged)
-      return fail(FP_ESTATE, "a pack of more than %d samples or %d images cannot be captured into a graph",
-                  fp::kInlineSamples, fp::kInlineImages);
+      return fail(FP_ESTATE, "a pack of more than %d samples or %d runs cannot be captured into a graph",
+                  fp::kInlineSamples, fp::kInlineRuns);
     // No event queries during capture: the writes must already be known complete.
     for (SampleRec* r : recs)
       if (r->written >= 0)
         return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
                                "before capturing its pack");
   }
-  std::vector<fp::PackSample> big_s;
-  std::vector<int2> big_i;
-  fp::PackSample* smp = a.samples;
-  int2* img = a.imgs;
-  if (staged) {
-    big_s.resize((size_t)n);
-    big_i.resize((size_t)n_imgs);
-    smp = big_s.data();
-    img = big_i.data();
-  }
-  int32_t base = 0;
-  for (int32_t i = 0; i < n; ++i) {
-    const SampleRec& r = *recs[(size_t)i];
-    smp[i] = fp::PackSample{r.len, r.n_img, base, r.n_text, r.text_off, r.page_off};
-    if (!staged) a.lens[i] = r.len;
-    for (int32_t j = 0; j < r.n_img; ++j) img[base + j] = int2{r.img[2 * (size_t)j], r.img[2 * (size_t)j + 1]};
-    base += r.n_img;
-  }
   Stage* s = nullptr;
-  if (staged) {
-    const size_t sb = sizeof(fp::PackSample) * (size_t)n, ib = sizeof(int2) * (size_t)n_imgs;
-    fp_status st = stage_acquire(p, sb + ib, sb + ib, &s);
+  if (!staged) {
+    if (n) std::memcpy(a.lens, lens.data(), 4 * lens.size());
+    if (n_runs) std::memcpy(a.runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
+    if (n_buckets) std::memcpy(a.bucket, bucket.data(), 2 * (size_t)n_buckets);
+    a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
+    a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
+  } else {
+    const size_t o_runs = (4 * lens.size() + 15) & ~(size_t)15;
+    const size_t o_b = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
+    const size_t bytes = o_b + 2 * bucket.size();
+    fp_status st = stage_acquire(p, bytes, bytes, &s);
     if (st != FP_OK) return st;
-    std::memcpy(s->host, smp, sb);
-    if (ib) std::memcpy(s->host + sb, img, ib);
-    FP_HIP(hipMemcpyAsync(s->dev, s->host, sb + ib, hipMemcpyHostToDevice, hs));
-    a.samples_dev = (const fp::PackSample*)s->dev;
-    a.imgs_dev = (const int2*)(s->dev + sb);
+    std::memset(s->host, 0, bytes);
+    if (n) std::memcpy(s->host, lens.data(), 4 * lens.size());
+    if (n_runs) std::memcpy(s->host + o_runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
+    if (!bucket.empty()) std::memcpy(s->host + o_b, bucket.data(), 2 * bucket.size());
+    FP_HIP(hipMemcpyAsync(s->dev, s->host, bytes, hipMemcpyHostToDevice, hs));
+    a.staged = s->dev;
+    a.off_runs = (int32_t)o_runs;
+    a.off_bucket = (int32_t)o_b;
   }
   {
     fp_status st = order_after_writes(p, recs, hs);

@@ -256,6 +256,17 @@ def test_tier_mask_split(fp):
     w.close()
 
 
+def _runs(spec):
+    """Maximal stretches of text rows or of image rows of one sample."""
+    n, ti, in_image = 0, 0, False
+    for p, t in zip(spec.img_pos.tolist(), spec.img_ntok.tolist()):
+        if p > ti:
+            n, ti, in_image = n + 1, p, False
+        if t > 0 and not in_image:
+            n, in_image = n + 1, True
+    return n + (spec.n_text > ti)
+
+
 def _head_specs(rng, n, max_img, vocab):
     """n samples of 1..29 text tokens; sample i has i % (max_img + 1) images of 0..40 rows each at
     random placeholder positions (some empty, some at 0 or at the end)."""
@@ -273,10 +284,11 @@ def _head_specs(rng, n, max_img, vocab):
                                                 (256, 16), (3584, 64), (8192, 32)])
 def test_chunk_head_shapes(fp, hidden, page_tokens):
     """Row resolution at every chunk shape: many rows per chunk (small H,
-    staged in LDS) down to chunks inside one row (large H); page sizes that
-    are not powers of two; 17..64 samples with inline headers, samples with
-    more than eight images, the 64-sample and 128-image limits of the inline
-    headers and microbatches just past them."""
+    one row per lane) down to chunks inside one row (large H); page sizes
+    that are not powers of two; 17..64 samples with an inline run table,
+    samples with eleven images, empty images and adjacent images (merged
+    runs), the 64-sample and 160-run limits of the inline table and
+    microbatches just past them (staged table)."""
     from paper_2606_23087_amd.harness import GpuWorkload
     say(f"case chunk-head H={hidden} P={page_tokens}")
     vocab = 257
@@ -294,13 +306,14 @@ def test_chunk_head_shapes(fp, hidden, page_tokens):
         total = sum(s.length for s in specs)
         out, cu, pos = w.alloc_outputs(rows=total + 64, fill=0x4545)
         cu = torch.full((150,), -1, dtype=torch.int32, device="cuda")
-        imgs = np.cumsum([len(s.img_ntok) for s in specs])
-        n128 = int(np.searchsorted(imgs, 128, side="right"))     # first n samples hold <= 128 images
-        groups = [list(range(17)), list(range(n128)), list(range(n128 + 1)),
+        runs = np.cumsum([_runs(s) for s in specs])
+        r160 = int(np.searchsorted(runs, 160, side="right"))     # first r160 samples form <= 160 runs
+        assert runs[r160 - 1] <= 160 < runs[r160] and r160 < 64
+        groups = [list(range(17)), list(range(r160)), list(range(r160 + 1)),
                   list(range(70, 134)), list(range(70, 135)), list(range(70)),
                   [11, 23, 11, 35, 140 - 1]]
         for g in groups:
-            say(f"  group of {len(g)} samples, {sum(len(specs[i].img_ntok) for i in g)} images")
+            say(f"  group of {len(g)} samples, {sum(_runs(specs[i]) for i in g)} runs")
             n, mx = w.pack([w.ids[i] for i in g], out, cu, pos)
             torch.cuda.synchronize()
             want = definitional_pack([specs[i] for i in g], [vis[i] for i in g], table)
