@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FP_ABI_VERSION 1
+#define FP_ABI_VERSION 2
 
 typedef struct fp_pool fp_pool;   /* opaque; created and owned by the library */
 typedef int32_t fp_status;
@@ -101,6 +101,11 @@ enum { FP_TIER_MASK_HBM = 1, FP_TIER_MASK_HOST = 2, FP_TIER_MASK_ALL = 3 };
  *                bytes (rounded down to whole pages); 0 = 1 GiB.
  *  hbm_backing, host_backing  reserved, must be NULL (the library allocates
  *                and frees all backing memory).
+ *  pack_cus      compute units the pack's chunk geometry is sized for (its last
+ *                chunks shrink over one and a half waves of resident
+ *                workgroups); 0 = the device's count. It changes timing only,
+ *                never results; tests set it small to reach every chunk size.
+ *  reserved      must be 0.
  */
 typedef struct fp_pool_config {
   int32_t hidden;
@@ -119,6 +124,8 @@ typedef struct fp_pool_config {
   int64_t chunk_bytes;
   void* hbm_backing;
   void* host_backing;
+  int32_t pack_cus;
+  int32_t reserved;
 } fp_pool_config;
 
 /* Library ABI version (FP_ABI_VERSION of the build). */

@@ -36,6 +36,12 @@ constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
 constexpr int kPackBlock = 256;      // threads per k_pack workgroup
 constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves (12 KiB chunks)
 constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
+// The last chunks of a pack are smaller, so the final workgroups finish
+// sooner and the launch drains faster: one wave of resident workgroups (CUs x
+// kPackPerCU) gets chunks of kTail1Vecs, half a wave then kTail2Vecs.
+constexpr int kPackPerCU = 8;        // k_pack workgroups resident per CU (occupancy 8)
+constexpr int kTail1Vecs = 512;
+constexpr int kTail2Vecs = 256;
 constexpr int kInlineSamples = 64;   // sample lengths passed by value to k_pack
 constexpr int kInlineRuns = 160;     // runs passed by value to k_pack
 constexpr int kBuckets = 256;        // row buckets of the run index
@@ -86,6 +92,8 @@ struct PackArgs {
   int32_t page_tokens;
   int32_t tier_mask;
   int32_t max_chunk_rows;     // rows one chunk can touch
+  int32_t g0, g1;             // workgroups [0, g0): full chunks; [g0, g1): kTail1Vecs; then kTail2Vecs
+  int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * kChunkVecs)
   int32_t bucket_shift;
   uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
   uint64_t pt_mul;            // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
@@ -114,6 +122,8 @@ struct WriteArgs {
 };
 
 size_t pack_lds_bytes(const PackArgs& a);
+// Chunk geometry of a pack (g0, g1, t1, t2) for a device with n_cu compute units.
+void pack_chunks(PackArgs* a, int n_cu);
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream);
 hipError_t launch_write(const WriteArgs& a, hipStream_t stream);
 hipError_t launch_cost(const SampleDesc* desc, const int32_t* slots, int32_t n, int64_t k,

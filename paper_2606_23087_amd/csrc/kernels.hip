@@ -17,6 +17,8 @@
 
 #include "fp_internal.h"
 
+#include <algorithm>
+
 namespace fp {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -100,9 +102,9 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
 
 // One workgroup packs one chunk of kChunkVecs 16-byte vectors of the output
 // (rows are contiguous in the output, so a chunk is a contiguous byte range
-// that may start and end inside rows): it resolves the source of every row
-// the chunk touches, then moves kVecsPerThread vectors per thread with all
-// loads in flight before the stores.
+// that may start and end inside rows; the last chunks are smaller): it
+// resolves the source of every row the chunk touches, then moves up to
+// kVecsPerThread vectors per thread with all loads in flight before the stores.
 //
 // Up to kWaveRows rows per wave (the usual case: a chunk touches two or three
 // rows at realistic hidden sizes), each row is resolved by one wave with
@@ -126,8 +128,18 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   const bool write_meta = (a.tier_mask & 1) != 0;
   const int vpr = a.row_bytes >> 4;
   const int total = a.n_tokens * vpr;                 // the host keeps this below 2^31
-  const int v0 = blockIdx.x * kChunkVecs;
-  const int v1 = min(v0 + kChunkVecs, total);
+  const int bx = (int)blockIdx.x;
+  int v0, v1;
+  if (bx < a.g0) {
+    v0 = bx * kChunkVecs;
+    v1 = v0 + kChunkVecs;
+  } else if (bx < a.g1) {
+    v0 = a.t1 + (bx - a.g0) * kTail1Vecs;
+    v1 = min(v0 + kTail1Vecs, a.t2);
+  } else {
+    v0 = a.t2 + (bx - a.g1) * kTail2Vecs;
+    v1 = min(v0 + kTail2Vecs, total);
+  }
   const int r0 = div_vpr(a, v0);
   const int rows = v1 > v0 ? div_vpr(a, v1 - 1) - r0 + 1 : 0;
 
@@ -287,9 +299,21 @@ constexpr int kUnroll = 8;
 
 size_t pack_lds_bytes(const PackArgs& a) { return sizeof(uint64_t) * (size_t)a.max_chunk_rows; }
 
+void pack_chunks(PackArgs* a, int n_cu) {
+  const int64_t vecs = (int64_t)a->n_tokens * (a->row_bytes >> 4);
+  const int64_t wave = (int64_t)std::max(n_cu, 1) * kPackPerCU;
+  const int64_t t2 = std::max<int64_t>(vecs - (wave / 2) * kTail2Vecs, 0);
+  const int64_t t1 = (std::max<int64_t>(t2 - wave * kTail1Vecs, 0) / kChunkVecs) * kChunkVecs;
+  a->g0 = (int32_t)(t1 / kChunkVecs);
+  a->g1 = (int32_t)(a->g0 + (t2 - t1 + kTail1Vecs - 1) / kTail1Vecs);
+  a->t1 = (int32_t)t1;
+  a->t2 = (int32_t)t2;
+}
+
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
-  const int grid = vecs > 0 ? (int)((vecs + kChunkVecs - 1) / kChunkVecs) : 1;
+  const int64_t grid64 = a.g1 + (vecs - a.t2 + kTail2Vecs - 1) / kTail2Vecs;
+  const int grid = grid64 > 0 ? (int)grid64 : 1;
   hipLaunchKernelGGL(k_pack, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
   return hipGetLastError();
 }

@@ -194,6 +194,7 @@ struct fp_pool {
   fp_pool_config cfg{};
   std::mutex mu;
   int64_t rb = 0, pb = 0;
+  int n_cu = 0;                       // compute units of the device (pack chunk geometry)
   int64_t n_pages[2] = {0, 0};
   uint64_t gva_start = 0;
   uint64_t region_start[2] = {0, 0};
@@ -491,6 +492,7 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
     return fail(FP_EINVAL, "world_size/rank %d/%d: this library runs one process", c.world_size, c.rank);
   if (c.vocab < 0 || c.vocab > (1ll << 31)) return fail(FP_EINVAL, "vocab %lld", (long long)c.vocab);
   if (c.hbm_backing || c.host_backing) return fail(FP_EINVAL, "caller-provided backing is not supported");
+  if (c.pack_cus < 0 || c.pack_cus > 65536 || c.reserved != 0) return fail(FP_EINVAL, "pack_cus %d / reserved", c.pack_cus);
   if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
   if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
   {
@@ -512,8 +514,11 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
   DeviceGuard guard(c.device);
   if (!guard.ok) return fail(FP_EHIP, "hipSetDevice(%d) failed", c.device);
 
+  int n_cu = c.pack_cus;
+  if (n_cu == 0) FP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, c.device));
   fp_pool* p = new fp_pool();
   p->cfg = c;
+  p->n_cu = n_cu;
   p->rb = 2ll * c.hidden;
   p->pb = p->rb * c.page_tokens;
   p->n_pages[0] = c.hbm_pages;
@@ -1217,6 +1222,7 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   a.page_tokens = p->cfg.page_tokens;
   a.tier_mask = tier_mask;
   a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
+  fp::pack_chunks(&a, p->n_cu);
   // Division of a vector index e < 2^31 by vpr as a multiply and a shift:
   // with s = 31 + ceil(log2 vpr) and m = ceil(2^s / vpr), e / vpr == (e * m) >> s.
   int ceil_log2 = 0;

@@ -33,6 +33,9 @@ except ImportError:
     pass
 
 _lib = C.CDLL(LIB_PATH)
+ABI_VERSION = 2   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
+if _lib.fp_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} has ABI version {_lib.fp_abi_version()}, the bindings expect {ABI_VERSION}; rebuild it")
 
 FP_OK, FP_EINVAL, FP_ENOMEM, FP_ENOENT, FP_ECAPACITY, FP_EALIGN, FP_EHIP, FP_ESTATE = 0, -1, -2, -3, -4, -5, -6, -7
 STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ENOENT", -4: "ECAPACITY", -5: "EALIGN",
@@ -53,6 +56,7 @@ class fp_pool_config(C.Structure):
         ("max_samples", C.c_int64), ("meta_bytes", C.c_int64),
         ("frame_shuffle_seed", C.c_uint64), ("chunk_bytes", C.c_int64),
         ("hbm_backing", C.c_void_p), ("host_backing", C.c_void_p),
+        ("pack_cus", C.c_int32), ("reserved", C.c_int32),
     ]
 
 
@@ -149,7 +153,7 @@ def fp_last_error() -> str:
 def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int = 0,
                 alloc: str = "contig", vocab: int = 0, device: int = 0, gva_start: int = 0,
                 max_samples: int = 0, meta_bytes: int = 0, frame_shuffle_seed: int = 0,
-                chunk_bytes: int = 0, world_size: int = 1, rank: int = 0) -> int:
+                chunk_bytes: int = 0, world_size: int = 1, rank: int = 0, pack_cus: int = 0) -> int:
     cfg = fp_pool_config()
     _lib.fp_config_init(C.byref(cfg))
     cfg.hidden, cfg.page_tokens = hidden, page_tokens
@@ -159,6 +163,7 @@ def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int =
     cfg.world_size, cfg.rank = world_size, rank
     cfg.max_samples, cfg.meta_bytes = max_samples, meta_bytes
     cfg.frame_shuffle_seed, cfg.chunk_bytes = frame_shuffle_seed, chunk_bytes
+    cfg.pack_cus = pack_cus
     out = _P()
     _check(_lib.pool_create(C.byref(cfg), C.byref(out)), "pool_create")
     return int(out.value)

@@ -65,13 +65,13 @@ class GpuWorkload:
                  specs: Optional[List[SampleSpec]] = None,
                  vis_fn: Optional[Callable[[int, SampleSpec], torch.Tensor]] = None,
                  table: Optional[torch.Tensor] = None, churn: bool = True,
-                 frame_shuffle_seed: int = 0, device: int = 0, log=None):
+                 frame_shuffle_seed: int = 0, device: int = 0, log=None, pack_cus: int = 0):
         self.cfg = cfg
         self.seed = seed
         self.device = device
         self.pool = fp.pool_create(hidden=cfg.hidden, page_tokens=cfg.page_tokens, hbm_pages=cfg.hbm_pages,
                                    host_pages=cfg.host_pages, alloc=cfg.alloc, vocab=cfg.vocab,
-                                   device=device, frame_shuffle_seed=frame_shuffle_seed)
+                                   device=device, frame_shuffle_seed=frame_shuffle_seed, pack_cus=pack_cus)
         dev = f"cuda:{device}"
         self.churn_ids: Dict[int, int] = {}
         if churn and cfg.churn_steps:

@@ -280,17 +280,21 @@ def _head_specs(rng, n, max_img, vocab):
     return specs
 
 
+@pytest.mark.parametrize("pack_cus", [0, 1])
 @pytest.mark.parametrize("hidden,page_tokens", [(8, 3), (16, 16), (64, 5), (96, 7), (128, 1),
                                                 (256, 16), (3584, 64), (8192, 32)])
-def test_chunk_head_shapes(fp, hidden, page_tokens):
+def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
     """Row resolution at every chunk shape: many rows per chunk (small H,
     one row per lane) down to chunks inside one row (large H); page sizes
     that are not powers of two; 17..64 samples with an inline run table,
     samples with eleven images, empty images and adjacent images (merged
     runs), the 64-sample and 160-run limits of the inline table and
-    microbatches just past them (staged table)."""
+    microbatches just past them (staged table). pack_cus=1 sizes the chunk
+    geometry for one compute unit, so these small packs also take full
+    chunks and both shrinking tail stages; with the device's count they are
+    all in the last stage."""
     from paper_2606_23087_amd.harness import GpuWorkload
-    say(f"case chunk-head H={hidden} P={page_tokens}")
+    say(f"case chunk-head H={hidden} P={page_tokens} pack_cus={pack_cus}")
     vocab = 257
     rng = np.random.default_rng(hidden * 1000 + page_tokens)
     specs = _head_specs(rng, 70, 11, vocab) + _head_specs(rng, 70, 1, vocab)
@@ -301,7 +305,7 @@ def test_chunk_head_shapes(fp, hidden, page_tokens):
     table = tagged_table(vocab, hidden)
     vis = [tagged_vis(i, s.n_vis, hidden) for i, s in enumerate(specs)]
     w = GpuWorkload(cfg, 0, specs=specs, table=to_dev(table),
-                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None)
+                    vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None, pack_cus=pack_cus)
     try:
         total = sum(s.length for s in specs)
         out, cu, pos = w.alloc_outputs(rows=total + 64, fill=0x4545)

@@ -29,12 +29,12 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(fp.EXPORTED)
-    assert fp.fp_abi_version() == 1
+    assert fp.fp_abi_version() == fp.ABI_VERSION == 2
 
 
 def test_config_struct_matches_header():
-    # fp_pool_config: 2*i32, 2*i64, 2*i32, i64, u64, 2*i32, 2*i64, u64, i64, 2 ptrs
-    assert ctypes.sizeof(fp.fp_pool_config) == 8 + 16 + 8 + 8 + 8 + 8 + 16 + 8 + 8 + 16
+    # fp_pool_config: 2*i32, 2*i64, 2*i32, i64, u64, 2*i32, 2*i64, u64, i64, 2 ptrs, 2*i32
+    assert ctypes.sizeof(fp.fp_pool_config) == 8 + 16 + 8 + 8 + 8 + 8 + 16 + 8 + 8 + 16 + 8
 
 
 @pytest.mark.parametrize("seed", range(30))
@@ -69,7 +69,7 @@ def test_plan_partition_errors():
 def test_pool_create_rejects_bad_config_without_gpu():
     # Argument checks come before any device call.
     for kw in [dict(hidden=4), dict(hidden=12), dict(page_tokens=0), dict(hbm_pages=0),
-               dict(alloc=7), dict(world_size=2)]:
+               dict(alloc=7), dict(world_size=2), dict(pack_cus=-1), dict(meta_bytes=(1 << 33) + 16)]:
         args = dict(hidden=256, page_tokens=16, hbm_pages=4)
         args.update(kw)
         with pytest.raises(fp.FlowPoolError) as e:
