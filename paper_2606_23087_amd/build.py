@@ -37,5 +37,29 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+DRIVER_SRC = os.path.join(ROOT, "tests", "c_abi", "pack_driver.c")
+DRIVER = os.path.join(ROOT, "tests", "c_abi", "pack_driver")
+
+
+def build_driver(verbose: bool = False) -> str:
+    """Compile the plain-C test driver of the C ABI (host code only, gcc),
+    linked against the in-tree library and the HIP runtime."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    tmp = DRIVER + ".tmp"
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(rocm, "include"),
+           DRIVER_SRC, "-o", tmp, "-L", HERE, "-lflowpool", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/../../paper_2606_23087_amd", "-Wl,-rpath," + os.path.join(rocm, "lib")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError(f"gcc failed with status {r.returncode}")
+    os.replace(tmp, DRIVER)
+    return DRIVER
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_driver(verbose=True))

@@ -96,3 +96,23 @@ def test_pool_create_rejects_gva_span_beyond_2_52():
     with pytest.raises(fp.FlowPoolError) as e:
         fp.pool_create(hidden=1 << 20, page_tokens=1 << 20, hbm_pages=1 << 20)
     assert e.value.code == "EINVAL"
+
+
+def test_c_driver_fails_loudly_without_a_device(tmp_path):
+    """The plain-C driver of the C ABI links and runs; with no usable GPU its
+    first pool call fails and it exits 1 with the library's message."""
+    import os
+    import struct
+    import subprocess
+    drv = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "tests", "c_abi", "pack_driver")
+    if not os.path.exists(drv):
+        pytest.skip("driver not built")
+    r = subprocess.run([drv], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 1 and "usage" in r.stderr
+    import torch
+    if torch.cuda.device_count() > 0:
+        pytest.skip("a GPU is present (the GPU test drives it)")
+    src = tmp_path / "in.bin"
+    src.write_bytes(struct.pack("<7i", 8, 4, 1, 1, 16, 1, 16) + bytes(16) + struct.pack("<3i", 1, 0, 0))
+    r = subprocess.run([drv, str(src), str(tmp_path / "out.bin")], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 1 and "pool_create failed" in r.stderr
