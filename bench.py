@@ -150,6 +150,8 @@ def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
     def timed(masks_streams):
         ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        gc.collect()
+        gc.disable()
         ev[0].record(stream)
         for _ in range(reps):
             for j, mb in enumerate(mbs):
@@ -161,6 +163,7 @@ def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
                     if st is not stream:
                         stream.wait_stream(st)
         ev[1].record(stream)
+        gc.enable()
         torch.cuda.synchronize()
         return ev[0].elapsed_time(ev[1]) * 1e-3 / reps
 
@@ -272,7 +275,6 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
 
     def packs() -> float:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        gc.collect()
         gc.disable()          # a collector pause between enqueues would be timed as GPU idle
         e0.record(pack_stream)
         for _ in range(passes):
@@ -280,11 +282,14 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
                 out, cu, pos = outs[j % len(outs)]
                 w.pack(mb, out, cu, pos, stream=pack_stream)
         e1.record(pack_stream)
+        gc.enable()
         e1.synchronize()
         return e0.elapsed_time(e1) * 1e-3
 
     torch.cuda.synchronize()
+    gc.collect()
     t_alone = packs()
+    gc.collect()            # before the producer starts: a collection holds the interpreter lock
     stop = threading.Event()
     stats = {"writes": 0, "bytes": 0, "error": None}
 
