@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
                "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start), "s"(a.pt_mul),
                "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
                "s"(a.tier_mask), "s"(a.row_bytes), "s"(a.n_tokens), "s"(a.div_mul),
-               "s"(a.div_shift));
+               "s"(a.div_shift), "s"(a.g0), "s"(a.g1), "s"(a.t1), "s"(a.t2));
   const uint8_t* tb = a.staged ? a.staged : reinterpret_cast<const uint8_t*>(a.lens);
   int my_skip = 0;                                  // a row of this chunk is not copied
 
