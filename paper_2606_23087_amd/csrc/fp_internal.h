@@ -36,6 +36,9 @@ constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
 constexpr int kPackBlock = 256;      // threads per k_pack workgroup
 constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves (12 KiB chunks)
 constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
+// Rows of at least this many bytes are packed in 8 KiB chunks (2 vectors per
+// thread) instead: measured faster from H 5120 up, slower at H 3584 and 4096.
+constexpr int kSmallChunkRowBytes = 10240;
 // The last chunks of a pack are smaller, so the final workgroups finish
 // sooner and the launch drains faster: one wave of resident workgroups (CUs x
 // kPackPerCU) gets chunks of kTail1Vecs, half a wave then kTail2Vecs.
@@ -93,7 +96,8 @@ struct PackArgs {
   int32_t tier_mask;
   int32_t max_chunk_rows;     // rows one chunk can touch
   int32_t g0, g1;             // workgroups [0, g0): full chunks; [g0, g1): kTail1Vecs; then kTail2Vecs
-  int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * kChunkVecs)
+  int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * full chunk)
+  int32_t vpt;                // vectors per thread of a full chunk (2 or kVecsPerThread)
   int32_t bucket_shift;
   uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
   uint64_t pt_mul;            // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31

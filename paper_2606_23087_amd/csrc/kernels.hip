@@ -35,8 +35,12 @@ __device__ __forceinline__ u32x4 load16(const uint8_t* p) {
 // on the pack this measured about 1.5 % faster than nt alone. The
 // compiler has no builtin for that bit combination, hence the asm; it has
 // no outputs, so the compiler still waits for the loaded data it stores.
+// The compiler does not see inside the asm, so the asm carries the wait that
+// gfx940-class parts need between a store of more than 8 bytes and a VALU
+// write to its data registers (two wait states): without it the compiler
+// may reuse those registers right after the store and corrupt its data.
 __device__ __forceinline__ void store16(uint8_t* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" : : "v"(p), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
 }
 
 // Reads through constant-address-space views of uniform addresses compile to
@@ -110,7 +114,9 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
 // rows at realistic hidden sizes), each row is resolved by one wave with
 // scalar loads, so the only vector memory loads are the copies. Chunks of
 // many short rows resolve one row per lane.
+template <int VPT>
 __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
+  constexpr int kChunk = kPackBlock * VPT;       // vectors of a full chunk
   extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
   const int tid = threadIdx.x;
@@ -131,8 +137,8 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   const int bx = (int)blockIdx.x;
   int v0, v1;
   if (bx < a.g0) {
-    v0 = bx * kChunkVecs;
-    v1 = v0 + kChunkVecs;
+    v0 = bx * kChunk;
+    v1 = v0 + kChunk;
   } else if (bx < a.g1) {
     v0 = a.t1 + (bx - a.g0) * kTail1Vecs;
     v1 = min(v0 + kTail1Vecs, a.t2);
@@ -174,10 +180,10 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   // Vector e of the chunk belongs to row e / vpr (multiply-shift division).
   // A vector is live if it lies in the chunk and its row is copied; only
   // live vectors get an address, dead ones are never loaded or stored.
-  uint64_t from[kVecsPerThread];
-  bool live[kVecsPerThread];
+  uint64_t from[VPT];
+  bool live[VPT];
 #pragma unroll
-  for (int u = 0; u < kVecsPerThread; ++u) {
+  for (int u = 0; u < VPT; ++u) {
     const int e = v0 + u * kPackBlock + tid;
     from[u] = 0;
     live[u] = false;
@@ -188,21 +194,21 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
       from[u] = live[u] ? base + (uint64_t)(e - row * vpr) * 16 : 0;
     }
   }
-  u32x4 v[kVecsPerThread];
-  if (v1 - v0 == kChunkVecs && !skip) {
+  u32x4 v[VPT];
+  if (v1 - v0 == kChunk && !skip) {
     // Whole chunk, every row copied: no predication, so the compiler can keep
     // all loads in flight and wait for them one at a time before each store.
 #pragma unroll
-    for (int u = 0; u < kVecsPerThread; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
+    for (int u = 0; u < VPT; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
 #pragma unroll
-    for (int u = 0; u < kVecsPerThread; ++u)
+    for (int u = 0; u < VPT; ++u)
       store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
   } else {
 #pragma unroll
-    for (int u = 0; u < kVecsPerThread; ++u)
+    for (int u = 0; u < VPT; ++u)
       if (live[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
 #pragma unroll
-    for (int u = 0; u < kVecsPerThread; ++u)
+    for (int u = 0; u < VPT; ++u)
       if (live[u]) store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
   }
 
@@ -300,11 +306,13 @@ constexpr int kUnroll = 8;
 size_t pack_lds_bytes(const PackArgs& a) { return sizeof(uint64_t) * (size_t)a.max_chunk_rows; }
 
 void pack_chunks(PackArgs* a, int n_cu) {
+  a->vpt = a->row_bytes >= kSmallChunkRowBytes ? 2 : kVecsPerThread;
+  const int64_t chunk = (int64_t)kPackBlock * a->vpt;
   const int64_t vecs = (int64_t)a->n_tokens * (a->row_bytes >> 4);
   const int64_t wave = (int64_t)std::max(n_cu, 1) * kPackPerCU;
   const int64_t t2 = std::max<int64_t>(vecs - (wave / 2) * kTail2Vecs, 0);
-  const int64_t t1 = (std::max<int64_t>(t2 - wave * kTail1Vecs, 0) / kChunkVecs) * kChunkVecs;
-  a->g0 = (int32_t)(t1 / kChunkVecs);
+  const int64_t t1 = (std::max<int64_t>(t2 - wave * kTail1Vecs, 0) / chunk) * chunk;
+  a->g0 = (int32_t)(t1 / chunk);
   a->g1 = (int32_t)(a->g0 + (t2 - t1 + kTail1Vecs - 1) / kTail1Vecs);
   a->t1 = (int32_t)t1;
   a->t2 = (int32_t)t2;
@@ -314,7 +322,10 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
   const int64_t grid64 = a.g1 + (vecs - a.t2 + kTail2Vecs - 1) / kTail2Vecs;
   const int grid = grid64 > 0 ? (int)grid64 : 1;
-  hipLaunchKernelGGL(k_pack, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
+  if (a.vpt == 2)
+    hipLaunchKernelGGL(k_pack<2>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
+  else
+    hipLaunchKernelGGL(k_pack<kVecsPerThread>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
   return hipGetLastError();
 }
 

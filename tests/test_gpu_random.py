@@ -45,7 +45,7 @@ def _spec(rng, vocab):
 @pytest.mark.parametrize("seed", range(64))
 def test_random_packs(fp, seed):
     rng = np.random.default_rng(9000 + seed)
-    hidden = int(rng.choice([8, 16, 24, 64, 104, 200, 512, 1000, 2048, 3584]))
+    hidden = int(rng.choice([8, 16, 24, 64, 104, 200, 512, 1000, 2048, 3584, 5120, 8192]))
     page_tokens = int(rng.integers(1, 70))
     alloc = "scatter" if seed % 2 else "contig"
     pack_cus = int(rng.choice([0, 1, 2, 5]))
