@@ -104,11 +104,12 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
   return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
 }
 
-// One workgroup packs one chunk of kChunkVecs 16-byte vectors of the output
+// One workgroup packs one chunk of 256 * VPT 16-byte vectors of the output
 // (rows are contiguous in the output, so a chunk is a contiguous byte range
 // that may start and end inside rows; the last chunks are smaller): it
-// resolves the source of every row the chunk touches, then moves up to
-// kVecsPerThread vectors per thread with all loads in flight before the stores.
+// resolves the source of every row the chunk touches, then moves up to VPT
+// vectors per thread with all loads in flight before the stores. VPT is 3
+// (12 KiB chunks), or 2 for rows of kSmallChunkRowBytes or more.
 //
 // Up to kWaveRows rows per wave (the usual case: a chunk touches two or three
 // rows at realistic hidden sizes), each row is resolved by one wave with
