@@ -47,6 +47,18 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def cpu_model_name() -> str:
+    """The host CPU's model string (from /proc/cpuinfo where there is one)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def pack_bytes(cfg, specs) -> int:
     rb = cfg.row_bytes
     tokens = sum(s.length for s in specs)
@@ -121,7 +133,7 @@ def cpu_baseline(cfg, w, mbs, seed: int, budget_s: float):
                 sample=f"{len(take)} of {cfg.n_mb} microbatches of seed {seed} "
                        f"({sum(len(m) for m in take)} samples), packed {packs} times in {el:.1f} s "
                        f"by the single-threaded numpy pool oracle",
-                cpu_model=platform.processor() or platform.machine(),
+                cpu_model=cpu_model_name(),
                 os_cpu_count=os.cpu_count(), affinity=len(os.sched_getaffinity(0)))
 
 
