@@ -211,6 +211,24 @@ def d2d_ceiling(nbytes: int = 1 << 30, iters: int = 10) -> float:
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def h2d_ceiling(nbytes: int = 1 << 30, iters: int = 5) -> float:
+    """Pinned host -> device copy rate of one large copy (the host tier's link)."""
+    import torch
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    d.copy_(h, non_blocking=True)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        d.copy_(h, non_blocking=True)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / iters
+    del h, d
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 SCHED_CAPACITIES = (2048, 4096, 8192, 16384, 32768)
 
 
@@ -689,6 +707,7 @@ def main() -> int:
                                                  for t, m in zip(plan["mb_tokens"], plan["mb_max_len"]))), 5)}
     if cfg.host_pages:
         result["tiers"] = tier_split(cfg, w, mbs, spec_of, outs, pack_stream)
+        result["tiers"]["h2d_copy_GBps"] = round(h2d_ceiling(), 1)
     result["d2d_copy_ceiling_GBps"] = round(d2d_ceiling(), 1)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
