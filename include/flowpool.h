@@ -101,10 +101,11 @@ enum { FP_TIER_MASK_HBM = 1, FP_TIER_MASK_HOST = 2, FP_TIER_MASK_ALL = 3 };
  *                bytes (rounded down to whole pages); 0 = 1 GiB.
  *  hbm_backing, host_backing  reserved, must be NULL (the library allocates
  *                and frees all backing memory).
- *  pack_cus      compute units the pack's chunk geometry is sized for (its last
- *                chunks shrink over one and a half waves of resident
- *                workgroups); 0 = the device's count. It changes timing only,
- *                never results; tests set it small to reach every chunk size.
+ *  pack_cus      compute units the pack's chunk geometry is sized for (the
+ *                chunks of its last wave and a half of resident workgroups are
+ *                8 KiB, then 4 KiB); 0 = the device's count. It changes timing
+ *                only, never results; tests set it small to reach every chunk
+ *                size.
  *  reserved      must be 0.
  */
 typedef struct fp_pool_config {

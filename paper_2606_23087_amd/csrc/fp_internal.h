@@ -41,7 +41,8 @@ constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per 
 constexpr int kSmallChunkRowBytes = 10240;
 // The last chunks of a pack are smaller, so the final workgroups finish
 // sooner and the launch drains faster: one wave of resident workgroups (CUs x
-// kPackPerCU) gets chunks of kTail1Vecs, half a wave then kTail2Vecs.
+// kPackPerCU) gets chunks of kTail1Vecs (the full size when rows take 8 KiB
+// chunks), half a wave then kTail2Vecs.
 constexpr int kPackPerCU = 8;        // k_pack workgroups resident per CU (occupancy 8)
 constexpr int kTail1Vecs = 512;
 constexpr int kTail2Vecs = 256;
