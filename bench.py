@@ -285,7 +285,11 @@ def scheduler_bench(args) -> int:
 def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
     """Pack GB/s of the workload's microbatches alone and while a producer
     thread keeps writing new samples on its own stream (and freeing the oldest
-    beyond a window of 16), both timed over the same packs."""
+    beyond a window of 16), both timed over the same packs. The packs of one
+    pass are captured into a HIP graph and replayed, so the consumer needs no
+    host work per pack: enqueuing 1280 packs from Python while the producer
+    thread holds the interpreter lock would starve the pack stream and time
+    the host instead of the GPU."""
     import collections
     import threading
 
@@ -303,14 +307,25 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
     mb_bytes = sum(pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs)
     passes = max(1, args.steps)
 
+    torch.cuda.synchronize()
+    fp.pool_reclaim(w.pool, True)                   # the packed samples' writes are known complete
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(pack_stream):
+        with torch.cuda.graph(graph, stream=pack_stream):
+            for j, mb in enumerate(mbs):
+                out, cu, pos = outs[j % len(outs)]
+                w.pack(mb, out, cu, pos, stream=pack_stream)
+    with torch.cuda.stream(pack_stream):
+        graph.replay()
+    torch.cuda.synchronize()
+
     def packs() -> float:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         gc.disable()          # a collector pause between enqueues would be timed as GPU idle
         e0.record(pack_stream)
-        for _ in range(passes):
-            for j, mb in enumerate(mbs):
-                out, cu, pos = outs[j % len(outs)]
-                w.pack(mb, out, cu, pos, stream=pack_stream)
+        with torch.cuda.stream(pack_stream):
+            for _ in range(passes):
+                graph.replay()
         e1.record(pack_stream)
         gc.enable()
         e1.synchronize()
@@ -356,6 +371,7 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
     stop.set()
     th.join()
     torch.cuda.synchronize()
+    del graph
     alone = mb_bytes * passes / t_alone / 1e9
     busy = mb_bytes * passes / t_busy / 1e9
     prod = (b1 - b0) / wall / 1e9

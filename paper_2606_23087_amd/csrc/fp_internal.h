@@ -32,7 +32,6 @@ constexpr uint64_t PTE_HOST = 2ull;
 constexpr uint64_t PTE_ADDR_MASK = ~0xFull;
 
 constexpr int kBlock = 256;          // threads per workgroup for all kernels
-constexpr int kMaxTileRows = 64;     // rows per workgroup tile in k_write
 constexpr int kPackBlock = 256;      // threads per k_pack workgroup
 constexpr int kVecsPerThread = 3;    // 16-byte vectors each k_pack thread moves (12 KiB chunks)
 constexpr int kChunkVecs = kPackBlock * kVecsPerThread;   // output vectors per k_pack workgroup
@@ -112,21 +111,39 @@ struct PackArgs {
 };
 static_assert(sizeof(PackArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
+// Division constants of a pool (host-computed once): for e < 2^31,
+// e / (row_bytes / 16) == (e * div_mul) >> div_shift and
+// e / page_tokens == (e * pt_mul) >> pt_shift; for d < 2^52,
+// d / page_bytes == umulhi64(d, pb_mul) >> pb_shift.
+struct Divisors {
+  uint64_t div_mul, pt_mul, pb_mul;
+  int32_t div_shift, pt_shift, pb_shift;
+};
+
+// Workgroups of one producer write at most; a larger write loops over its
+// chunks. (Smaller caps, 128 to 512, made writes slower and did not make the
+// packs beside them measurably faster.)
+constexpr int kWriteGrid = 1 << 16;
+
+// The producer's write of one sample: its visual rows (contiguous at `vis`)
+// are copied into its pages in chunks of kChunkVecs vectors, like a pack
+// with source and destination exchanged.
 struct WriteArgs {
   SampleDesc desc;            // descriptor to publish into the table
   SampleDesc* desc_table;
   int32_t slot;
+  int32_t row_bytes;
   const uint8_t* meta;
   const uint64_t* pte;
   uint64_t gva_start;
-  uint64_t page_bytes;
   const uint8_t* vis;         // producer rows, or null
-  int32_t row_bytes;
   int32_t page_tokens;
-  int32_t tile_rows;
+  int32_t max_chunk_rows;     // rows one chunk can touch
+  Divisors dv;
 };
 
 size_t pack_lds_bytes(const PackArgs& a);
+Divisors make_divisors(int64_t row_bytes, int64_t page_tokens, uint64_t page_bytes);
 // Chunk geometry of a pack (g0, g1, t1, t2) for a device with n_cu compute units.
 void pack_chunks(PackArgs* a, int n_cu);
 hipError_t launch_pack(const PackArgs& a, hipStream_t stream);

@@ -255,40 +255,74 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   }
 }
 
-template <int U>
-__global__ __launch_bounds__(kBlock) void k_write(WriteArgs a) {
-  __shared__ uint8_t* s_dst[kMaxTileRows];
+// Producer write (Sec. 3.2): the sample's contiguous visual rows are cut into
+// chunks of kChunkVecs vectors; each workgroup loops over chunks b, b + grid,
+// ... (the grid is capped at kWriteGrid). Per chunk, each wave walks the page
+// table for rows wave, wave + 4, ... with scalar loads (visual row -> page
+// GVA -> page-table entry -> row in the physical page), a barrier shares the
+// destinations, and every thread moves up to kVecsPerThread vectors. Chunks
+// of many short rows walk one row per lane. Workgroup 0 also publishes the
+// sample descriptor.
+__global__ __launch_bounds__(kPackBlock) void k_write(WriteArgs a) {
+  extern __shared__ __align__(16) uint64_t s_dst[];
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
   if (blockIdx.x == 0 && tid == 0) a.desc_table[a.slot] = a.desc;
   if (!a.vis) return;
-  const int row0 = blockIdx.x * a.tile_rows;
-  const int rows = min(a.tile_rows, a.desc.n_vis - row0);
-  if (tid < rows) {
-    const int v = row0 + tid;
-    const int lp = v / a.page_tokens;
-    const int off = v - lp * a.page_tokens;
-    const uint64_t gva = reinterpret_cast<const uint64_t*>(a.meta + a.desc.page_off)[lp];
-    const uint64_t pte = a.pte[(gva - a.gva_start) / a.page_bytes];
-    s_dst[tid] = reinterpret_cast<uint8_t*>(pte & PTE_ADDR_MASK) + (size_t)off * a.row_bytes;
-  }
-  __syncthreads();
-  // Source rows are contiguous; destinations come from the page walk.
   const int vpr = a.row_bytes >> 4;
-  const int total = rows * vpr;
-  const uint8_t* src = a.vis + (size_t)row0 * a.row_bytes;
-  for (int e0 = tid; e0 < total; e0 += kBlock * U) {
-    u32x4 v[U];
-    int rr[U], cc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int e = e0 + u * kBlock;
-      rr[u] = e < total ? e / vpr : -1;
-      cc[u] = e - (rr[u] < 0 ? 0 : rr[u]) * vpr;
-      if (rr[u] >= 0) v[u] = load16(src + (size_t)e * 16);
+  const int total = a.desc.n_vis * vpr;               // the host keeps this below 2^31
+  const uint64_t* pages = reinterpret_cast<const uint64_t*>(a.meta + a.desc.page_off);
+  auto div_row = [&](int e) { return (int)(((uint64_t)(uint32_t)e * a.dv.div_mul) >> a.dv.div_shift); };
+  auto dest = [&](auto ldk, int v) {
+    const int lp = (int)(((uint64_t)(uint32_t)v * a.dv.pt_mul) >> a.dv.pt_shift);
+    const int in_page = v - lp * a.page_tokens;
+    const uint64_t gva = ldk(pages + lp);
+    const uint64_t vpn = __umul64hi(gva - a.gva_start, a.dv.pb_mul) >> a.dv.pb_shift;
+    return (ldk(a.pte + vpn) & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
+  };
+  for (int64_t chunk = blockIdx.x; chunk * kChunkVecs < total; chunk += gridDim.x) {
+    const int v0 = (int)chunk * kChunkVecs;
+    const int v1 = min(v0 + kChunkVecs, total);
+    const int r0 = div_row(v0);
+    const int rows = div_row(v1 - 1) - r0 + 1;
+    if (rows <= kWaveRows * (kPackBlock / 64)) {
+      const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+      for (int t = wave; t < rows; t += kPackBlock / 64) {
+        const uint64_t d = dest([](const uint64_t* p) { return ld<true, uint64_t>(p); }, r0 + t);
+        if (lane == 0) s_dst[t] = d;
+      }
+    } else {
+      for (int t = tid; t < rows; t += kPackBlock)
+        s_dst[t] = dest([](const uint64_t* p) { return ld<false, uint64_t>(p); }, r0 + t);
     }
+    __syncthreads();
+    uint64_t to[kVecsPerThread];
+    u32x4 v[kVecsPerThread];
+    if (v1 - v0 == kChunkVecs) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (rr[u] >= 0) store16(s_dst[rr[u]] + (size_t)cc[u] * 16, v[u]);
+      for (int u = 0; u < kVecsPerThread; ++u) {
+        const int e = v0 + u * kPackBlock + tid;
+        const int row = div_row(e);
+        to[u] = s_dst[row - r0] + (uint64_t)(e - row * vpr) * 16;
+        v[u] = load16(a.vis + (size_t)e * 16);
+      }
+#pragma unroll
+      for (int u = 0; u < kVecsPerThread; ++u) store16(reinterpret_cast<uint8_t*>(to[u]), v[u]);
+    } else {
+#pragma unroll
+      for (int u = 0; u < kVecsPerThread; ++u) {
+        const int e = v0 + u * kPackBlock + tid;
+        if (e < v1) {
+          const int row = div_row(e);
+          to[u] = s_dst[row - r0] + (uint64_t)(e - row * vpr) * 16;
+          v[u] = load16(a.vis + (size_t)e * 16);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kVecsPerThread; ++u)
+        if (v0 + u * kPackBlock + tid < v1) store16(reinterpret_cast<uint8_t*>(to[u]), v[u]);
+    }
+    __syncthreads();                                  // s_dst is rewritten for the next chunk
   }
 }
 
@@ -301,8 +335,6 @@ __global__ __launch_bounds__(kBlock) void k_cost(const SampleDesc* __restrict__ 
     out[i] = k * l + l * l;
   }
 }
-
-constexpr int kUnroll = 8;
 
 size_t pack_lds_bytes(const PackArgs& a) { return sizeof(uint64_t) * (size_t)a.max_chunk_rows; }
 
@@ -331,10 +363,33 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_write(const WriteArgs& a, hipStream_t stream) {
-  const int rows = a.vis ? a.desc.n_vis : 0;
-  const int grid = rows > 0 ? (rows + a.tile_rows - 1) / a.tile_rows : 1;
-  hipLaunchKernelGGL(k_write<kUnroll>, dim3(grid), dim3(kBlock), 0, stream, a);
+  const int64_t vecs = a.vis ? (int64_t)a.desc.n_vis * (a.row_bytes >> 4) : 0;
+  const int grid = vecs > 0 ? (int)std::min<int64_t>((vecs + kChunkVecs - 1) / kChunkVecs, kWriteGrid) : 1;
+  hipLaunchKernelGGL(k_write, dim3(grid), dim3(kPackBlock), sizeof(uint64_t) * (size_t)std::max(a.max_chunk_rows, 1),
+                     stream, a);
   return hipGetLastError();
+}
+
+Divisors make_divisors(int64_t row_bytes, int64_t page_tokens, uint64_t page_bytes) {
+  Divisors d{};
+  // e / q for e < 2^31: with s = 31 + ceil(log2 q), m = ceil(2^s / q), e / q == (e * m) >> s.
+  auto small = [](int64_t q, uint64_t* mul, int32_t* shift) {
+    int c = 0;
+    while ((1ll << c) < q) ++c;
+    *shift = 31 + c;
+    *mul = (uint64_t)(((1ull << *shift) + (uint64_t)q - 1) / (uint64_t)q);
+  };
+  small(row_bytes / 16, &d.div_mul, &d.div_shift);
+  small(page_tokens, &d.pt_mul, &d.pt_shift);
+  // GVA offset d < 2^52 by page_bytes: with c = ceil(log2 pb), N = max(52, 64 - c)
+  // and s = N + c, m = ceil(2^s / pb) fits in 64 bits and d / pb == (d * m) >> s,
+  // taken as the high 64 bits of the 128-bit product shifted by s - 64.
+  int c = 0;
+  while ((1ull << c) < page_bytes) ++c;
+  const int sh = std::max(52, 64 - c) + c;
+  d.pb_mul = (uint64_t)((((unsigned __int128)1 << sh) + page_bytes - 1) / page_bytes);
+  d.pb_shift = sh - 64;
+  return d;
 }
 
 hipError_t launch_cost(const SampleDesc* desc, const int32_t* slots, int32_t n, int64_t k,

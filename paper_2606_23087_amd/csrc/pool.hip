@@ -222,7 +222,7 @@ struct fp_pool {
   // staging
   Stage ring[kRing];
   int ring_next = 0;
-  int tile_rows = 1;
+  fp::Divisors dv{};                  // division constants of the row, page and GVA sizes
 
   uint64_t page_gva(int tier, int64_t idx) const { return seg_start[tier] + (uint64_t)idx * (uint64_t)pb; }
   int page_index(uint64_t gva, int64_t* idx) const {
@@ -531,7 +531,7 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
   p->region_start[0] = c.gva_start;
   p->region_start[1] = c.gva_start + (uint64_t)c.world_size * p->max_size[0];
   for (int t = 0; t < 2; ++t) p->seg_start[t] = p->region_start[t] + (uint64_t)c.rank * p->max_size[t];
-  p->tile_rows = (int)std::max<int64_t>(1, std::min<int64_t>(fp::kMaxTileRows, 65536 / p->rb));
+  p->dv = fp::make_divisors(p->rb, c.page_tokens, (uint64_t)p->pb);
 
   auto bail = [&](fp_status s) {
     std::string keep = t_err;
@@ -630,6 +630,9 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   }
   const int64_t len = n_vis + n_text;
   if (len < 1 || len > kMaxSampleRows) return fail(FP_EINVAL, "sample length %lld", (long long)len);
+  if (n_vis * (p->rb / 16) > 0x7fffffffll)
+    return fail(FP_EINVAL, "%lld visual rows of %lld bytes are too many for one write", (long long)n_vis,
+                (long long)p->rb);
   for (int32_t i = 0; i < n_text; ++i)
     if (text_ids[i] < 0 || text_ids[i] >= p->cfg.vocab)
       return fail(FP_EINVAL, "text id %d at %d outside [0, %lld)", text_ids[i], i, (long long)p->cfg.vocab);
@@ -716,11 +719,11 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   wa.meta = p->meta_dev;
   wa.pte = p->pte_dev;
   wa.gva_start = p->gva_start;
-  wa.page_bytes = (uint64_t)p->pb;
   wa.vis = vis_dev;
   wa.row_bytes = (int32_t)p->rb;
   wa.page_tokens = p->cfg.page_tokens;
-  wa.tile_rows = p->tile_rows;
+  wa.max_chunk_rows = (int32_t)std::min<int64_t>(n_vis, fp::kChunkVecs / (p->rb / 16) + 2);
+  wa.dv = p->dv;
   hipError_t e = fp::launch_write(wa, hs);
   if (e != hipSuccess) return rollback(fail(FP_EHIP, "write kernel: %s", hipGetErrorString(e)));
   int32_t ev = -1;
@@ -1223,31 +1226,12 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   a.tier_mask = tier_mask;
   a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
   fp::pack_chunks(&a, p->n_cu);
-  // Division of a vector index e < 2^31 by vpr as a multiply and a shift:
-  // with s = 31 + ceil(log2 vpr) and m = ceil(2^s / vpr), e / vpr == (e * m) >> s.
-  int ceil_log2 = 0;
-  while ((1ll << ceil_log2) < vpr) ++ceil_log2;
-  a.div_shift = 31 + ceil_log2;
-  a.div_mul = (uint64_t)(((1ull << a.div_shift) + (uint64_t)vpr - 1) / (uint64_t)vpr);
-  // The same for a visual-row index by page_tokens.
-  const int64_t pt = p->cfg.page_tokens;
-  ceil_log2 = 0;
-  while ((1ll << ceil_log2) < pt) ++ceil_log2;
-  a.pt_shift = 31 + ceil_log2;
-  a.pt_mul = (uint64_t)(((1ull << a.pt_shift) + (uint64_t)pt - 1) / (uint64_t)pt);
-  // GVA offset d < 2^52 by page_bytes: with c = ceil(log2 pb), N = max(52, 64 - c)
-  // and s = N + c, m = ceil(2^s / pb) fits in 64 bits and d / pb == (d * m) >> s,
-  // taken as the high 64 bits of the 128-bit product shifted by s - 64.
-  {
-    const uint64_t pbu = (uint64_t)p->pb;
-    int c = 0;
-    while ((1ull << c) < pbu) ++c;
-    const int nbits = std::max(52, 64 - c);
-    const int sh = nbits + c;
-    const unsigned __int128 m = (((unsigned __int128)1 << sh) + pbu - 1) / pbu;
-    a.pb_mul = (uint64_t)m;
-    a.pb_shift = sh - 64;
-  }
+  a.div_mul = p->dv.div_mul;
+  a.div_shift = p->dv.div_shift;
+  a.pt_mul = p->dv.pt_mul;
+  a.pt_shift = p->dv.pt_shift;
+  a.pb_mul = p->dv.pb_mul;
+  a.pb_shift = p->dv.pb_shift;
   // The run table: sample lengths, then the runs of every sample in row
   // order (a text run per nonempty stretch of text rows, an image run per
   // stretch of images with no text row between them), then the bucket index.
