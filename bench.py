@@ -653,27 +653,44 @@ def main() -> int:
     durs = np.array([s_.elapsed_time(e_) * 1e-3 for s_, e_ in events])   # seconds
 
     graph_s = None
+    graph2_s = None
     if args.graph:
         # One step's packs captured into a HIP graph and replayed: no host
         # work per pack (matters when the packs are small and host-bound).
+        # Captured once as one chain of packs, once as two independent chains
+        # (forked from the capture stream): packs into distinct buffers do not
+        # depend on each other, and two at a time hide each other's launch
+        # ramp and drain.
         fp.pool_reclaim(w.pool, True)
         gouts = [w.alloc_outputs() for _ in range(len(mbs))]
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(pack_stream):
-            with torch.cuda.graph(g, stream=pack_stream):
-                for mb, (o, c, q) in zip(mbs, gouts):
-                    w.pack(mb, o, c, q, stream=pack_stream)
-        g.replay()
-        torch.cuda.synchronize()
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        g0.record(pack_stream)
-        with torch.cuda.stream(pack_stream):
-            for _ in range(args.steps):
+
+        def replay_s(branches: int) -> float:
+            side = [torch.cuda.Stream() for _ in range(branches)]
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(pack_stream):
+                with torch.cuda.graph(g, stream=pack_stream):
+                    for st in side:
+                        st.wait_stream(pack_stream)
+                    for j, (mb, (o, c, q)) in enumerate(zip(mbs, gouts)):
+                        w.pack(mb, o, c, q, stream=side[j % branches] if branches > 1 else pack_stream)
+                    for st in side:
+                        pack_stream.wait_stream(st)
+            with torch.cuda.stream(pack_stream):
                 g.replay()
-        g1.record(pack_stream)
-        torch.cuda.synchronize()
-        graph_s = g0.elapsed_time(g1) * 1e-3 / args.steps
-        del g, gouts
+            torch.cuda.synchronize()
+            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            g0.record(pack_stream)
+            with torch.cuda.stream(pack_stream):
+                for _ in range(args.steps):
+                    g.replay()
+            g1.record(pack_stream)
+            torch.cuda.synchronize()
+            del g
+            return g0.elapsed_time(g1) * 1e-3 / args.steps
+
+        graph_s = replay_s(1)
+        graph2_s = replay_s(2)
+        del gouts
 
     value = step_bytes * args.steps / wall / 1e9
     kernel_gbps = float(mb_bytes.mean()) / launch_s / 1e9
@@ -714,6 +731,8 @@ def main() -> int:
                      "traffic_over_algorithmic": (round(traffic / mean_bytes, 4) if traffic else None)},
     }
     if graph_s is not None:
+        result["graph_pack_two_chains"] = {"replay_ms": round(graph2_s * 1e3, 4),
+                                           "GBps": round(step_bytes / graph2_s / 1e9, 2)}
         result["graph_pack"] = {"packs_per_replay": n_packs, "replay_ms": round(graph_s * 1e3, 4),
                                 "GBps": round(step_bytes / graph_s / 1e9, 2),
                                 "per_call_GBps_same_packs": round(step_bytes / (launch_s * n_packs) / 1e9, 2)}
