@@ -168,7 +168,8 @@ fp_status pool_destroy(fp_pool* p);
  * possibly partial). All-or-nothing. *out_sample_id (host) receives a new id,
  * never reused, >= 1.
  * Errors: EINVAL (positions, counts, ids, empty sample, wish, more than 2^31
- *         16-byte vectors of visual rows), EALIGN,
+ *         16-byte vectors of visual rows, vis_emb in memory the GPU cannot
+ *         read, such as ordinary pageable host memory), EALIGN,
  * ENOMEM (pages, slots or metadata exhausted), EHIP. */
 fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
                             const int32_t* img_pos, const int32_t* img_ntok, int32_t n_img,

@@ -649,12 +649,15 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   const uint8_t* vis_dev = nullptr;
   if (vis_emb && n_vis > 0) {
     if ((uintptr_t)vis_emb % 16) return fail(FP_EALIGN, "vis_emb must be 16-byte aligned");
-    hipPointerAttribute_t attr;
+    // Ordinary (unregistered) host memory would fault the write kernel.
+    hipPointerAttribute_t attr{};
     if (hipPointerGetAttributes(&attr, vis_emb) != hipSuccess) {
       (void)hipGetLastError();
       return fail(FP_EINVAL, "vis_emb is not device-accessible memory");
     }
-    vis_dev = (const uint8_t*)(attr.devicePointer ? attr.devicePointer : vis_emb);
+    if (attr.type == hipMemoryTypeUnregistered || !attr.devicePointer)
+      return fail(FP_EINVAL, "vis_emb is ordinary host memory, not device-accessible");
+    vis_dev = (const uint8_t*)attr.devicePointer;
   }
   const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);
   int64_t meta_off = 0;

@@ -123,11 +123,15 @@ def _arr(a, dtype, ptype):
 
 
 def _ptr(x) -> Optional[int]:
-    """Device address of a torch tensor / integer / None."""
+    """Device address of a torch tensor / integer / None. A tensor must live
+    on the GPU or in pinned host memory: the kernels read and write it
+    directly, and an ordinary CPU tensor's address would fault them."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if not (x.is_cuda or x.is_pinned()):
+        raise ValueError("tensor argument must be on the GPU or in pinned host memory")
     return int(x.data_ptr())
 
 

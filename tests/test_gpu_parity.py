@@ -205,8 +205,13 @@ def test_error_paths(fp):
             fp.pool_write_sample(pool, **kw)
         assert e.value.code == code
         assert fp.pool_stats(pool) == before
+    with pytest.raises(ValueError):               # ordinary host memory never reaches a kernel
+        fp.pool_write_sample(pool, [1], [0], [2], torch.zeros((2, cfg.hidden), dtype=torch.int16))
+    assert fp.pool_stats(pool) == before
     sid = w.ids[0]
     n = specs[0].length
+    with pytest.raises(ValueError):
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, torch.empty((n, cfg.hidden), dtype=torch.int16), n)
     with pytest.raises(fp.FlowPoolError) as e:
         fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out, n - 1)
     assert e.value.code == "ECAPACITY"
@@ -227,6 +232,37 @@ def test_error_paths(fp):
             call()
         assert e.value.code == "ENOENT"
     w.close()
+
+
+def test_write_from_pinned_host_memory(fp):
+    """A producer may hand over its embeddings in pinned host memory (mapped
+    into the GPU's address space): the write kernel reads them over PCIe and
+    the pack is the same as from device memory."""
+    say("case pinned-host producer buffer")
+    H, P, vocab = 512, 16, 50
+    specs = [SampleSpec(np.array([3, 4, 5], np.int32), np.array([1, 3], np.int32), np.array([40, 7], np.int32)),
+             SampleSpec(np.zeros(0, np.int32), np.array([0], np.int32), np.array([33], np.int32))]
+    table = tagged_table(vocab, H, 3)
+    vis = [tagged_vis(i, s.n_vis, H, 3) for i, s in enumerate(specs)]
+    pool = fp.pool_create(hidden=H, page_tokens=P, hbm_pages=16, vocab=vocab, alloc="scatter")
+    try:
+        ids = []
+        for s, v in zip(specs, vis):
+            hv = torch.from_numpy(v.view(np.int16)).pin_memory()
+            ids.append(fp.pool_write_sample(pool, s.text_ids, s.img_pos, s.img_ntok, hv))
+            torch.cuda.synchronize()              # hv must outlive the write
+        n = sum(s.length for s in specs)
+        out = torch.full((n, H), 0x2222, dtype=torch.int16, device="cuda")
+        cu = torch.empty((3,), dtype=torch.int32, device="cuda")
+        pos = torch.empty((n,), dtype=torch.int32, device="cuda")
+        m, _ = fp.pack_microbatch(pool, ids, to_dev(table), vocab, out, n, cu, pos)
+        torch.cuda.synchronize()
+        want = definitional_pack(specs, vis, table)
+        assert m == n and np.array_equal(to_host(out), want[0])
+        assert cu.cpu().numpy().tolist() == want[1].tolist() and pos.cpu().numpy().tolist() == want[2].tolist()
+    finally:
+        torch.cuda.synchronize()
+        fp.pool_destroy(pool)
 
 
 def test_tier_mask_split(fp):

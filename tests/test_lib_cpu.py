@@ -92,6 +92,15 @@ def test_null_pool_is_rejected_by_every_pool_call():
     assert fp.pool_destroy(0) is None                          # NULL is accepted
 
 
+def test_bindings_refuse_ordinary_host_tensors():
+    """Tensors handed to a kernel must be device or pinned memory; an ordinary
+    CPU tensor is refused before the library is called."""
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        fp._ptr(torch.zeros(8, dtype=torch.int16))
+    assert fp._ptr(None) is None and fp._ptr(4096) == 4096
+
+
 def test_pool_create_rejects_gva_span_beyond_2_52():
     with pytest.raises(fp.FlowPoolError) as e:
         fp.pool_create(hidden=1 << 20, page_tokens=1 << 20, hbm_pages=1 << 20)
