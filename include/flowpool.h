@@ -167,8 +167,8 @@ fp_status pool_destroy(fp_pool* p);
  * The sample's visual rows fill its own pages densely in order (last page
  * possibly partial). All-or-nothing. *out_sample_id (host) receives a new id,
  * never reused, >= 1.
- * Errors: EINVAL (positions, counts, ids, empty sample, wish, more than 2^31
- *         16-byte vectors of visual rows, vis_emb in memory the GPU cannot
+ * Errors: EINVAL (positions, counts, ids, empty sample, wish, more than
+ *         2^31 - 1024 16-byte vectors of visual rows, vis_emb in memory the GPU cannot
  *         read, such as ordinary pageable host memory), EALIGN,
  * ENOMEM (pages, slots or metadata exhausted), EHIP. */
 fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
@@ -331,7 +331,9 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
  *                    copies rows on host-tier pages; FP_TIER_MASK_ALL both.
  *                    Two launches with the two masks write what one ALL does.
  * Asynchronous on `stream`. Duplicated ids are packed twice.
- * Errors: EINVAL, ENOENT, ECAPACITY (sum of l > out_rows_cap), EALIGN, EHIP. */
+ * Errors: EINVAL (also more than 1024 samples or images, or a microbatch of
+ * more than 2^31 - 1024 16-byte vectors, i.e. n_tokens * 2H / 16), ENOENT,
+ * ECAPACITY (sum of l > out_rows_cap), EALIGN, EHIP. */
 fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n,
                           const void* embed_table, int64_t vocab,
                           void* out_emb, int64_t out_rows_cap,

@@ -54,6 +54,11 @@ constexpr int64_t kDefaultMaxSamples = 65536;
 constexpr int64_t kDefaultMetaBytes = 64ll << 20;
 constexpr int64_t kDefaultChunkBytes = 1ll << 30;
 constexpr int64_t kMaxSampleRows = 1 << 24;
+// 16-byte vectors one pack or one write may move. The kernels index vectors
+// with 32-bit integers, and a thread forms the indices of its vectors (up to
+// 767 past its chunk's start) before testing them against the chunk's end,
+// so the count stays that far below 2^31.
+constexpr int64_t kMaxVectors = (1ll << 31) - 1024;
 constexpr int kRing = 8;
 
 // Restores the caller's current device on scope exit.
@@ -630,7 +635,7 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
   }
   const int64_t len = n_vis + n_text;
   if (len < 1 || len > kMaxSampleRows) return fail(FP_EINVAL, "sample length %lld", (long long)len);
-  if (n_vis * (p->rb / 16) > 0x7fffffffll)
+  if (n_vis * (p->rb / 16) > kMaxVectors)
     return fail(FP_EINVAL, "%lld visual rows of %lld bytes are too many for one write", (long long)n_vis,
                 (long long)p->rb);
   for (int32_t i = 0; i < n_text; ++i)
@@ -1204,7 +1209,8 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
     return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
   if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
   const int64_t vpr = p->rb / 16;
-  if (total * vpr > 0x7fffffffll) return fail(FP_EINVAL, "microbatch of %lld rows is too large", (long long)total);
+  if (total * vpr > kMaxVectors)
+    return fail(FP_EINVAL, "microbatch of %lld rows of %lld bytes is too large", (long long)total, (long long)p->rb);
   if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
   if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
     if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");

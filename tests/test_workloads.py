@@ -50,3 +50,16 @@ def test_bf16_conversion_rne():
     assert visual_rows_np(CONFIGS["tiny"], 0, 3, 5).shape == (5, 256)
     t = page_tier_draws(0, 1, 1000)
     assert set(np.unique(t)) == {0, 1} and 400 < t.sum() < 600
+
+
+def test_pattern_rows_generator_matches_host_twin():
+    """The block-wise tensor generator of large inputs and its row-at-a-time
+    host twin give the same bits (checked on the CPU, across block edges and
+    past 2^16 rows, where the row tag's high word starts to count)."""
+    torch = pytest.importorskip("torch")
+    from tagging import pattern_base, pattern_row, pattern_rows_dev
+    base = pattern_base(24, 5)
+    got = pattern_rows_dev(3, 70000, 24, 5, block=4099, device="cpu").numpy().view(np.uint16)
+    for r in [0, 1, 4098, 4099, 65535, 65536, 69999] + list(range(96, 200)):
+        assert np.array_equal(got[r], pattern_row(3, r, 24, 5, base)), r
+    assert got[65536, 3] == 1 and got[65536, 2] == 0
