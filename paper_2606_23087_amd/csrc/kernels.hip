@@ -57,9 +57,24 @@ __device__ __forceinline__ T ld(const void* p) {
   }
 }
 
+// The pack's leading kernel arguments: everything a wave needs to address its
+// row's bucket entry. They are separate scalar arguments, ahead of PackArgs,
+// so that the hardware preloads them into scalar registers at wave launch
+// (kernarg preloading); the first load of the row lookup then leaves at once,
+// alongside the kernel-argument loads of the rest.
+struct PackHead {
+  int32_t g0, g1, t1, t2;   // chunk geometry (as in PackArgs)
+  uint64_t div_mul;         // e / (row_bytes / 16) == (e * div_mul) >> div_shift
+  int32_t div_shift;
+  int32_t bucket_shift;
+  const uint8_t* tb;        // run table: staged copy, or null = the one in PackArgs
+  int32_t off_bucket;       // byte offset of the bucket index in the run table
+  int32_t total;            // vectors of the microbatch
+};
+
 // e / (row_bytes / 16) as a multiply and a shift (host-computed constants).
-__device__ __forceinline__ int div_vpr(const PackArgs& a, int e) {
-  return (int)(((uint64_t)(uint32_t)e * a.div_mul) >> a.div_shift);
+__device__ __forceinline__ int div_vpr(const PackHead& h, int e) {
+  return (int)(((uint64_t)(uint32_t)e * h.div_mul) >> h.div_shift);
 }
 
 // One run, as a single 16-byte load.
@@ -72,9 +87,14 @@ __device__ __forceinline__ PackRun ld_run(const PackRun* rp) {
 // Run holding packed row `row`: the bucket of the row names a run starting
 // at or before it; runs that end at or before the row are stepped over.
 template <bool kScalar>
-__device__ __forceinline__ PackRun run_of(const PackArgs& a, const uint8_t* tb, int row, int* s_out = nullptr) {
-  const int b = row >> a.bucket_shift;
-  const uint32_t w = ld<kScalar, uint32_t>(tb + a.off_bucket + 4 * (b >> 1));
+__device__ __forceinline__ uint32_t bucket_word(const PackHead& h, const uint8_t* tb, int row) {
+  return ld<kScalar, uint32_t>(tb + h.off_bucket + 4 * ((row >> h.bucket_shift) >> 1));
+}
+
+template <bool kScalar>
+__device__ __forceinline__ PackRun run_of(const PackHead& h, const PackArgs& a, const uint8_t* tb, int row,
+                                          uint32_t w, int* s_out = nullptr) {
+  const int b = row >> h.bucket_shift;
   int s = (int)((b & 1) ? (w >> 16) : (w & 0xffffu));
   const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
   PackRun r = ld_run<kScalar>(runs + s);
@@ -116,47 +136,53 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
 // scalar loads, so the only vector memory loads are the copies. Chunks of
 // many short rows resolve one row per lane.
 template <int VPT>
-__global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
+__global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int32_t t1, int32_t t2,
+                                                      uint64_t div_mul, int32_t div_shift, int32_t bucket_shift,
+                                                      const uint8_t* staged, int32_t off_bucket, int32_t total,
+                                                      PackArgs a) {
   constexpr int kChunk = kPackBlock * VPT;       // vectors of a full chunk
   extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
+  const PackHead h{g0, g1, t1, t2, div_mul, div_shift, bucket_shift, staged, off_bucket, total};
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  // Every kernel argument the row resolution uses, read in one batch of
-  // scalar loads instead of in several batches on the way.
-  asm volatile("" : : "s"(a.staged), "s"(a.off_runs), "s"(a.off_bucket), "s"(a.bucket_shift),
-               "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start), "s"(a.pt_mul),
-               "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
-               "s"(a.tier_mask), "s"(a.row_bytes), "s"(a.n_tokens), "s"(a.div_mul),
-               "s"(a.div_shift), "s"(a.g0), "s"(a.g1), "s"(a.t1), "s"(a.t2));
-  const uint8_t* tb = a.staged ? a.staged : reinterpret_cast<const uint8_t*>(a.lens);
+  const uint8_t* tb = h.tb ? h.tb : reinterpret_cast<const uint8_t*>(a.lens);
   int my_skip = 0;                                  // a row of this chunk is not copied
 
-  const bool write_meta = (a.tier_mask & 1) != 0;
-  const int vpr = a.row_bytes >> 4;
-  const int total = a.n_tokens * vpr;                 // the host keeps this below 2^31
   const int bx = (int)blockIdx.x;
   int v0, v1;
-  if (bx < a.g0) {
+  if (bx < h.g0) {
     v0 = bx * kChunk;
     v1 = v0 + kChunk;
-  } else if (bx < a.g1) {
-    v0 = a.t1 + (bx - a.g0) * kTail1Vecs;
-    v1 = min(v0 + kTail1Vecs, a.t2);
+  } else if (bx < h.g1) {
+    v0 = h.t1 + (bx - h.g0) * kTail1Vecs;
+    v1 = min(v0 + kTail1Vecs, h.t2);
   } else {
-    v0 = a.t2 + (bx - a.g1) * kTail2Vecs;
-    v1 = min(v0 + kTail2Vecs, total);
+    v0 = h.t2 + (bx - h.g1) * kTail2Vecs;
+    v1 = min(v0 + kTail2Vecs, h.total);
   }
-  const int r0 = div_vpr(a, v0);
-  const int rows = v1 > v0 ? div_vpr(a, v1 - 1) - r0 + 1 : 0;
+  const int r0 = div_vpr(h, v0);
+  const int rows = v1 > v0 ? div_vpr(h, v1 - 1) - r0 + 1 : 0;
+  // The bucket entry of the wave's first row (a row of the chunk; row 0 of an
+  // empty pack, whose inline index always has an entry), then the other kernel
+  // arguments the row resolution uses in one batch of scalar loads, in flight
+  // together with it (the compiler would otherwise split the batch and load
+  // it first).
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t w0 = bucket_word<true>(h, tb, r0 + min(wave, max(rows - 1, 0)));
+  asm volatile("" : : "s"(w0), "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start),
+               "s"(a.pt_mul), "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
+               "s"(a.tier_mask), "s"(a.row_bytes));
+  const bool write_meta = (a.tier_mask & 1) != 0;
+  const int vpr = a.row_bytes >> 4;
 
   if (rows <= kWaveRows * (kPackBlock / 64)) {
     // Wave w resolves rows w, w + 4, ... of the chunk, so the dependent load
     // chains of different rows overlap.
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
-      const uint64_t src = row_source<true>(a, run_of<true>(a, tb, row), row);
+      const uint32_t w = t == wave ? w0 : bucket_word<true>(h, tb, row);
+      const uint64_t src = row_source<true>(a, run_of<true>(h, a, tb, row, w), row);
       if (lane == 0) {
         s_src[t] = src;
         if (!src) my_skip = 1;
@@ -165,7 +191,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
   } else {
     for (int t = tid; t < rows; t += kPackBlock) {
       const int row = r0 + t;
-      const uint64_t src = row_source<false>(a, run_of<false>(a, tb, row), row);
+      const uint64_t src = row_source<false>(a, run_of<false>(h, a, tb, row, bucket_word<false>(h, tb, row)), row);
       s_src[t] = src;
       if (!src) my_skip = 1;
     }
@@ -189,7 +215,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
     from[u] = 0;
     live[u] = false;
     if (e < v1) {
-      const int row = div_vpr(a, e);
+      const int row = div_vpr(h, e);
       const uint64_t base = s_src[row - r0];
       live[u] = base != 0;
       from[u] = live[u] ? base + (uint64_t)(e - row * vpr) * 16 : 0;
@@ -242,7 +268,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(PackArgs a) {
         const int first = blk * 64, row = first + lane;
         const int last = min(first + 63, a.n_tokens - 1);
         int s;
-        PackRun r = run_of<true>(a, tb, first, &s);
+        PackRun r = run_of<true>(h, a, tb, first, bucket_word<true>(h, tb, first), &s);
         int start = r.head & 0x7fffffff;
         while (r.end <= last) {
           const int next = r.end;
@@ -355,10 +381,13 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
   const int64_t grid64 = a.g1 + (vecs - a.t2 + kTail2Vecs - 1) / kTail2Vecs;
   const int grid = grid64 > 0 ? (int)grid64 : 1;
+  const int32_t total = (int32_t)vecs;               // the host keeps this below 2^31
   if (a.vpt == 2)
-    hipLaunchKernelGGL(k_pack<2>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
+    hipLaunchKernelGGL(k_pack<2>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1, a.t1, a.t2,
+                       a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_bucket, total, a);
   else
-    hipLaunchKernelGGL(k_pack<kVecsPerThread>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a);
+    hipLaunchKernelGGL(k_pack<kVecsPerThread>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1,
+                       a.t1, a.t2, a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_bucket, total, a);
   return hipGetLastError();
 }
 

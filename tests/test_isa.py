@@ -7,6 +7,10 @@
   so it does not insert them).
 - The pack kernels spill nothing to scratch and stay within the registers
   that keep 8 waves per SIMD resident.
+- The pack kernels' leading scalar arguments (12 dwords) arrive preloaded in
+  scalar registers, and the first load of the row lookup (the bucket entry)
+  is issued before the wait for the other kernel arguments, so the two are in
+  flight together.
 """
 
 import os
@@ -26,8 +30,9 @@ def isa(tmp_path_factory):
     if not os.path.exists(hipcc) and not shutil.which("hipcc"):
         pytest.skip("hipcc not available")
     out = tmp_path_factory.mktemp("isa") / "kernels.s"
-    cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    from paper_2606_23087_amd.build import HIPCC_FLAGS
+    flags = [f for f in HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    cmd = [hipcc, *flags, "--cuda-device-only", "-S",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC, os.path.join(CSRC, "kernels.hip"), "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr[-2000:]
@@ -67,3 +72,19 @@ def test_pack_kernels_keep_full_occupancy(isa):
         scratch = int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", meta).group(1))
         assert scratch == 0, name
         assert vgpr <= 64, (name, vgpr)         # 512 VGPRs per lane / 8 waves
+
+
+def test_pack_kernels_preload_their_head_arguments(isa):
+    packs = {k: v for k, v in _kernels(isa).items() if "k_pack" in k}
+    assert len(packs) == 2
+    for name, (lines, meta) in packs.items():
+        assert re.search(r"\.amdhsa_user_sgpr_kernarg_preload_length 12\b", meta), name
+        # Entry with preloaded arguments: 256 bytes past the kernel symbol,
+        # after the compatibility prologue that loads them for firmware that
+        # does not preload. There, the first scalar load that is not a
+        # kernel-argument load (the bucket entry) comes before the first wait.
+        entry = next(i for i, l in enumerate(lines) if l.startswith(".LBB") and "_0:" in l)
+        body = [l.strip() for l in lines[entry:]]
+        first_wait = next(i for i, l in enumerate(body) if l.startswith("s_waitcnt"))
+        loads = [l for l in body[:first_wait] if l.startswith("s_load")]
+        assert loads and not loads[0].split(",")[1].strip().startswith("s[0:1]"), (name, loads[:3])
