@@ -71,14 +71,17 @@ def pack_bytes(cfg, specs) -> int:
 
 def kernel_source_hash() -> str:
     """Hash of the kernel sources (kernels.hip and the launch-layout header
-    fp_internal.h) with comments and whitespace removed, so that only a change
-    to the code itself invalidates recorded counters."""
+    fp_internal.h) with comments and whitespace removed, and of the hipcc
+    flags they are built with, so that only a change to the code or its
+    compilation invalidates recorded counters."""
+    from paper_2606_23087_amd.build import HIPCC_FLAGS
     src = ""
     for name in ("kernels.hip", "fp_internal.h"):
         src += open(os.path.join(ROOT, "paper_2606_23087_amd", "csrc", name)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     src = re.sub(r"//[^\n]*", "", src)
     src = re.sub(r"\s+", "", src)
+    src += " ".join(HIPCC_FLAGS)
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
