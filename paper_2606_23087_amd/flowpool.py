@@ -135,6 +135,22 @@ def _ptr(x) -> Optional[int]:
     return int(x.data_ptr())
 
 
+# Hidden size of each pool created through these bindings, to check buffer
+# sizes before the kernels touch them (pools created elsewhere are not checked).
+_HIDDEN = {}
+
+
+def _buf(x, nbytes: int, name: str) -> Optional[int]:
+    """Like ``_ptr``; a tensor must also be contiguous and hold ``nbytes``."""
+    if x is None or isinstance(x, int):
+        return _ptr(x)
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if x.numel() * x.element_size() < nbytes:
+        raise ValueError(f"{name} holds {x.numel() * x.element_size()} bytes, the call needs {nbytes}")
+    return _ptr(x)
+
+
 def _stream(s) -> Optional[int]:
     if s is None:
         import torch
@@ -170,11 +186,13 @@ def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int =
     cfg.pack_cus = pack_cus
     out = _P()
     _check(_lib.pool_create(C.byref(cfg), C.byref(out)), "pool_create")
+    _HIDDEN[int(out.value)] = hidden
     return int(out.value)
 
 
 def pool_destroy(pool: int) -> None:
     _check(_lib.pool_destroy(pool), "pool_destroy")
+    _HIDDEN.pop(pool, None)
 
 
 def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page_tier_wish=None,
@@ -184,7 +202,9 @@ def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page
     v, vp = _arr(img_ntok, np.int32, _i32p)
     w, wp = _arr(page_tier_wish, np.uint8, _u8p)
     sid = C.c_uint64()
-    _check(_lib.pool_write_sample(pool, tp, len(t), pp, vp, len(p), _ptr(vis_emb), wp, _stream(stream),
+    rb = 2 * _HIDDEN.get(pool, 0)
+    vis = _buf(vis_emb, int(v.sum(dtype=np.int64)) * rb if v is not None else 0, "vis_emb")
+    _check(_lib.pool_write_sample(pool, tp, len(t), pp, vp, len(p), vis, wp, _stream(stream),
                                   C.byref(sid)), "pool_write_sample")
     return int(sid.value)
 
@@ -305,8 +325,12 @@ def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out
     ids, idp = _arr(sample_ids, np.uint64, _u64p)
     n_tok = C.c_int32()
     mx = C.c_int32()
-    _check(_lib.pack_microbatch(pool, idp, len(ids), _ptr(embed_table), vocab, _ptr(out_emb), out_rows_cap,
-                                _ptr(out_cu_seqlens), _ptr(out_position_ids), C.byref(n_tok), C.byref(mx),
+    rb = 2 * _HIDDEN.get(pool, 0)
+    cap = max(int(out_rows_cap), 0)
+    _check(_lib.pack_microbatch(pool, idp, len(ids), _buf(embed_table, max(int(vocab), 0) * rb, "embed_table"), vocab,
+                                _buf(out_emb, cap * rb, "out_emb"), out_rows_cap,
+                                _buf(out_cu_seqlens, 4 * (len(ids) + 1), "out_cu_seqlens"),
+                                _buf(out_position_ids, 4 * cap, "out_position_ids"), C.byref(n_tok), C.byref(mx),
                                 tier_mask, _stream(stream)), "pack_microbatch")
     return int(n_tok.value), int(mx.value)
 

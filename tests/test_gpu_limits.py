@@ -99,7 +99,7 @@ def test_largest_microbatch(fp):
         extra = fp.pool_write_sample(pool, [3], [], [])
         before = fp.pool_stats(pool)
         with pytest.raises(fp.FlowPoolError) as e:
-            fp.pack_microbatch(pool, ids + [extra], table, VOCAB, out, out.shape[0], cu, pos)
+            fp.pack_microbatch(pool, ids + [extra], table, VOCAB, out, out.shape[0], None, pos)
         assert e.value.code == "EINVAL"
         with pytest.raises(fp.FlowPoolError) as e:
             fp.pool_write_sample(pool, [], [0], [max_rows + 1])

@@ -212,6 +212,12 @@ def test_error_paths(fp):
     n = specs[0].length
     with pytest.raises(ValueError):
         fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, torch.empty((n, cfg.hidden), dtype=torch.int16), n)
+    with pytest.raises(ValueError):               # a buffer smaller than the call says
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out[:n - 1], n)
+    with pytest.raises(ValueError):
+        fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out, n, cu, pos[:n - 1])
+    with pytest.raises(ValueError):
+        fp.pack_microbatch(pool, [sid], w.table[:cfg.vocab - 1], cfg.vocab, out, n)
     with pytest.raises(fp.FlowPoolError) as e:
         fp.pack_microbatch(pool, [sid], w.table, cfg.vocab, out, n - 1)
     assert e.value.code == "ECAPACITY"

@@ -99,6 +99,11 @@ def test_bindings_refuse_ordinary_host_tensors():
     with pytest.raises(ValueError):
         fp._ptr(torch.zeros(8, dtype=torch.int16))
     assert fp._ptr(None) is None and fp._ptr(4096) == 4096
+    x = torch.zeros((4, 8), dtype=torch.int16)
+    with pytest.raises(ValueError, match="contiguous"):
+        fp._buf(x.t(), 64, "out_emb")
+    with pytest.raises(ValueError, match="needs 65"):
+        fp._buf(x, 65, "out_emb")
 
 
 def test_pool_create_rejects_gva_span_beyond_2_52():
