@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FP_ABI_VERSION 2
+#define FP_ABI_VERSION 3
 
 typedef struct fp_pool fp_pool;   /* opaque; created and owned by the library */
 typedef int32_t fp_status;
@@ -99,8 +99,15 @@ enum { FP_TIER_MASK_HBM = 1, FP_TIER_MASK_HOST = 2, FP_TIER_MASK_ALL = 3 };
  *                a seeded permutation of frames (placement-independence tests).
  *  chunk_bytes   the library allocates tier backing in chunks of this many
  *                bytes (rounded down to whole pages); 0 = 1 GiB.
- *  hbm_backing, host_backing  reserved, must be NULL (the library allocates
- *                and frees all backing memory).
+ *  hbm_backing   NULL = the library allocates the HBM tier's backing;
+ *                else caller-owned device memory of `device`, 256-byte
+ *                aligned, with at least hbm_pages * 2H * page_tokens bytes
+ *                from this address inside one allocation (e.g. a torch
+ *                tensor). The pool binds its frames to it in order and never
+ *                frees it; it must stay valid until pool_destroy.
+ *  host_backing  the same for the host tier: caller-owned pinned host memory
+ *                mapped into the GPU at the same address (hipHostMalloc, a
+ *                torch pinned tensor), host_pages * 2H * page_tokens bytes.
  *  pack_cus      compute units the pack's chunk geometry is sized for (the
  *                chunks of its last wave and a half of resident workgroups are
  *                8 KiB, then 4 KiB); 0 = the device's count. It changes timing
@@ -142,7 +149,9 @@ void fp_config_init(fp_pool_config* cfg);
 /* Create a pool (Sec. 3.2 initialisation): reserve this rank's GVA segments,
  * allocate the tiers' physical memory, bind it to the GVA pages through the
  * page table and upload the table to the device. cfg: host. *out receives the
- * pool handle. Errors: EINVAL (bad field), EHIP (allocation failed). */
+ * pool handle. Errors: EINVAL (bad field; a backing of the wrong kind, device
+ * or size), EALIGN (a backing not 256-byte aligned), EHIP (allocation
+ * failed). */
 fp_status pool_create(const fp_pool_config* cfg, fp_pool** out);
 
 /* Destroy a pool and free all its memory. The caller must have synchronised

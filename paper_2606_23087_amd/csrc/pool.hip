@@ -207,7 +207,8 @@ struct fp_pool {
   uint64_t max_size[2] = {0, 0};
   // physical backing
   std::vector<void*> chunks[2];
-  int64_t frames_per_chunk = 1;
+  int64_t frames_per_chunk[2] = {1, 1};
+  bool owned[2] = {true, true};       // false: the caller's backing, never freed here
   std::vector<uint64_t> pte;          // host mirror, index = global vpn
   uint64_t* pte_dev = nullptr;
   // allocators, page index inside the tier's segment
@@ -289,8 +290,10 @@ void free_all(fp_pool* p) {
     if (s.ev) (void)hipEventDestroy(s.ev);
     s = Stage{};
   }
-  for (void* c : p->chunks[0]) (void)hipFree(c);
-  for (void* c : p->chunks[1]) (void)hipHostFree(c);
+  if (p->owned[0])
+    for (void* c : p->chunks[0]) (void)hipFree(c);
+  if (p->owned[1])
+    for (void* c : p->chunks[1]) (void)hipHostFree(c);
   p->chunks[0].clear();
   p->chunks[1].clear();
   if (p->pte_dev) (void)hipFree(p->pte_dev);
@@ -434,6 +437,40 @@ bool capturing(hipStream_t stream) {
   return cs != hipStreamCaptureStatusNone;
 }
 
+// A caller-provided tier backing: 256-byte aligned, at least `bytes` long
+// inside one allocation, and of the tier's kind: device memory of `device`
+// (HBM tier), or pinned host memory mapped into the GPU at the same address
+// (host tier).
+fp_status check_backing(int tier, void* ptr, uint64_t bytes, int device) {
+  const char* name = tier ? "host_backing" : "hbm_backing";
+  if (bytes == 0) return fail(FP_EINVAL, "%s given for a tier without pages", name);
+  if ((uintptr_t)ptr % 256) return fail(FP_EALIGN, "%s must be 256-byte aligned", name);
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(FP_EINVAL, "%s is not memory the HIP runtime knows", name);
+  }
+  if (tier == 0 && (attr.type != hipMemoryTypeDevice || attr.device != device))
+    return fail(FP_EINVAL, "hbm_backing must be device memory of device %d", device);
+  if (tier == 1) {
+    void* dptr = nullptr;
+    if (attr.type != hipMemoryTypeHost || hipHostGetDevicePointer(&dptr, ptr, 0) != hipSuccess || dptr != ptr) {
+      (void)hipGetLastError();
+      return fail(FP_EINVAL, "host_backing must be pinned host memory mapped at the same address");
+    }
+  }
+  void* base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, ptr) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(FP_EINVAL, "%s: its allocation's extent is unknown", name);
+  }
+  if ((uint64_t)(uintptr_t)ptr + bytes > (uint64_t)(uintptr_t)base + (uint64_t)size)
+    return fail(FP_EINVAL, "%s: %llu bytes needed, %llu left in its allocation", name, (unsigned long long)bytes,
+                (unsigned long long)((uintptr_t)base + size - (uintptr_t)ptr));
+  return FP_OK;
+}
+
 fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
                  int32_t n_mb, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
                  int32_t* mb_max) {
@@ -496,7 +533,6 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
   if (c.world_size != 1 || c.rank != 0)
     return fail(FP_EINVAL, "world_size/rank %d/%d: this library runs one process", c.world_size, c.rank);
   if (c.vocab < 0 || c.vocab > (1ll << 31)) return fail(FP_EINVAL, "vocab %lld", (long long)c.vocab);
-  if (c.hbm_backing || c.host_backing) return fail(FP_EINVAL, "caller-provided backing is not supported");
   if (c.pack_cus < 0 || c.pack_cus > 65536 || c.reserved != 0) return fail(FP_EINVAL, "pack_cus %d / reserved", c.pack_cus);
   if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
   if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
@@ -546,11 +582,21 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
     return s;
   };
 
-  // Physical backing in chunks of whole pages.
-  p->frames_per_chunk = std::max<int64_t>(1, c.chunk_bytes / p->pb);
+  // Physical backing: the caller's buffer as one chunk, or library chunks of
+  // whole pages.
+  void* backing[2] = {c.hbm_backing, c.host_backing};
   for (int t = 0; t < 2; ++t) {
-    for (int64_t f = 0; f < p->n_pages[t]; f += p->frames_per_chunk) {
-      const int64_t frames = std::min(p->frames_per_chunk, p->n_pages[t] - f);
+    if (backing[t]) {
+      fp_status bs = check_backing(t, backing[t], (uint64_t)p->n_pages[t] * (uint64_t)p->pb, c.device);
+      if (bs != FP_OK) return bail(bs);
+      p->chunks[t].push_back(backing[t]);
+      p->frames_per_chunk[t] = std::max<int64_t>(1, p->n_pages[t]);
+      p->owned[t] = false;
+      continue;
+    }
+    p->frames_per_chunk[t] = std::max<int64_t>(1, c.chunk_bytes / p->pb);
+    for (int64_t f = 0; f < p->n_pages[t]; f += p->frames_per_chunk[t]) {
+      const int64_t frames = std::min(p->frames_per_chunk[t], p->n_pages[t] - f);
       void* ptr = nullptr;
       hipError_t e = (t == 0) ? hipMalloc(&ptr, (size_t)(frames * p->pb))
                               : hipHostMalloc(&ptr, (size_t)(frames * p->pb), hipHostMallocMapped);
@@ -583,8 +629,8 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
     }
     for (int64_t i = 0; i < p->n_pages[t]; ++i) {
       const int64_t f = order[(size_t)i];
-      const uint64_t addr = (uint64_t)p->chunks[t][(size_t)(f / p->frames_per_chunk)] +
-                            (uint64_t)(f % p->frames_per_chunk) * (uint64_t)p->pb;
+      const uint64_t addr = (uint64_t)p->chunks[t][(size_t)(f / p->frames_per_chunk[t])] +
+                            (uint64_t)(f % p->frames_per_chunk[t]) * (uint64_t)p->pb;
       const int64_t vpn = (int64_t)((p->page_gva(t, i) - p->gva_start) / (uint64_t)p->pb);
       p->pte[(size_t)vpn] = addr | fp::PTE_VALID | (t ? fp::PTE_HOST : 0);
     }
@@ -896,14 +942,15 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
   struct Run { uint64_t src, dst, bytes; int src_chunk, dst_chunk; };
   std::vector<Run> runs;
   const int64_t P = p->cfg.page_tokens;
-  const uint64_t chunk_span = (uint64_t)p->frames_per_chunk * (uint64_t)p->pb;
   auto chunk_of = [&](uint64_t addr) {
     int id = 0;
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t) {
+      const uint64_t chunk_span = (uint64_t)p->frames_per_chunk[t] * (uint64_t)p->pb;
       for (void* c : p->chunks[t]) {
         if (addr >= (uint64_t)c && addr < (uint64_t)c + chunk_span) return id;
         ++id;
       }
+    }
     return -1;
   };
   for (size_t j = 0; j < recs.size(); ++j) {

@@ -33,7 +33,7 @@ except ImportError:
     pass
 
 _lib = C.CDLL(LIB_PATH)
-ABI_VERSION = 2   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
+ABI_VERSION = 3   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
 if _lib.fp_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI version {_lib.fp_abi_version()}, the bindings expect {ABI_VERSION}; rebuild it")
 
@@ -138,6 +138,8 @@ def _ptr(x) -> Optional[int]:
 # Hidden size of each pool created through these bindings, to check buffer
 # sizes before the kernels touch them (pools created elsewhere are not checked).
 _HIDDEN = {}
+# Caller-provided tier backings, kept alive while their pool exists.
+_BACKING = {}
 
 
 def _buf(x, nbytes: int, name: str) -> Optional[int]:
@@ -173,7 +175,11 @@ def fp_last_error() -> str:
 def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int = 0,
                 alloc: str = "contig", vocab: int = 0, device: int = 0, gva_start: int = 0,
                 max_samples: int = 0, meta_bytes: int = 0, frame_shuffle_seed: int = 0,
-                chunk_bytes: int = 0, world_size: int = 1, rank: int = 0, pack_cus: int = 0) -> int:
+                chunk_bytes: int = 0, world_size: int = 1, rank: int = 0, pack_cus: int = 0,
+                hbm_backing=None, host_backing=None) -> int:
+    """Create a pool. ``hbm_backing`` / ``host_backing``: optional caller-owned
+    memory for a tier (a device tensor / a pinned host tensor, or a raw address);
+    the bindings keep a tensor alive until ``pool_destroy``."""
     cfg = fp_pool_config()
     _lib.fp_config_init(C.byref(cfg))
     cfg.hidden, cfg.page_tokens = hidden, page_tokens
@@ -184,15 +190,20 @@ def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int =
     cfg.max_samples, cfg.meta_bytes = max_samples, meta_bytes
     cfg.frame_shuffle_seed, cfg.chunk_bytes = frame_shuffle_seed, chunk_bytes
     cfg.pack_cus = pack_cus
+    page_bytes = 2 * hidden * page_tokens
+    cfg.hbm_backing = _buf(hbm_backing, max(hbm_pages, 0) * page_bytes, "hbm_backing")
+    cfg.host_backing = _buf(host_backing, max(host_pages, 0) * page_bytes, "host_backing")
     out = _P()
     _check(_lib.pool_create(C.byref(cfg), C.byref(out)), "pool_create")
     _HIDDEN[int(out.value)] = hidden
+    _BACKING[int(out.value)] = (hbm_backing, host_backing)
     return int(out.value)
 
 
 def pool_destroy(pool: int) -> None:
     _check(_lib.pool_destroy(pool), "pool_destroy")
     _HIDDEN.pop(pool, None)
+    _BACKING.pop(pool, None)
 
 
 def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page_tier_wish=None,

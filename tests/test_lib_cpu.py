@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(fp.EXPORTED)
-    assert fp.fp_abi_version() == fp.ABI_VERSION == 2
+    assert fp.fp_abi_version() == fp.ABI_VERSION == 3
 
 
 def test_config_struct_matches_header():
@@ -104,6 +104,15 @@ def test_bindings_refuse_ordinary_host_tensors():
         fp._buf(x.t(), 64, "out_emb")
     with pytest.raises(ValueError, match="needs 65"):
         fp._buf(x, 65, "out_emb")
+
+
+def test_pool_create_checks_backing_tensors_before_the_library():
+    torch = pytest.importorskip("torch")
+    small = torch.zeros(4 * 16 * 512 - 1, dtype=torch.uint8)       # one byte short of 4 pages
+    with pytest.raises(ValueError, match="hbm_backing"):
+        fp.pool_create(hidden=256, page_tokens=16, hbm_pages=4, hbm_backing=small)
+    with pytest.raises(ValueError, match="host_backing"):
+        fp.pool_create(hidden=256, page_tokens=16, hbm_pages=4, host_pages=4, host_backing=small)
 
 
 def test_pool_create_rejects_gva_span_beyond_2_52():
