@@ -18,6 +18,15 @@ that fits nowhere is deferred (-1) and stays in the pool for a later plan.
 Since K*l + l^2 is strictly increasing in l, decreasing cost is decreasing
 length.
 
+The zig-zag policy (a reading: Alg. 1 deals its sorted microbatches to the
+data-parallel ranks in a snake order; applied here to samples and
+microbatches): samples in the same decreasing-cost order; the sample at
+position p of that order goes to microbatch snake(p), where snake runs
+0, 1, ..., M-1, M-1, ..., 1, 0, 0, 1, ... (period 2M); if that microbatch has
+no room, to the first microbatch with room among snake(p+1), snake(p+2), ...
+(2M positions cover every microbatch); deferred (-1) if none has room. The
+position advances with every sample, placed or deferred.
+
 Brute force enumerates every assignment for tiny inputs to give the optimal
 max-cost partition.
 """
@@ -58,6 +67,31 @@ def greedy_partition(lengths: Sequence[int], k: int, capacity: int, n_mb: int):
             assign[i] = best
             tokens[best] += int(lengths[i])
             mb_cost[best] += costs[i]
+    return assign, tokens, mb_cost
+
+
+def snake(p: int, n_mb: int) -> int:
+    """Microbatch of snake position p: 0, 1, ..., M-1, M-1, ..., 0, 0, 1, ..."""
+    q = p % (2 * n_mb)
+    return q if q < n_mb else 2 * n_mb - 1 - q
+
+
+def zigzag_partition(lengths: Sequence[int], k: int, capacity: int, n_mb: int):
+    """The zig-zag policy. Returns (assign, mb_tokens, mb_cost_scaled) like greedy_partition."""
+    n = len(lengths)
+    costs = [cost_scaled(int(l), k) for l in lengths]
+    order = sorted(range(n), key=lambda i: (-costs[i], i))
+    tokens = [0] * n_mb
+    mb_cost = [0] * n_mb
+    assign = [-1] * n
+    for p, i in enumerate(order):
+        for q in range(2 * n_mb):
+            j = snake(p + q, n_mb)
+            if tokens[j] + int(lengths[i]) <= capacity:
+                assign[i] = j
+                tokens[j] += int(lengths[i])
+                mb_cost[j] += costs[i]
+                break
     return assign, tokens, mb_cost
 
 

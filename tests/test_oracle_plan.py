@@ -1,7 +1,7 @@
 """Pins for the planner oracle (CPU only).
 
-- hand-worked costs, Eq. 3 values, greedy assignments and optima
-  (tests/golden/plan_worked_example.txt);
+- hand-worked costs, Eq. 3 values, greedy and zig-zag assignments and
+  optima (tests/golden/plan_worked_example.txt);
 - brute force on tiny inputs: the greedy never beats the optimum, and when
   the capacity does not bind it stays within Graham's LPT bound
   (4/3 - 1/(3M)) * OPT;
@@ -14,7 +14,8 @@ import math
 import numpy as np
 import pytest
 
-from oracle.plan import brute_force, cost_scaled, eq3_cost, greedy_partition, imbalance, members
+from oracle.plan import (brute_force, cost_scaled, eq3_cost, greedy_partition, imbalance, members, snake,
+                         zigzag_partition)
 from conftest import read_golden
 
 
@@ -48,12 +49,18 @@ def test_worked_examples():
             b = _kv_lists(f[arrow + 1:])
             assign, tok, cst = greedy_partition(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
             assert assign == b["assign"] and tok == b["tokens"] and cst == b["cost"]
+        elif f[0] == "zigzag":
+            arrow = f.index("->")
+            a = _kv_lists(f[1:arrow])
+            b = _kv_lists(f[arrow + 1:])
+            assign, tok, cst = zigzag_partition(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
+            assert assign == b["assign"] and tok == b["tokens"] and cst == b["cost"]
         elif f[0] == "opt":
             eq = f.index("=")
             a = _kv_lists(f[1:eq])
             opt, _ = brute_force(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
             assert opt == int(f[eq + 1])
-    assert seen == {"cost", "eq3", "greedy", "opt"}
+    assert seen == {"cost", "eq3", "greedy", "zigzag", "opt"}
 
 
 def _check_plan(lengths, capacity, n_mb, assign, tok, cst, k):
@@ -116,3 +123,27 @@ def test_members_keep_input_order_and_imbalance():
     assign = [1, 0, 1, -1, 0]
     assert members(assign, 3) == [[1, 4], [0, 2], []]
     assert imbalance([2, 4, 6]) == 1.5
+
+
+def test_snake_order():
+    assert [snake(p, 3) for p in range(13)] == [0, 1, 2, 2, 1, 0, 0, 1, 2, 2, 1, 0, 0]
+    assert [snake(p, 1) for p in range(4)] == [0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_zigzag_properties(seed):
+    """I8 for the zig-zag policy; without a binding capacity the sample at
+    sorted position p lands in snake(p); with one microbatch it is the greedy."""
+    rng = np.random.default_rng(600 + seed)
+    n, m, k = int(rng.integers(0, 30)), int(rng.integers(1, 6)), int(rng.integers(1, 5000))
+    lengths = rng.integers(1, 200, size=n).tolist()
+    for capacity in (10 ** 9, int(rng.integers(1, 600))):
+        assign, tok, cst = zigzag_partition(lengths, k, capacity, m)
+        _check_plan(lengths, capacity, m, assign, tok, cst, k)
+        if capacity == 10 ** 9:
+            order = sorted(range(n), key=lambda i: (-cost_scaled(lengths[i], k), i))
+            assert [assign[i] for i in order] == [snake(p, m) for p in range(n)]
+        for i, a in enumerate(assign):            # a deferred sample fit in no microbatch then,
+            if a < 0:                             # nor after (token counts only grow)
+                assert all(t + lengths[i] > capacity for t in tok)
+    assert zigzag_partition(lengths, k, 300, 1) == greedy_partition(lengths, k, 300, 1)
