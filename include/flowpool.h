@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FP_ABI_VERSION 3
+#define FP_ABI_VERSION 4
 
 typedef struct fp_pool fp_pool;   /* opaque; created and owned by the library */
 typedef int32_t fp_status;
@@ -222,13 +222,25 @@ fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages);
 fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t tier,
                        void* stream, int64_t* out_pages_moved);
 
+/* Planning policies. */
+enum {
+  FP_PLAN_LPT = 0,     /* each sample to the fitting microbatch of least accumulated cost */
+  FP_PLAN_ZIGZAG = 1   /* the sample at position p of the order to microbatch snake(p) */
+};
+
 /* Planner (Sec. 3.4): evaluate each sample's cost K*l + l^2 (the per-sample
  * cost l + l^2/K scaled by K; l = text + visual rows) with a GPU kernel over
- * the device sample table, then partition greedily into n_mb microbatches of
- * at most `capacity` tokens: samples by decreasing cost (ties: lower index),
- * each to the fitting microbatch of least accumulated cost (ties: lower
- * microbatch index), deferred (-1) if none fits; deferred samples stay
- * resident. Samples of one microbatch keep their order in sample_ids.
+ * the device sample table, then partition into n_mb microbatches of at most
+ * `capacity` tokens, samples taken by decreasing cost (ties: lower index):
+ *  FP_PLAN_LPT      each to the fitting microbatch of least accumulated cost
+ *                   (ties: lower microbatch index);
+ *  FP_PLAN_ZIGZAG   the sample at position p of that order to microbatch
+ *                   snake(p), snake = 0, 1, ..., n_mb-1, n_mb-1, ..., 0, 0, 1, ...
+ *                   (Alg. 1's zig-zag dealing, applied to samples); if it
+ *                   has no room, to the first with room among snake(p+1),
+ *                   snake(p+2), ...
+ * A sample that fits nowhere is deferred (-1) and stays resident. Samples of
+ * one microbatch keep their order in sample_ids.
  *  sample_ids       host uint64[n], distinct, resident.
  *  out_assign       host int32[n]: microbatch index or -1.
  *  out_mb_tokens    host int32[n_mb]: tokens per microbatch.
@@ -237,18 +249,19 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
  *                   (with out_mb_tokens this gives Eq. 3).
  *  out_sample_cost_scaled  host int64[n] or NULL: the per-sample costs.
  * Synchronous: returns after `stream` has finished the cost kernel.
- * Errors: EINVAL (n_mb < 1, capacity < 1, cost_k < 1, duplicates), ENOENT, EHIP. */
+ * Errors: EINVAL (n_mb outside [1, 2^20], capacity < 1, cost_k < 1, policy,
+ * duplicates), ENOENT, EHIP. */
 fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n,
-                            int32_t capacity, int32_t n_mb, int32_t cost_k,
+                            int32_t capacity, int32_t n_mb, int32_t cost_k, int32_t policy,
                             int32_t* out_assign, int32_t* out_mb_tokens,
                             int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
                             int64_t* out_sample_cost_scaled, void* stream);
 
-/* The greedy partition of plan_microbatches on given lengths and costs, host
- * only (no pool, no GPU). lengths: host int32[n] >= 1; costs_scaled: host
+/* The partition of plan_microbatches on given lengths and costs, host only
+ * (no pool, no GPU). lengths: host int32[n] >= 1; costs_scaled: host
  * int64[n]; outputs as in plan_microbatches. Errors: EINVAL. */
 fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
-                         int32_t capacity, int32_t n_mb, int32_t* out_assign,
+                         int32_t capacity, int32_t n_mb, int32_t policy, int32_t* out_assign,
                          int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
                          int32_t* out_mb_max_len);
 

@@ -54,6 +54,7 @@ constexpr int64_t kDefaultMaxSamples = 65536;
 constexpr int64_t kDefaultMetaBytes = 64ll << 20;
 constexpr int64_t kDefaultChunkBytes = 1ll << 30;
 constexpr int64_t kMaxSampleRows = 1 << 24;
+constexpr int32_t kMaxPlanMicrobatches = 1 << 20;
 // 16-byte vectors one pack or one write may move. The kernels index vectors
 // with 32-bit integers, and a thread forms the indices of its vectors (up to
 // 767 past its chunk's start) before testing them against the chunk's end,
@@ -471,8 +472,9 @@ fp_status check_backing(int tier, void* ptr, uint64_t bytes, int device) {
   return FP_OK;
 }
 
+// Partition by FP_PLAN_LPT or FP_PLAN_ZIGZAG (flowpool.h states both).
 fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
-                 int32_t n_mb, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
+                 int32_t n_mb, int32_t policy, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
                  int32_t* mb_max) {
   std::vector<int32_t> order((size_t)n);
   std::iota(order.begin(), order.end(), 0);
@@ -482,12 +484,22 @@ fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_
   std::vector<int64_t> tok((size_t)n_mb, 0), cst((size_t)n_mb, 0);
   std::vector<int32_t> mx((size_t)n_mb, 0);
   for (int32_t i = 0; i < n; ++i) assign[i] = -1;
-  for (int32_t i : order) {
+  const int64_t period = 2ll * n_mb;
+  for (int32_t pos = 0; pos < n; ++pos) {
+    const int32_t i = order[(size_t)pos];
     int best = -1;
-    for (int j = 0; j < n_mb; ++j) {
-      if (tok[(size_t)j] + lengths[i] <= capacity &&
-          (best < 0 || cst[(size_t)j] < cst[(size_t)best]))
-        best = j;
+    if (policy == FP_PLAN_ZIGZAG) {
+      for (int64_t q = 0; q < period && best < 0; ++q) {
+        const int64_t r = ((int64_t)pos + q) % period;
+        const int j = (int)(r < n_mb ? r : period - 1 - r);
+        if (tok[(size_t)j] + lengths[i] <= capacity) best = j;
+      }
+    } else {
+      for (int j = 0; j < n_mb; ++j) {
+        if (tok[(size_t)j] + lengths[i] <= capacity &&
+            (best < 0 || cst[(size_t)j] < cst[(size_t)best]))
+          best = j;
+      }
     }
     if (best >= 0) {
       assign[i] = best;
@@ -1045,26 +1057,29 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
 }
 
 fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
-                         int32_t capacity, int32_t n_mb, int32_t* out_assign,
+                         int32_t capacity, int32_t n_mb, int32_t policy, int32_t* out_assign,
                          int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
                          int32_t* out_mb_max_len) {
-  if (n < 0 || n_mb < 1 || capacity < 1 || capacity > (1 << 28))
+  if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28))
     return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d", n, n_mb, capacity);
+  if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
   if (n && (!lengths || !costs_scaled || !out_assign)) return fail(FP_EINVAL, "null array");
   for (int32_t i = 0; i < n; ++i)
     if (lengths[i] < 1 || costs_scaled[i] < 0) return fail(FP_EINVAL, "sample %d length/cost", i);
-  return greedy(lengths, costs_scaled, n, capacity, n_mb, out_assign, out_mb_tokens, out_mb_cost_scaled,
+  return greedy(lengths, costs_scaled, n, capacity, n_mb, policy, out_assign, out_mb_tokens, out_mb_cost_scaled,
                 out_mb_max_len);
 }
 
 fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
-                            int32_t n_mb, int32_t cost_k, int32_t* out_assign, int32_t* out_mb_tokens,
-                            int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
+                            int32_t n_mb, int32_t cost_k, int32_t policy, int32_t* out_assign,
+                            int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
                             int64_t* out_sample_cost_scaled, void* stream) {
   if (!p) return fail(FP_EINVAL, "null pool");
   std::lock_guard<std::mutex> lock(p->mu);
-  if (n < 0 || n_mb < 1 || capacity < 1 || capacity > (1 << 28) || cost_k < 1 || cost_k > (1 << 24))
+  if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28) || cost_k < 1 ||
+      cost_k > (1 << 24))
     return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d, cost_k %d", n, n_mb, capacity, cost_k);
+  if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
   if (n && (!sample_ids || !out_assign)) return fail(FP_EINVAL, "null array");
   std::vector<int32_t> slots((size_t)n), lens((size_t)n);
   std::vector<SampleRec*> recs((size_t)n);
@@ -1101,8 +1116,8 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
     if (st != FP_OK) return st;
   }
   if (out_sample_cost_scaled) std::memcpy(out_sample_cost_scaled, costs.data(), 8 * (size_t)n);
-  return greedy(lens.data(), costs.data(), n, capacity, n_mb, out_assign, out_mb_tokens, out_mb_cost_scaled,
-                out_mb_max_len);
+  return greedy(lens.data(), costs.data(), n, capacity, n_mb, policy, out_assign, out_mb_tokens,
+                out_mb_cost_scaled, out_mb_max_len);
 }
 
 namespace {

@@ -33,7 +33,7 @@ except ImportError:
     pass
 
 _lib = C.CDLL(LIB_PATH)
-ABI_VERSION = 3   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
+ABI_VERSION = 4   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
 if _lib.fp_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI version {_lib.fp_abi_version()}, the bindings expect {ABI_VERSION}; rebuild it")
 
@@ -43,6 +43,7 @@ STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ENOENT", -4: "ECAPACIT
 FP_ALLOC_CONTIG, FP_ALLOC_SCATTER = 0, 1
 FP_TIER_HBM, FP_TIER_HOST = 0, 1
 FP_TIER_MASK_HBM, FP_TIER_MASK_HOST, FP_TIER_MASK_ALL = 1, 2, 3
+FP_PLAN_LPT, FP_PLAN_ZIGZAG = 0, 1
 ALLOC_POLICIES = {"contig": FP_ALLOC_CONTIG, "scatter": FP_ALLOC_SCATTER}
 
 
@@ -81,9 +82,10 @@ _SIGS = {
     "pool_destroy": (C.c_int32, [_P]),
     "pool_write_sample": (C.c_int32, [_P, _i32p, C.c_int32, _i32p, _i32p, C.c_int32, _P, _u8p, _P, _u64p]),
     "pool_free_sample": (C.c_int32, [_P, C.c_uint64]),
-    "plan_microbatches": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+    "plan_microbatches": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                       _i32p, _i32p, _i64p, _i32p, _i64p, _P]),
-    "plan_partition": (C.c_int32, [_i32p, _i64p, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i64p, _i32p]),
+    "plan_partition": (C.c_int32, [_i32p, _i64p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i64p,
+                                   _i32p]),
     "pack_microbatch": (C.c_int32, [_P, _u64p, C.c_int32, _P, C.c_int64, _P, C.c_int64, _P, _P,
                                     _i32p, _i32p, C.c_int32, _P]),
     "pool_stats": (C.c_int32, [_P, _i64p, _i64p, _i64p]),
@@ -240,7 +242,8 @@ def pool_migrate(pool: int, sample_ids, tier: int, stream=None) -> int:
     return int(moved.value)
 
 
-def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: int, stream=None):
+def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: int, stream=None,
+                      policy: int = FP_PLAN_LPT):
     """Returns dict(assign, mb_tokens, mb_cost_scaled, mb_max_len, sample_cost_scaled)."""
     ids, idp = _arr(sample_ids, np.uint64, _u64p)
     n = len(ids)
@@ -249,15 +252,15 @@ def plan_microbatches(pool: int, sample_ids, capacity: int, n_mb: int, cost_k: i
     cst = np.empty(n_mb, np.int64)
     mx = np.empty(n_mb, np.int32)
     sc = np.empty(n, np.int64)
-    _check(_lib.plan_microbatches(pool, idp, n, capacity, n_mb, cost_k,
+    _check(_lib.plan_microbatches(pool, idp, n, capacity, n_mb, cost_k, policy,
                                   assign.ctypes.data_as(_i32p), tok.ctypes.data_as(_i32p),
                                   cst.ctypes.data_as(_i64p), mx.ctypes.data_as(_i32p),
                                   sc.ctypes.data_as(_i64p), _stream(stream)), "plan_microbatches")
     return dict(assign=assign, mb_tokens=tok, mb_cost_scaled=cst, mb_max_len=mx, sample_cost_scaled=sc)
 
 
-def plan_partition(lengths, costs_scaled, capacity: int, n_mb: int):
-    """Host-only greedy partition. Returns dict(assign, mb_tokens, mb_cost_scaled, mb_max_len)."""
+def plan_partition(lengths, costs_scaled, capacity: int, n_mb: int, policy: int = FP_PLAN_LPT):
+    """Host-only partition. Returns dict(assign, mb_tokens, mb_cost_scaled, mb_max_len)."""
     ln, lp = _arr(lengths, np.int32, _i32p)
     cs, cp = _arr(costs_scaled, np.int64, _i64p)
     n = len(ln)
@@ -265,7 +268,7 @@ def plan_partition(lengths, costs_scaled, capacity: int, n_mb: int):
     tok = np.empty(n_mb, np.int32)
     cst = np.empty(n_mb, np.int64)
     mx = np.empty(n_mb, np.int32)
-    _check(_lib.plan_partition(lp, cp, n, capacity, n_mb, assign.ctypes.data_as(_i32p),
+    _check(_lib.plan_partition(lp, cp, n, capacity, n_mb, policy, assign.ctypes.data_as(_i32p),
                                tok.ctypes.data_as(_i32p), cst.ctypes.data_as(_i64p),
                                mx.ctypes.data_as(_i32p)), "plan_partition")
     return dict(assign=assign, mb_tokens=tok, mb_cost_scaled=cst, mb_max_len=mx)

@@ -136,7 +136,8 @@ int main(int argc, char** argv) {
   int32_t* mb_tokens = (int32_t*)xmalloc(4 * (size_t)n_mb);
   int32_t* mb_max = (int32_t*)xmalloc(4 * (size_t)n_mb);
   int64_t* mb_cost = (int64_t*)xmalloc(8 * (size_t)n_mb);
-  if (plan_microbatches(pool, ids, n, capacity, n_mb, cost_k, assign, mb_tokens, mb_cost, mb_max, NULL, NULL) != FP_OK)
+  if (plan_microbatches(pool, ids, n, capacity, n_mb, cost_k, FP_PLAN_LPT, assign, mb_tokens, mb_cost, mb_max, NULL,
+                        NULL) != FP_OK)
     die("plan_microbatches");
 
   FILE* out = fopen(argv[2], "wb");

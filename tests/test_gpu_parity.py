@@ -373,6 +373,39 @@ def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
         w.close()
 
 
+def test_zigzag_plan_then_pack(fp):
+    """plan_microbatches with the zig-zag policy: the per-sample costs from
+    the GPU cost kernel and the assignment equal the oracle's, and the
+    microbatches pack bit-exactly."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    from oracle.plan import cost_scaled, members, zigzag_partition
+    say("case zig-zag plan")
+    cfg = scaled(CONFIGS["qwen"], hbm_pages=600, vocab=3000, capacity=6000, n_mb=3)
+    specs = gen_samples(cfg, 2, count=9)
+    table, vis = _inputs(cfg, 2, specs, "tagged")
+    w = GpuWorkload(cfg, 2, specs=specs, table=to_dev(table), vis_fn=lambda i, s: to_dev(vis[i]) if s.n_vis else None)
+    try:
+        plan = fp.plan_microbatches(w.pool, w.ids, cfg.capacity, cfg.n_mb, cfg.cost_k, policy=fp.FP_PLAN_ZIGZAG)
+        lengths = [s.length for s in specs]
+        assign, tok, cst = zigzag_partition(lengths, cfg.cost_k, cfg.capacity, cfg.n_mb)
+        assert plan["sample_cost_scaled"].tolist() == [cost_scaled(l, cfg.cost_k) for l in lengths]
+        assert plan["assign"].tolist() == assign
+        assert plan["mb_tokens"].tolist() == tok and plan["mb_cost_scaled"].tolist() == cst
+        out, cu, pos = w.alloc_outputs()
+        for j, idx in enumerate(members(assign, cfg.n_mb)):
+            n, _ = w.pack([w.ids[i] for i in idx], out, cu, pos)
+            torch.cuda.synchronize()
+            want = definitional_pack([specs[i] for i in idx], [vis[i] for i in idx], table)
+            assert n == len(want[0]) and np.array_equal(to_host(out[:n]), want[0]), f"microbatch {j}"
+            assert cu[:len(idx) + 1].cpu().numpy().tolist() == want[1].tolist()
+            assert pos[:n].cpu().numpy().tolist() == want[2].tolist()
+        with pytest.raises(fp.FlowPoolError) as e:
+            fp.plan_microbatches(w.pool, w.ids, cfg.capacity, cfg.n_mb, cfg.cost_k, policy=7)
+        assert e.value.code == "EINVAL"
+    finally:
+        w.close()
+
+
 def test_dynamic_packing_then_pack(fp):
     """Alg. 1 over resident samples (plan_pool_packing) gives the oracle's
     plan, and every microbatch it forms, packed in each rank's dispatch

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 from conftest import ROOT
-from oracle.plan import cost_scaled, greedy_partition
+from oracle.plan import cost_scaled, greedy_partition, zigzag_partition
 
 fp = pytest.importorskip("paper_2606_23087_amd.flowpool",
                          reason="libflowpool.so not built (run __graft_entry__.build())")
@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(fp.EXPORTED)
-    assert fp.fp_abi_version() == fp.ABI_VERSION == 3
+    assert fp.fp_abi_version() == fp.ABI_VERSION == 4
 
 
 def test_config_struct_matches_header():
@@ -37,8 +37,9 @@ def test_config_struct_matches_header():
     assert ctypes.sizeof(fp.fp_pool_config) == 8 + 16 + 8 + 8 + 8 + 8 + 16 + 8 + 8 + 16 + 8
 
 
+@pytest.mark.parametrize("policy", ["lpt", "zigzag"])
 @pytest.mark.parametrize("seed", range(30))
-def test_plan_partition_equals_oracle(seed):
+def test_plan_partition_equals_oracle(seed, policy):
     rng = np.random.default_rng(seed)
     n = int(rng.integers(0, 300))
     M = int(rng.integers(1, 70))
@@ -48,8 +49,12 @@ def test_plan_partition_equals_oracle(seed):
         lengths = rng.choice([100, 200, 300], size=n)       # many ties
     C = int(rng.integers(5000, 40000))
     costs = [cost_scaled(int(l), K) for l in lengths]
-    got = fp.plan_partition(lengths, costs, C, M)
-    assign, tok, cst = greedy_partition([int(x) for x in lengths], K, C, M)
+    if policy == "lpt":
+        got = fp.plan_partition(lengths, costs, C, M)
+        assign, tok, cst = greedy_partition([int(x) for x in lengths], K, C, M)
+    else:
+        got = fp.plan_partition(lengths, costs, C, M, fp.FP_PLAN_ZIGZAG)
+        assign, tok, cst = zigzag_partition([int(x) for x in lengths], K, C, M)
     assert got["assign"].tolist() == assign
     assert got["mb_tokens"].tolist() == tok and got["mb_cost_scaled"].tolist() == cst
     mx = [max([int(lengths[i]) for i in range(n) if assign[i] == j], default=0) for j in range(M)]
@@ -64,6 +69,12 @@ def test_plan_partition_errors():
         fp.plan_partition([0], [0], 10, 1)
     assert e.value.code == "EINVAL"
     assert fp.plan_partition([], [], 10, 2)["mb_tokens"].tolist() == [0, 0]
+    for bad in (dict(policy=2), dict(policy=-1), dict(n_mb=(1 << 20) + 1)):
+        args = dict(lengths=[1], costs_scaled=[1], capacity=10, n_mb=2)
+        args.update(bad)
+        with pytest.raises(fp.FlowPoolError) as e:
+            fp.plan_partition(**args)
+        assert e.value.code == "EINVAL"
 
 
 def test_pool_create_rejects_bad_config_without_gpu():
