@@ -16,7 +16,9 @@
  *  - Return value: FP_OK (0) or a negative FP_E* status. Nothing throws or
  *    aborts across the ABI. fp_last_error() returns a message for the last
  *    failing call on the calling thread.
- *  - A failing call leaves the pool unchanged and launches nothing.
+ *  - A failing call leaves the pool unchanged and launches nothing. Host
+ *    memory exhausted inside a call returns ENOMEM (the one case where a
+ *    call that already changed the pool may not have undone it).
  *  - "host" pointers are ordinary CPU memory read or written before the call
  *    returns; "device" pointers must be readable/writable by the GPU (device
  *    memory, or pinned host memory mapped into the GPU address space).
@@ -313,7 +315,7 @@ fp_status plan_allocation(int32_t n_modules, const int32_t* n_configs, const int
  * 0..N-1, then N-1..0, and so on, restarting at rank 0 for every bucket.
  *  lengths             host int32[n], each in [1, capacity]
  *  capacity            L, tokens per microbatch, at most 2^20
- *  n_ranks, n_buckets  N >= 1 data-parallel ranks, K >= 1 buckets
+ *  n_ranks, n_buckets  N in [1, 2^20] data-parallel ranks, K >= 1 buckets
  * Outputs (host, caller-owned, any may be NULL; per-microbatch arrays need
  * room for n entries, of which *out_n_mb are written):
  *  out_mb_of_seq[n]    microbatch of each sequence

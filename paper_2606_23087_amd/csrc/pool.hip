@@ -16,6 +16,8 @@
 #include <cstring>
 #include <map>
 #include <mutex>
+#include <new>
+#include <stdexcept>
 #include <numeric>
 #include <string>
 #include <unordered_map>
@@ -473,6 +475,19 @@ fp_status check_backing(int tier, void* ptr, uint64_t bytes, int device) {
 }
 
 // Partition by FP_PLAN_LPT or FP_PLAN_ZIGZAG (flowpool.h states both).
+// Runs an entry point's body; host memory exhaustion inside it becomes
+// ENOMEM instead of an exception crossing the C ABI.
+template <class F>
+fp_status guarded(F&& body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(FP_ENOMEM, "host memory exhausted");
+  } catch (const std::exception& e) {
+    return fail(FP_EINVAL, "%s", e.what());
+  }
+}
+
 fp_status greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity,
                  int32_t n_mb, int32_t policy, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost,
                  int32_t* mb_max) {
@@ -531,593 +546,615 @@ void fp_config_init(fp_pool_config* cfg) {
 }
 
 fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
-  if (!cfg_in || !out) return fail(FP_EINVAL, "null argument");
-  *out = nullptr;
-  fp_pool_config c = *cfg_in;
-  if (c.hidden < 8 || ((2ll * c.hidden) % 16) != 0 || c.hidden > (1 << 20))
-    return fail(FP_EINVAL, "hidden %d: 2*hidden must be a positive multiple of 16", c.hidden);
-  if (c.page_tokens < 1 || c.page_tokens > (1 << 20)) return fail(FP_EINVAL, "page_tokens %d", c.page_tokens);
-  if (c.hbm_pages < 0 || c.host_pages < 0 || c.hbm_pages + c.host_pages < 1 ||
-      c.hbm_pages + c.host_pages > (1ll << 31))
-    return fail(FP_EINVAL, "page counts %lld/%lld", (long long)c.hbm_pages, (long long)c.host_pages);
-  if (c.alloc_policy != FP_ALLOC_CONTIG && c.alloc_policy != FP_ALLOC_SCATTER)
-    return fail(FP_EINVAL, "alloc_policy %d", c.alloc_policy);
-  if (c.world_size != 1 || c.rank != 0)
-    return fail(FP_EINVAL, "world_size/rank %d/%d: this library runs one process", c.world_size, c.rank);
-  if (c.vocab < 0 || c.vocab > (1ll << 31)) return fail(FP_EINVAL, "vocab %lld", (long long)c.vocab);
-  if (c.pack_cus < 0 || c.pack_cus > 65536 || c.reserved != 0) return fail(FP_EINVAL, "pack_cus %d / reserved", c.pack_cus);
-  if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
-  if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
-  {
-    // The pack kernel divides GVA offsets below 2^52 by the page size.
-    const unsigned __int128 span = (unsigned __int128)(c.hbm_pages + c.host_pages) *
-                                   (unsigned __int128)(2ll * c.hidden) * (unsigned __int128)c.page_tokens;
-    if (span >= ((unsigned __int128)1 << 52) || (unsigned __int128)c.gva_start + span > ~(uint64_t)0)
-      return fail(FP_EINVAL, "GVA span of the pool exceeds 2^52 bytes or the address space");
-  }
-  if (c.max_samples == 0) c.max_samples = kDefaultMaxSamples;
-  if (c.max_samples < 1 || c.max_samples > (1ll << 31) - 1) return fail(FP_EINVAL, "max_samples");
-  if (c.meta_bytes == 0) c.meta_bytes = kDefaultMetaBytes;
-  if (c.meta_bytes < 16 || c.meta_bytes > fp::kMaxMetaBytes) return fail(FP_EINVAL, "meta_bytes");
-  if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunkBytes;
-  if (c.chunk_bytes < 0) return fail(FP_EINVAL, "chunk_bytes");
-  int ndev = 0;
-  FP_HIP(hipGetDeviceCount(&ndev));
-  if (c.device < 0 || c.device >= ndev) return fail(FP_EINVAL, "device %d of %d", c.device, ndev);
-  DeviceGuard guard(c.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice(%d) failed", c.device);
-
-  int n_cu = c.pack_cus;
-  if (n_cu == 0) FP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, c.device));
-  fp_pool* p = new fp_pool();
-  p->cfg = c;
-  p->n_cu = n_cu;
-  p->rb = 2ll * c.hidden;
-  p->pb = p->rb * c.page_tokens;
-  p->n_pages[0] = c.hbm_pages;
-  p->n_pages[1] = c.host_pages;
-  p->gva_start = c.gva_start;
-  // Sec. 3.2: per tier a region [start, start + world_size*max_size); this
-  // rank's segment [start + rank*max_size, start + (rank+1)*max_size); the
-  // DRAM region follows the HBM region.
-  for (int t = 0; t < 2; ++t) p->max_size[t] = (uint64_t)p->n_pages[t] * (uint64_t)p->pb;
-  p->region_start[0] = c.gva_start;
-  p->region_start[1] = c.gva_start + (uint64_t)c.world_size * p->max_size[0];
-  for (int t = 0; t < 2; ++t) p->seg_start[t] = p->region_start[t] + (uint64_t)c.rank * p->max_size[t];
-  p->dv = fp::make_divisors(p->rb, c.page_tokens, (uint64_t)p->pb);
-
-  auto bail = [&](fp_status s) {
-    std::string keep = t_err;
-    free_all(p);
-    delete p;
-    t_err = keep;
-    return s;
-  };
-
-  // Physical backing: the caller's buffer as one chunk, or library chunks of
-  // whole pages.
-  void* backing[2] = {c.hbm_backing, c.host_backing};
-  for (int t = 0; t < 2; ++t) {
-    if (backing[t]) {
-      fp_status bs = check_backing(t, backing[t], (uint64_t)p->n_pages[t] * (uint64_t)p->pb, c.device);
-      if (bs != FP_OK) return bail(bs);
-      p->chunks[t].push_back(backing[t]);
-      p->frames_per_chunk[t] = std::max<int64_t>(1, p->n_pages[t]);
-      p->owned[t] = false;
-      continue;
+  return guarded([&]() -> fp_status {
+    if (!cfg_in || !out) return fail(FP_EINVAL, "null argument");
+    *out = nullptr;
+    fp_pool_config c = *cfg_in;
+    if (c.hidden < 8 || ((2ll * c.hidden) % 16) != 0 || c.hidden > (1 << 20))
+      return fail(FP_EINVAL, "hidden %d: 2*hidden must be a positive multiple of 16", c.hidden);
+    if (c.page_tokens < 1 || c.page_tokens > (1 << 20)) return fail(FP_EINVAL, "page_tokens %d", c.page_tokens);
+    if (c.hbm_pages < 0 || c.host_pages < 0 || c.hbm_pages + c.host_pages < 1 ||
+        c.hbm_pages + c.host_pages > (1ll << 31))
+      return fail(FP_EINVAL, "page counts %lld/%lld", (long long)c.hbm_pages, (long long)c.host_pages);
+    if (c.alloc_policy != FP_ALLOC_CONTIG && c.alloc_policy != FP_ALLOC_SCATTER)
+      return fail(FP_EINVAL, "alloc_policy %d", c.alloc_policy);
+    if (c.world_size != 1 || c.rank != 0)
+      return fail(FP_EINVAL, "world_size/rank %d/%d: this library runs one process", c.world_size, c.rank);
+    if (c.vocab < 0 || c.vocab > (1ll << 31)) return fail(FP_EINVAL, "vocab %lld", (long long)c.vocab);
+    if (c.pack_cus < 0 || c.pack_cus > 65536 || c.reserved != 0) return fail(FP_EINVAL, "pack_cus %d / reserved", c.pack_cus);
+    if (c.gva_start == 0) c.gva_start = kDefaultGvaStart;
+    if (c.gva_start % 4096) return fail(FP_EINVAL, "gva_start must be a multiple of 4096");
+    {
+      // The pack kernel divides GVA offsets below 2^52 by the page size.
+      const unsigned __int128 span = (unsigned __int128)(c.hbm_pages + c.host_pages) *
+                                     (unsigned __int128)(2ll * c.hidden) * (unsigned __int128)c.page_tokens;
+      if (span >= ((unsigned __int128)1 << 52) || (unsigned __int128)c.gva_start + span > ~(uint64_t)0)
+        return fail(FP_EINVAL, "GVA span of the pool exceeds 2^52 bytes or the address space");
     }
-    p->frames_per_chunk[t] = std::max<int64_t>(1, c.chunk_bytes / p->pb);
-    for (int64_t f = 0; f < p->n_pages[t]; f += p->frames_per_chunk[t]) {
-      const int64_t frames = std::min(p->frames_per_chunk[t], p->n_pages[t] - f);
-      void* ptr = nullptr;
-      hipError_t e = (t == 0) ? hipMalloc(&ptr, (size_t)(frames * p->pb))
-                              : hipHostMalloc(&ptr, (size_t)(frames * p->pb), hipHostMallocMapped);
-      if (e != hipSuccess)
-        return bail(fail(FP_EHIP, "allocating %s backing (%lld bytes): %s", t ? "host" : "HBM",
-                         (long long)(frames * p->pb), hipGetErrorString(e)));
-      if (t == 1) {
-        void* dptr = nullptr;
-        e = hipHostGetDevicePointer(&dptr, ptr, 0);
-        if (e != hipSuccess || dptr != ptr) {
-          (void)hipHostFree(ptr);
-          return bail(fail(FP_EHIP, "host backing is not mapped at the same address"));
+    if (c.max_samples == 0) c.max_samples = kDefaultMaxSamples;
+    if (c.max_samples < 1 || c.max_samples > (1ll << 31) - 1) return fail(FP_EINVAL, "max_samples");
+    if (c.meta_bytes == 0) c.meta_bytes = kDefaultMetaBytes;
+    if (c.meta_bytes < 16 || c.meta_bytes > fp::kMaxMetaBytes) return fail(FP_EINVAL, "meta_bytes");
+    if (c.chunk_bytes == 0) c.chunk_bytes = kDefaultChunkBytes;
+    if (c.chunk_bytes < 0) return fail(FP_EINVAL, "chunk_bytes");
+    int ndev = 0;
+    FP_HIP(hipGetDeviceCount(&ndev));
+    if (c.device < 0 || c.device >= ndev) return fail(FP_EINVAL, "device %d of %d", c.device, ndev);
+    DeviceGuard guard(c.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice(%d) failed", c.device);
+
+    int n_cu = c.pack_cus;
+    if (n_cu == 0) FP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, c.device));
+    fp_pool* p = new fp_pool();
+    p->cfg = c;
+    p->n_cu = n_cu;
+    p->rb = 2ll * c.hidden;
+    p->pb = p->rb * c.page_tokens;
+    p->n_pages[0] = c.hbm_pages;
+    p->n_pages[1] = c.host_pages;
+    p->gva_start = c.gva_start;
+    // Sec. 3.2: per tier a region [start, start + world_size*max_size); this
+    // rank's segment [start + rank*max_size, start + (rank+1)*max_size); the
+    // DRAM region follows the HBM region.
+    for (int t = 0; t < 2; ++t) p->max_size[t] = (uint64_t)p->n_pages[t] * (uint64_t)p->pb;
+    p->region_start[0] = c.gva_start;
+    p->region_start[1] = c.gva_start + (uint64_t)c.world_size * p->max_size[0];
+    for (int t = 0; t < 2; ++t) p->seg_start[t] = p->region_start[t] + (uint64_t)c.rank * p->max_size[t];
+    p->dv = fp::make_divisors(p->rb, c.page_tokens, (uint64_t)p->pb);
+
+    // Until the pool is handed out, leaving this scope (an error return or an
+    // exception) frees everything it holds.
+    struct Hold {
+      fp_pool* p;
+      ~Hold() {
+        if (!p) return;
+        std::string keep = t_err;
+        free_all(p);
+        delete p;
+        t_err = keep;
+      }
+    } hold{p};
+
+    // Physical backing: the caller's buffer as one chunk, or library chunks of
+    // whole pages.
+    void* backing[2] = {c.hbm_backing, c.host_backing};
+    for (int t = 0; t < 2; ++t) {
+      if (backing[t]) {
+        fp_status bs = check_backing(t, backing[t], (uint64_t)p->n_pages[t] * (uint64_t)p->pb, c.device);
+        if (bs != FP_OK) return bs;
+        p->chunks[t].push_back(backing[t]);
+        p->frames_per_chunk[t] = std::max<int64_t>(1, p->n_pages[t]);
+        p->owned[t] = false;
+        continue;
+      }
+      p->frames_per_chunk[t] = std::max<int64_t>(1, c.chunk_bytes / p->pb);
+      for (int64_t f = 0; f < p->n_pages[t]; f += p->frames_per_chunk[t]) {
+        const int64_t frames = std::min(p->frames_per_chunk[t], p->n_pages[t] - f);
+        void* ptr = nullptr;
+        hipError_t e = (t == 0) ? hipMalloc(&ptr, (size_t)(frames * p->pb))
+                                : hipHostMalloc(&ptr, (size_t)(frames * p->pb), hipHostMallocMapped);
+        if (e != hipSuccess)
+          return fail(FP_EHIP, "allocating %s backing (%lld bytes): %s", t ? "host" : "HBM",
+                           (long long)(frames * p->pb), hipGetErrorString(e));
+        if (t == 1) {
+          void* dptr = nullptr;
+          e = hipHostGetDevicePointer(&dptr, ptr, 0);
+          if (e != hipSuccess || dptr != ptr) {
+            (void)hipHostFree(ptr);
+            return fail(FP_EHIP, "host backing is not mapped at the same address");
+          }
+        }
+        p->chunks[t].push_back(ptr);
+      }
+    }
+    // Page table: GVA page (HBM pages, then host pages) -> physical frame.
+    const int64_t total = p->n_pages[0] + p->n_pages[1];
+    p->pte.resize((size_t)total);
+    uint64_t seed = c.frame_shuffle_seed;
+    for (int t = 0; t < 2; ++t) {
+      std::vector<int64_t> order((size_t)p->n_pages[t]);
+      std::iota(order.begin(), order.end(), 0);
+      if (seed) {
+        for (int64_t i = p->n_pages[t] - 1; i > 0; --i) {
+          const int64_t j = (int64_t)(splitmix64(seed) % (uint64_t)(i + 1));
+          std::swap(order[(size_t)i], order[(size_t)j]);
         }
       }
-      p->chunks[t].push_back(ptr);
-    }
-  }
-  // Page table: GVA page (HBM pages, then host pages) -> physical frame.
-  const int64_t total = p->n_pages[0] + p->n_pages[1];
-  p->pte.resize((size_t)total);
-  uint64_t seed = c.frame_shuffle_seed;
-  for (int t = 0; t < 2; ++t) {
-    std::vector<int64_t> order((size_t)p->n_pages[t]);
-    std::iota(order.begin(), order.end(), 0);
-    if (seed) {
-      for (int64_t i = p->n_pages[t] - 1; i > 0; --i) {
-        const int64_t j = (int64_t)(splitmix64(seed) % (uint64_t)(i + 1));
-        std::swap(order[(size_t)i], order[(size_t)j]);
+      for (int64_t i = 0; i < p->n_pages[t]; ++i) {
+        const int64_t f = order[(size_t)i];
+        const uint64_t addr = (uint64_t)p->chunks[t][(size_t)(f / p->frames_per_chunk[t])] +
+                              (uint64_t)(f % p->frames_per_chunk[t]) * (uint64_t)p->pb;
+        const int64_t vpn = (int64_t)((p->page_gva(t, i) - p->gva_start) / (uint64_t)p->pb);
+        p->pte[(size_t)vpn] = addr | fp::PTE_VALID | (t ? fp::PTE_HOST : 0);
       }
+      p->used[t].assign((size_t)p->n_pages[t], 0);
+      p->stack[t].resize((size_t)p->n_pages[t]);
+      for (int64_t i = 0; i < p->n_pages[t]; ++i) p->stack[t][(size_t)i] = p->n_pages[t] - 1 - i;
+      p->n_free[t] = p->n_pages[t];
     }
-    for (int64_t i = 0; i < p->n_pages[t]; ++i) {
-      const int64_t f = order[(size_t)i];
-      const uint64_t addr = (uint64_t)p->chunks[t][(size_t)(f / p->frames_per_chunk[t])] +
-                            (uint64_t)(f % p->frames_per_chunk[t]) * (uint64_t)p->pb;
-      const int64_t vpn = (int64_t)((p->page_gva(t, i) - p->gva_start) / (uint64_t)p->pb);
-      p->pte[(size_t)vpn] = addr | fp::PTE_VALID | (t ? fp::PTE_HOST : 0);
-    }
-    p->used[t].assign((size_t)p->n_pages[t], 0);
-    p->stack[t].resize((size_t)p->n_pages[t]);
-    for (int64_t i = 0; i < p->n_pages[t]; ++i) p->stack[t][(size_t)i] = p->n_pages[t] - 1 - i;
-    p->n_free[t] = p->n_pages[t];
-  }
-  hipError_t e = hipMalloc((void**)&p->pte_dev, sizeof(uint64_t) * (size_t)total);
-  if (e == hipSuccess)
-    e = hipMemcpy(p->pte_dev, p->pte.data(), sizeof(uint64_t) * (size_t)total, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMalloc((void**)&p->desc_dev, sizeof(SampleDesc) * (size_t)c.max_samples);
-  if (e == hipSuccess) e = hipMalloc((void**)&p->meta_dev, (size_t)c.meta_bytes);
-  for (int i = 0; e == hipSuccess && i < kRing; ++i)
-    e = hipEventCreateWithFlags(&p->ring[i].ev, hipEventDisableTiming);
-  if (e != hipSuccess) return bail(fail(FP_EHIP, "pool metadata allocation: %s", hipGetErrorString(e)));
-  p->meta.init(c.meta_bytes);
-  p->free_slots.resize((size_t)c.max_samples);
-  for (int64_t i = 0; i < c.max_samples; ++i) p->free_slots[(size_t)i] = (int32_t)(c.max_samples - 1 - i);
-  *out = p;
-  return FP_OK;
+    hipError_t e = hipMalloc((void**)&p->pte_dev, sizeof(uint64_t) * (size_t)total);
+    if (e == hipSuccess)
+      e = hipMemcpy(p->pte_dev, p->pte.data(), sizeof(uint64_t) * (size_t)total, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMalloc((void**)&p->desc_dev, sizeof(SampleDesc) * (size_t)c.max_samples);
+    if (e == hipSuccess) e = hipMalloc((void**)&p->meta_dev, (size_t)c.meta_bytes);
+    for (int i = 0; e == hipSuccess && i < kRing; ++i)
+      e = hipEventCreateWithFlags(&p->ring[i].ev, hipEventDisableTiming);
+    if (e != hipSuccess) return fail(FP_EHIP, "pool metadata allocation: %s", hipGetErrorString(e));
+    p->meta.init(c.meta_bytes);
+    p->free_slots.resize((size_t)c.max_samples);
+    for (int64_t i = 0; i < c.max_samples; ++i) p->free_slots[(size_t)i] = (int32_t)(c.max_samples - 1 - i);
+    hold.p = nullptr;
+    *out = p;
+    return FP_OK;
+  });
 }
 
 fp_status pool_destroy(fp_pool* p) {
-  if (!p) return FP_OK;
-  {
-    DeviceGuard guard(p->cfg.device);
-    free_all(p);
-  }
-  delete p;
-  return FP_OK;
+  return guarded([&]() -> fp_status {
+    if (!p) return FP_OK;
+    {
+      DeviceGuard guard(p->cfg.device);
+      free_all(p);
+    }
+    delete p;
+    return FP_OK;
+  });
 }
 
 fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
                             const int32_t* img_pos, const int32_t* img_ntok, int32_t n_img,
                             const void* vis_emb, const uint8_t* page_tier_wish, void* stream,
                             uint64_t* out_sample_id) {
-  if (!p || !out_sample_id) return fail(FP_EINVAL, "null argument");
-  std::lock_guard<std::mutex> lock(p->mu);
-  if (n_text < 0 || n_img < 0) return fail(FP_EINVAL, "negative count");
-  if ((n_text && !text_ids) || (n_img && (!img_pos || !img_ntok))) return fail(FP_EINVAL, "null array");
-  int64_t n_vis = 0;
-  for (int32_t j = 0; j < n_img; ++j) {
-    if (img_ntok[j] < 0) return fail(FP_EINVAL, "image %d has %d rows", j, img_ntok[j]);
-    if (img_pos[j] < 0 || img_pos[j] > n_text || (j && img_pos[j] < img_pos[j - 1]))
-      return fail(FP_EINVAL, "image %d placeholder %d (text %d)", j, img_pos[j], n_text);
-    n_vis += img_ntok[j];
-  }
-  const int64_t len = n_vis + n_text;
-  if (len < 1 || len > kMaxSampleRows) return fail(FP_EINVAL, "sample length %lld", (long long)len);
-  if (n_vis * (p->rb / 16) > kMaxVectors)
-    return fail(FP_EINVAL, "%lld visual rows of %lld bytes are too many for one write", (long long)n_vis,
-                (long long)p->rb);
-  for (int32_t i = 0; i < n_text; ++i)
-    if (text_ids[i] < 0 || text_ids[i] >= p->cfg.vocab)
-      return fail(FP_EINVAL, "text id %d at %d outside [0, %lld)", text_ids[i], i, (long long)p->cfg.vocab);
-  const int64_t n_pages = (n_vis + p->cfg.page_tokens - 1) / p->cfg.page_tokens;
-  if (page_tier_wish) {
-    if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "tier wishes need the scatter policy");
-    for (int64_t j = 0; j < n_pages; ++j)
-      if (page_tier_wish[j] > 1) return fail(FP_EINVAL, "tier wish %d", page_tier_wish[j]);
-  }
-  DeviceGuard guard(p->cfg.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-  if (capturing((hipStream_t)stream))
-    return fail(FP_ESTATE, "pool_write_sample cannot be captured into a graph (its staging buffers are reused)");
-  const uint8_t* vis_dev = nullptr;
-  if (vis_emb && n_vis > 0) {
-    if ((uintptr_t)vis_emb % 16) return fail(FP_EALIGN, "vis_emb must be 16-byte aligned");
-    // Ordinary (unregistered) host memory would fault the write kernel.
-    hipPointerAttribute_t attr{};
-    if (hipPointerGetAttributes(&attr, vis_emb) != hipSuccess) {
-      (void)hipGetLastError();
-      return fail(FP_EINVAL, "vis_emb is not device-accessible memory");
-    }
-    if (attr.type == hipMemoryTypeUnregistered || !attr.devicePointer)
-      return fail(FP_EINVAL, "vis_emb is ordinary host memory, not device-accessible");
-    vis_dev = (const uint8_t*)attr.devicePointer;
-  }
-  const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);
-  int64_t meta_off = 0;
-  SampleRec rec;
-  fp_status st = FP_OK;
-  // Frees deferred behind packs in flight come back first; if that is not
-  // enough, wait for those packs (the producer yields to the consumer).
-  reclaim(p, false);
-  for (int attempt = 0;; ++attempt) {
-    st = FP_OK;
-    if (p->free_slots.empty()) {
-      st = fail(FP_ENOMEM, "all %lld sample slots in use", (long long)p->cfg.max_samples);
-    } else if (meta_len > 0 && (meta_off = p->meta.alloc(meta_len)) < 0) {
-      st = fail(FP_ENOMEM, "metadata arena full (%lld bytes wanted)", (long long)meta_len);
-    } else {
-      st = alloc_pages(p, n_pages, page_tier_wish, &rec.pages);
-      if (st != FP_OK && meta_len > 0) p->meta.release(meta_off, meta_len);
-    }
-    if (st == FP_OK) break;
-    if (attempt > 0 || p->deferred.empty()) return st;
-    reclaim(p, true);
-  }
-  auto rollback = [&](fp_status s) {
-    std::string keep = t_err;
-    release_pages(p, rec.pages);
-    if (meta_len > 0) p->meta.release(meta_off, meta_len);
-    t_err = keep;
-    return s;
-  };
-  hipStream_t hs = (hipStream_t)stream;
-  SampleDesc d{};
-  d.len = (int32_t)len;
-  d.n_text = n_text;
-  d.n_img = n_img;
-  d.n_vis = (int32_t)n_vis;
-  d.n_pages = (int32_t)n_pages;
-  d.page_off = meta_off;
-  d.img_off = meta_off + align16(8 * n_pages);
-  d.text_off = d.img_off + align16(8ll * n_img);
-  if (meta_len > 0) {
-    Stage* s = nullptr;
-    st = stage_acquire(p, (size_t)meta_len, 0, &s);
-    if (st != FP_OK) return rollback(st);
-    std::memcpy(s->host, rec.pages.data(), 8 * (size_t)n_pages);
-    int32_t* img = (int32_t*)(s->host + (d.img_off - meta_off));
+  return guarded([&]() -> fp_status {
+    if (!p || !out_sample_id) return fail(FP_EINVAL, "null argument");
+    std::lock_guard<std::mutex> lock(p->mu);
+    if (n_text < 0 || n_img < 0) return fail(FP_EINVAL, "negative count");
+    if ((n_text && !text_ids) || (n_img && (!img_pos || !img_ntok))) return fail(FP_EINVAL, "null array");
+    int64_t n_vis = 0;
     for (int32_t j = 0; j < n_img; ++j) {
-      img[2 * j] = img_pos[j];
-      img[2 * j + 1] = img_ntok[j];
+      if (img_ntok[j] < 0) return fail(FP_EINVAL, "image %d has %d rows", j, img_ntok[j]);
+      if (img_pos[j] < 0 || img_pos[j] > n_text || (j && img_pos[j] < img_pos[j - 1]))
+        return fail(FP_EINVAL, "image %d placeholder %d (text %d)", j, img_pos[j], n_text);
+      n_vis += img_ntok[j];
     }
-    if (n_text) std::memcpy(s->host + (d.text_off - meta_off), text_ids, 4 * (size_t)n_text);
-    hipError_t e = hipMemcpyAsync(p->meta_dev + meta_off, s->host, (size_t)meta_len,
-                                  hipMemcpyHostToDevice, hs);
-    if (e != hipSuccess) return rollback(fail(FP_EHIP, "metadata upload: %s", hipGetErrorString(e)));
-    st = stage_release(s, hs);
-    if (st != FP_OK) return rollback(st);
-  }
-  const int32_t slot = p->free_slots.back();
-  fp::WriteArgs wa{};
-  wa.desc = d;
-  wa.desc_table = p->desc_dev;
-  wa.slot = slot;
-  wa.meta = p->meta_dev;
-  wa.pte = p->pte_dev;
-  wa.gva_start = p->gva_start;
-  wa.vis = vis_dev;
-  wa.row_bytes = (int32_t)p->rb;
-  wa.page_tokens = p->cfg.page_tokens;
-  wa.max_chunk_rows = (int32_t)std::min<int64_t>(n_vis, fp::kChunkVecs / (p->rb / 16) + 2);
-  wa.dv = p->dv;
-  hipError_t e = fp::launch_write(wa, hs);
-  if (e != hipSuccess) return rollback(fail(FP_EHIP, "write kernel: %s", hipGetErrorString(e)));
-  int32_t ev = -1;
-  e = p->events.acquire(&ev);
-  if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
-  if (e != hipSuccess) {
-    // The write is already queued: wait for it rather than hand out its pages again.
-    (void)hipStreamSynchronize(hs);
-    if (ev >= 0) p->events.unref(ev);
-    return rollback(fail(FP_EHIP, "write event: %s", hipGetErrorString(e)));
-  }
-  rec.written = ev;
-  rec.write_stream = stream;
-  p->free_slots.pop_back();
-  rec.slot = slot;
-  rec.len = (int32_t)len;
-  rec.n_text = n_text;
-  rec.n_img = n_img;
-  rec.n_vis = (int32_t)n_vis;
-  rec.meta_off = meta_off;
-  rec.meta_len = meta_len;
-  rec.text_off = d.text_off;
-  rec.page_off = d.page_off;
-  rec.img.resize(2 * (size_t)n_img);
-  for (int32_t j = 0; j < n_img; ++j) {
-    rec.img[2 * (size_t)j] = img_pos[j];
-    rec.img[2 * (size_t)j + 1] = img_ntok[j];
-  }
-  const uint64_t id = p->next_id++;
-  p->samples.emplace(id, std::move(rec));
-  *out_sample_id = id;
-  return FP_OK;
+    const int64_t len = n_vis + n_text;
+    if (len < 1 || len > kMaxSampleRows) return fail(FP_EINVAL, "sample length %lld", (long long)len);
+    if (n_vis * (p->rb / 16) > kMaxVectors)
+      return fail(FP_EINVAL, "%lld visual rows of %lld bytes are too many for one write", (long long)n_vis,
+                  (long long)p->rb);
+    for (int32_t i = 0; i < n_text; ++i)
+      if (text_ids[i] < 0 || text_ids[i] >= p->cfg.vocab)
+        return fail(FP_EINVAL, "text id %d at %d outside [0, %lld)", text_ids[i], i, (long long)p->cfg.vocab);
+    const int64_t n_pages = (n_vis + p->cfg.page_tokens - 1) / p->cfg.page_tokens;
+    if (page_tier_wish) {
+      if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "tier wishes need the scatter policy");
+      for (int64_t j = 0; j < n_pages; ++j)
+        if (page_tier_wish[j] > 1) return fail(FP_EINVAL, "tier wish %d", page_tier_wish[j]);
+    }
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    if (capturing((hipStream_t)stream))
+      return fail(FP_ESTATE, "pool_write_sample cannot be captured into a graph (its staging buffers are reused)");
+    const uint8_t* vis_dev = nullptr;
+    if (vis_emb && n_vis > 0) {
+      if ((uintptr_t)vis_emb % 16) return fail(FP_EALIGN, "vis_emb must be 16-byte aligned");
+      // Ordinary (unregistered) host memory would fault the write kernel.
+      hipPointerAttribute_t attr{};
+      if (hipPointerGetAttributes(&attr, vis_emb) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(FP_EINVAL, "vis_emb is not device-accessible memory");
+      }
+      if (attr.type == hipMemoryTypeUnregistered || !attr.devicePointer)
+        return fail(FP_EINVAL, "vis_emb is ordinary host memory, not device-accessible");
+      vis_dev = (const uint8_t*)attr.devicePointer;
+    }
+    const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);
+    int64_t meta_off = 0;
+    SampleRec rec;
+    fp_status st = FP_OK;
+    // Frees deferred behind packs in flight come back first; if that is not
+    // enough, wait for those packs (the producer yields to the consumer).
+    reclaim(p, false);
+    for (int attempt = 0;; ++attempt) {
+      st = FP_OK;
+      if (p->free_slots.empty()) {
+        st = fail(FP_ENOMEM, "all %lld sample slots in use", (long long)p->cfg.max_samples);
+      } else if (meta_len > 0 && (meta_off = p->meta.alloc(meta_len)) < 0) {
+        st = fail(FP_ENOMEM, "metadata arena full (%lld bytes wanted)", (long long)meta_len);
+      } else {
+        st = alloc_pages(p, n_pages, page_tier_wish, &rec.pages);
+        if (st != FP_OK && meta_len > 0) p->meta.release(meta_off, meta_len);
+      }
+      if (st == FP_OK) break;
+      if (attempt > 0 || p->deferred.empty()) return st;
+      reclaim(p, true);
+    }
+    auto rollback = [&](fp_status s) {
+      std::string keep = t_err;
+      release_pages(p, rec.pages);
+      if (meta_len > 0) p->meta.release(meta_off, meta_len);
+      t_err = keep;
+      return s;
+    };
+    hipStream_t hs = (hipStream_t)stream;
+    SampleDesc d{};
+    d.len = (int32_t)len;
+    d.n_text = n_text;
+    d.n_img = n_img;
+    d.n_vis = (int32_t)n_vis;
+    d.n_pages = (int32_t)n_pages;
+    d.page_off = meta_off;
+    d.img_off = meta_off + align16(8 * n_pages);
+    d.text_off = d.img_off + align16(8ll * n_img);
+    if (meta_len > 0) {
+      Stage* s = nullptr;
+      st = stage_acquire(p, (size_t)meta_len, 0, &s);
+      if (st != FP_OK) return rollback(st);
+      std::memcpy(s->host, rec.pages.data(), 8 * (size_t)n_pages);
+      int32_t* img = (int32_t*)(s->host + (d.img_off - meta_off));
+      for (int32_t j = 0; j < n_img; ++j) {
+        img[2 * j] = img_pos[j];
+        img[2 * j + 1] = img_ntok[j];
+      }
+      if (n_text) std::memcpy(s->host + (d.text_off - meta_off), text_ids, 4 * (size_t)n_text);
+      hipError_t e = hipMemcpyAsync(p->meta_dev + meta_off, s->host, (size_t)meta_len,
+                                    hipMemcpyHostToDevice, hs);
+      if (e != hipSuccess) return rollback(fail(FP_EHIP, "metadata upload: %s", hipGetErrorString(e)));
+      st = stage_release(s, hs);
+      if (st != FP_OK) return rollback(st);
+    }
+    const int32_t slot = p->free_slots.back();
+    fp::WriteArgs wa{};
+    wa.desc = d;
+    wa.desc_table = p->desc_dev;
+    wa.slot = slot;
+    wa.meta = p->meta_dev;
+    wa.pte = p->pte_dev;
+    wa.gva_start = p->gva_start;
+    wa.vis = vis_dev;
+    wa.row_bytes = (int32_t)p->rb;
+    wa.page_tokens = p->cfg.page_tokens;
+    wa.max_chunk_rows = (int32_t)std::min<int64_t>(n_vis, fp::kChunkVecs / (p->rb / 16) + 2);
+    wa.dv = p->dv;
+    hipError_t e = fp::launch_write(wa, hs);
+    if (e != hipSuccess) return rollback(fail(FP_EHIP, "write kernel: %s", hipGetErrorString(e)));
+    int32_t ev = -1;
+    e = p->events.acquire(&ev);
+    if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
+    if (e != hipSuccess) {
+      // The write is already queued: wait for it rather than hand out its pages again.
+      (void)hipStreamSynchronize(hs);
+      if (ev >= 0) p->events.unref(ev);
+      return rollback(fail(FP_EHIP, "write event: %s", hipGetErrorString(e)));
+    }
+    rec.written = ev;
+    rec.write_stream = stream;
+    p->free_slots.pop_back();
+    rec.slot = slot;
+    rec.len = (int32_t)len;
+    rec.n_text = n_text;
+    rec.n_img = n_img;
+    rec.n_vis = (int32_t)n_vis;
+    rec.meta_off = meta_off;
+    rec.meta_len = meta_len;
+    rec.text_off = d.text_off;
+    rec.page_off = d.page_off;
+    rec.img.resize(2 * (size_t)n_img);
+    for (int32_t j = 0; j < n_img; ++j) {
+      rec.img[2 * (size_t)j] = img_pos[j];
+      rec.img[2 * (size_t)j + 1] = img_ntok[j];
+    }
+    const uint64_t id = p->next_id++;
+    p->samples.emplace(id, std::move(rec));
+    *out_sample_id = id;
+    return FP_OK;
+  });
 }
 
 fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  std::lock_guard<std::mutex> lock(p->mu);
-  auto it = p->samples.find(sample_id);
-  if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
-  SampleRec& r = it->second;
-  DeviceGuard guard(p->cfg.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-  // The sample's own write is waited for here, so that reuse of its pages
-  // never races with it on another stream and, without packs in flight,
-  // pages return in free order. Packs still reading it defer the release.
-  if (r.written >= 0) {
-    FP_HIP(hipEventSynchronize(p->events.ev[(size_t)r.written]));
-    p->events.unref(r.written);
-    r.written = -1;
-  }
-  Deferred d;
-  // An event recorded now on every stream that packed the sample and still
-  // has work queued follows those packs; idle streams need none.
-  fp_status st = mark_readers(p, r.readers, &d.events);
-  if (st != FP_OK) {
-    for (int32_t x : d.events) p->events.unref(x);
-    return st;
-  }
-  d.pages = std::move(r.pages);
-  d.meta.emplace_back(r.meta_off, r.meta_len);
-  if (r.pl_off >= 0) d.meta.emplace_back(r.pl_off, r.pl_len);
-  d.slot = r.slot;
-  p->samples.erase(it);
-  defer_or_release(p, std::move(d));
-  return FP_OK;
-}
-
-fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  std::lock_guard<std::mutex> lock(p->mu);
-  DeviceGuard guard(p->cfg.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-  reclaim(p, wait != 0);
-  // Forget the write events that have completed (or, with wait, all of them).
-  for (auto& kv : p->samples) {
-    SampleRec& r = kv.second;
-    if (r.written < 0) continue;
-    if (wait) (void)hipEventSynchronize(p->events.ev[(size_t)r.written]);
-    if (p->events.done(r.written)) {
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    auto it = p->samples.find(sample_id);
+    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
+    SampleRec& r = it->second;
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    // The sample's own write is waited for here, so that reuse of its pages
+    // never races with it on another stream and, without packs in flight,
+    // pages return in free order. Packs still reading it defer the release.
+    if (r.written >= 0) {
+      FP_HIP(hipEventSynchronize(p->events.ev[(size_t)r.written]));
       p->events.unref(r.written);
       r.written = -1;
     }
-  }
-  if (out_deferred_pages) *out_deferred_pages = p->deferred_pages;
-  return FP_OK;
+    Deferred d;
+    // An event recorded now on every stream that packed the sample and still
+    // has work queued follows those packs; idle streams need none.
+    fp_status st = mark_readers(p, r.readers, &d.events);
+    if (st != FP_OK) {
+      for (int32_t x : d.events) p->events.unref(x);
+      return st;
+    }
+    d.pages = std::move(r.pages);
+    d.meta.emplace_back(r.meta_off, r.meta_len);
+    if (r.pl_off >= 0) d.meta.emplace_back(r.pl_off, r.pl_len);
+    d.slot = r.slot;
+    p->samples.erase(it);
+    defer_or_release(p, std::move(d));
+    return FP_OK;
+  });
+}
+
+fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    reclaim(p, wait != 0);
+    // Forget the write events that have completed (or, with wait, all of them).
+    for (auto& kv : p->samples) {
+      SampleRec& r = kv.second;
+      if (r.written < 0) continue;
+      if (wait) (void)hipEventSynchronize(p->events.ev[(size_t)r.written]);
+      if (p->events.done(r.written)) {
+        p->events.unref(r.written);
+        r.written = -1;
+      }
+    }
+    if (out_deferred_pages) *out_deferred_pages = p->deferred_pages;
+    return FP_OK;
+  });
 }
 
 fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t tier, void* stream,
                        int64_t* out_pages_moved) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  std::lock_guard<std::mutex> lock(p->mu);
-  if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "migration needs the scatter policy");
-  if (tier != FP_TIER_HBM && tier != FP_TIER_HOST) return fail(FP_EINVAL, "tier %d", tier);
-  if (n < 0 || (n > 0 && !sample_ids)) return fail(FP_EINVAL, "n %d / null sample_ids", n);
-  DeviceGuard guard(p->cfg.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-  std::vector<SampleRec*> recs;
-  std::vector<std::vector<int32_t>> moving;   // per sample: indices of pages to move
-  std::unordered_set<uint64_t> seen;
-  int64_t need = 0;
-  for (int32_t i = 0; i < n; ++i) {
-    auto it = p->samples.find(sample_ids[i]);
-    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-    if (!seen.insert(sample_ids[i]).second)
-      return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
-    std::vector<int32_t> mv;
-    for (size_t k = 0; k < it->second.pages.size(); ++k) {
-      int64_t idx = 0;
-      if (p->page_index(it->second.pages[k], &idx) != tier) mv.push_back((int32_t)k);
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    if (p->cfg.alloc_policy != FP_ALLOC_SCATTER) return fail(FP_EINVAL, "migration needs the scatter policy");
+    if (tier != FP_TIER_HBM && tier != FP_TIER_HOST) return fail(FP_EINVAL, "tier %d", tier);
+    if (n < 0 || (n > 0 && !sample_ids)) return fail(FP_EINVAL, "n %d / null sample_ids", n);
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    std::vector<SampleRec*> recs;
+    std::vector<std::vector<int32_t>> moving;   // per sample: indices of pages to move
+    std::unordered_set<uint64_t> seen;
+    int64_t need = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      auto it = p->samples.find(sample_ids[i]);
+      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+      if (!seen.insert(sample_ids[i]).second)
+        return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
+      std::vector<int32_t> mv;
+      for (size_t k = 0; k < it->second.pages.size(); ++k) {
+        int64_t idx = 0;
+        if (p->page_index(it->second.pages[k], &idx) != tier) mv.push_back((int32_t)k);
+      }
+      if (mv.empty()) continue;
+      need += (int64_t)mv.size();
+      recs.push_back(&it->second);
+      moving.push_back(std::move(mv));
     }
-    if (mv.empty()) continue;
-    need += (int64_t)mv.size();
-    recs.push_back(&it->second);
-    moving.push_back(std::move(mv));
-  }
-  if (out_pages_moved) *out_pages_moved = need;
-  if (need == 0) return FP_OK;
-  // All-or-nothing: target pages and the new page lists are reserved first.
-  reclaim(p, false);
-  std::vector<int64_t> pl_off(recs.size(), -1);
-  auto unreserve = [&]() {
-    for (size_t j = 0; j < recs.size(); ++j)
-      if (pl_off[j] >= 0) p->meta.release(pl_off[j], align16(8 * (int64_t)recs[j]->pages.size()));
-    std::fill(pl_off.begin(), pl_off.end(), -1);
-  };
-  for (int attempt = 0;; ++attempt) {
-    bool ok = (int64_t)p->stack[tier].size() >= need;
-    for (size_t j = 0; ok && j < recs.size(); ++j) {
-      pl_off[j] = p->meta.alloc(align16(8 * (int64_t)recs[j]->pages.size()));
-      ok = pl_off[j] >= 0;
+    if (out_pages_moved) *out_pages_moved = need;
+    if (need == 0) return FP_OK;
+    // All-or-nothing: target pages and the new page lists are reserved first.
+    reclaim(p, false);
+    std::vector<int64_t> pl_off(recs.size(), -1);
+    auto unreserve = [&]() {
+      for (size_t j = 0; j < recs.size(); ++j)
+        if (pl_off[j] >= 0) p->meta.release(pl_off[j], align16(8 * (int64_t)recs[j]->pages.size()));
+      std::fill(pl_off.begin(), pl_off.end(), -1);
+    };
+    for (int attempt = 0;; ++attempt) {
+      bool ok = (int64_t)p->stack[tier].size() >= need;
+      for (size_t j = 0; ok && j < recs.size(); ++j) {
+        pl_off[j] = p->meta.alloc(align16(8 * (int64_t)recs[j]->pages.size()));
+        ok = pl_off[j] >= 0;
+      }
+      if (ok) break;
+      unreserve();
+      if (attempt > 0 || p->deferred.empty())
+        return fail(FP_ENOMEM, "%lld pages (or their page lists) do not fit in tier %d", (long long)need, tier);
+      reclaim(p, true);
     }
-    if (ok) break;
-    unreserve();
-    if (attempt > 0 || p->deferred.empty())
-      return fail(FP_ENOMEM, "%lld pages (or their page lists) do not fit in tier %d", (long long)need, tier);
-    reclaim(p, true);
-  }
-  hipStream_t hs = (hipStream_t)stream;
-  if (capturing(hs)) {
-    unreserve();
-    return fail(FP_ESTATE, "pool_migrate cannot be captured into a graph (it moves pages now)");
-  }
-  fp_status st = order_after_writes(p, recs, hs);   // the copies read what the writes wrote
-  if (st != FP_OK) {
-    unreserve();
-    return st;
-  }
-  // Staging: the new page lists, then each sample's new page_off for its descriptor.
-  size_t stage_bytes = 0;
-  for (SampleRec* r : recs) stage_bytes += (size_t)align16(8 * (int64_t)r->pages.size()) + 16;
-  Stage* sg = nullptr;
-  st = stage_acquire(p, stage_bytes, 0, &sg);
-  if (st != FP_OK) {
-    unreserve();
-    return st;
-  }
-  // From here on nothing fails half-way but a HIP error: take the pages.
-  std::vector<std::vector<uint64_t>> new_pages(recs.size());
-  std::vector<std::vector<uint64_t>> old_pages(recs.size());
-  // Consecutive pages whose old and new frames are both adjacent inside one
-  // backing chunk are copied as one run.
-  struct Run { uint64_t src, dst, bytes; int src_chunk, dst_chunk; };
-  std::vector<Run> runs;
-  const int64_t P = p->cfg.page_tokens;
-  auto chunk_of = [&](uint64_t addr) {
-    int id = 0;
-    for (int t = 0; t < 2; ++t) {
-      const uint64_t chunk_span = (uint64_t)p->frames_per_chunk[t] * (uint64_t)p->pb;
-      for (void* c : p->chunks[t]) {
-        if (addr >= (uint64_t)c && addr < (uint64_t)c + chunk_span) return id;
-        ++id;
+    hipStream_t hs = (hipStream_t)stream;
+    if (capturing(hs)) {
+      unreserve();
+      return fail(FP_ESTATE, "pool_migrate cannot be captured into a graph (it moves pages now)");
+    }
+    fp_status st = order_after_writes(p, recs, hs);   // the copies read what the writes wrote
+    if (st != FP_OK) {
+      unreserve();
+      return st;
+    }
+    // Staging: the new page lists, then each sample's new page_off for its descriptor.
+    size_t stage_bytes = 0;
+    for (SampleRec* r : recs) stage_bytes += (size_t)align16(8 * (int64_t)r->pages.size()) + 16;
+    Stage* sg = nullptr;
+    st = stage_acquire(p, stage_bytes, 0, &sg);
+    if (st != FP_OK) {
+      unreserve();
+      return st;
+    }
+    // From here on nothing fails half-way but a HIP error: take the pages.
+    std::vector<std::vector<uint64_t>> new_pages(recs.size());
+    std::vector<std::vector<uint64_t>> old_pages(recs.size());
+    // Consecutive pages whose old and new frames are both adjacent inside one
+    // backing chunk are copied as one run.
+    struct Run { uint64_t src, dst, bytes; int src_chunk, dst_chunk; };
+    std::vector<Run> runs;
+    const int64_t P = p->cfg.page_tokens;
+    auto chunk_of = [&](uint64_t addr) {
+      int id = 0;
+      for (int t = 0; t < 2; ++t) {
+        const uint64_t chunk_span = (uint64_t)p->frames_per_chunk[t] * (uint64_t)p->pb;
+        for (void* c : p->chunks[t]) {
+          if (addr >= (uint64_t)c && addr < (uint64_t)c + chunk_span) return id;
+          ++id;
+        }
+      }
+      return -1;
+    };
+    for (size_t j = 0; j < recs.size(); ++j) {
+      SampleRec& r = *recs[j];
+      new_pages[j] = r.pages;
+      for (int32_t k : moving[j]) {
+        const int64_t i = p->stack[tier].back();
+        p->stack[tier].pop_back();
+        p->used[tier][i] = 1;
+        p->n_free[tier] -= 1;
+        const uint64_t gva = p->page_gva(tier, i);
+        const uint64_t src = p->pte[(size_t)((r.pages[(size_t)k] - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
+        const uint64_t dst = p->pte[(size_t)((gva - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
+        const int64_t rows = std::min<int64_t>(P, r.n_vis - (int64_t)k * P);
+        const uint64_t bytes = (uint64_t)(rows * p->rb);
+        const int sc = chunk_of(src), dc = chunk_of(dst);
+        if (!runs.empty() && runs.back().src + runs.back().bytes == src && runs.back().dst + runs.back().bytes == dst &&
+            runs.back().bytes % (uint64_t)p->pb == 0 && runs.back().src_chunk == sc && runs.back().dst_chunk == dc)
+          runs.back().bytes += bytes;
+        else
+          runs.push_back(Run{src, dst, bytes, sc, dc});
+        old_pages[j].push_back(r.pages[(size_t)k]);
+        new_pages[j][(size_t)k] = gva;
       }
     }
-    return -1;
-  };
-  for (size_t j = 0; j < recs.size(); ++j) {
-    SampleRec& r = *recs[j];
-    new_pages[j] = r.pages;
-    for (int32_t k : moving[j]) {
-      const int64_t i = p->stack[tier].back();
-      p->stack[tier].pop_back();
-      p->used[tier][i] = 1;
-      p->n_free[tier] -= 1;
-      const uint64_t gva = p->page_gva(tier, i);
-      const uint64_t src = p->pte[(size_t)((r.pages[(size_t)k] - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
-      const uint64_t dst = p->pte[(size_t)((gva - p->gva_start) / (uint64_t)p->pb)] & fp::PTE_ADDR_MASK;
-      const int64_t rows = std::min<int64_t>(P, r.n_vis - (int64_t)k * P);
-      const uint64_t bytes = (uint64_t)(rows * p->rb);
-      const int sc = chunk_of(src), dc = chunk_of(dst);
-      if (!runs.empty() && runs.back().src + runs.back().bytes == src && runs.back().dst + runs.back().bytes == dst &&
-          runs.back().bytes % (uint64_t)p->pb == 0 && runs.back().src_chunk == sc && runs.back().dst_chunk == dc)
-        runs.back().bytes += bytes;
-      else
-        runs.push_back(Run{src, dst, bytes, sc, dc});
-      old_pages[j].push_back(r.pages[(size_t)k]);
-      new_pages[j][(size_t)k] = gva;
+    hipError_t e = hipSuccess;
+    for (const Run& run : runs) {
+      e = hipMemcpyAsync((void*)run.dst, (const void*)run.src, run.bytes, hipMemcpyDefault, hs);
+      if (e != hipSuccess) break;
     }
-  }
-  hipError_t e = hipSuccess;
-  for (const Run& run : runs) {
-    e = hipMemcpyAsync((void*)run.dst, (const void*)run.src, run.bytes, hipMemcpyDefault, hs);
-    if (e != hipSuccess) break;
-  }
-  size_t at = 0;
-  for (size_t j = 0; e == hipSuccess && j < recs.size(); ++j) {
-    const size_t nb = 8 * new_pages[j].size();
-    std::memcpy(sg->host + at, new_pages[j].data(), nb);
-    e = hipMemcpyAsync(p->meta_dev + pl_off[j], sg->host + at, nb, hipMemcpyHostToDevice, hs);
-    at += (size_t)align16((int64_t)nb);
-    if (e != hipSuccess) break;
-    std::memcpy(sg->host + at, &pl_off[j], 8);
-    e = hipMemcpyAsync(&p->desc_dev[recs[j]->slot].page_off, sg->host + at, 8, hipMemcpyHostToDevice, hs);
-    at += 16;
-  }
-  int32_t ev = -1;
-  if (e == hipSuccess) e = p->events.acquire(&ev);
-  if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
-  if (e != hipSuccess) {
-    // Queued copies may still run: wait for them, then put everything back.
-    (void)hipStreamSynchronize(hs);
-    if (ev >= 0) p->events.unref(ev);
+    size_t at = 0;
+    for (size_t j = 0; e == hipSuccess && j < recs.size(); ++j) {
+      const size_t nb = 8 * new_pages[j].size();
+      std::memcpy(sg->host + at, new_pages[j].data(), nb);
+      e = hipMemcpyAsync(p->meta_dev + pl_off[j], sg->host + at, nb, hipMemcpyHostToDevice, hs);
+      at += (size_t)align16((int64_t)nb);
+      if (e != hipSuccess) break;
+      std::memcpy(sg->host + at, &pl_off[j], 8);
+      e = hipMemcpyAsync(&p->desc_dev[recs[j]->slot].page_off, sg->host + at, 8, hipMemcpyHostToDevice, hs);
+      at += 16;
+    }
+    int32_t ev = -1;
+    if (e == hipSuccess) e = p->events.acquire(&ev);
+    if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
+    if (e != hipSuccess) {
+      // Queued copies may still run: wait for them, then put everything back.
+      (void)hipStreamSynchronize(hs);
+      if (ev >= 0) p->events.unref(ev);
+      for (size_t j = 0; j < recs.size(); ++j) {
+        std::vector<uint64_t> taken;
+        for (int32_t k : moving[j]) taken.push_back(new_pages[j][(size_t)k]);
+        release_pages(p, taken);
+      }
+      unreserve();
+      return fail(FP_EHIP, "migration copies: %s", hipGetErrorString(e));
+    }
+    st = stage_release(sg, hs);
+    // The pages left behind and the old page lists wait for the copies and for
+    // every pack that may still read them.
     for (size_t j = 0; j < recs.size(); ++j) {
-      std::vector<uint64_t> taken;
-      for (int32_t k : moving[j]) taken.push_back(new_pages[j][(size_t)k]);
-      release_pages(p, taken);
+      SampleRec& r = *recs[j];
+      Deferred d;
+      d.pages = std::move(old_pages[j]);
+      const int64_t pl_bytes = align16(8 * (int64_t)r.pages.size());
+      if (r.pl_off >= 0) {
+        d.meta.emplace_back(r.pl_off, r.pl_len);
+      } else {
+        d.meta.emplace_back(r.meta_off, pl_bytes);     // the head of the main block
+        r.meta_off += pl_bytes;
+        r.meta_len -= pl_bytes;
+      }
+      r.pl_off = pl_off[j];
+      r.pl_len = pl_bytes;
+      r.page_off = pl_off[j];
+      r.pages = std::move(new_pages[j]);
+      fp_status ms = mark_readers(p, r.readers, &d.events);
+      if (ms != FP_OK) {
+        // Without an event on every reader, wait for the whole device instead.
+        (void)hipDeviceSynchronize();
+        if (st == FP_OK) st = ms;
+      }
+      p->events.ref(ev);
+      d.events.push_back(ev);
+      if (r.written >= 0) p->events.unref(r.written);
+      p->events.ref(ev);
+      r.written = ev;
+      r.write_stream = stream;
+      defer_or_release(p, std::move(d));
     }
-    unreserve();
-    return fail(FP_EHIP, "migration copies: %s", hipGetErrorString(e));
-  }
-  st = stage_release(sg, hs);
-  // The pages left behind and the old page lists wait for the copies and for
-  // every pack that may still read them.
-  for (size_t j = 0; j < recs.size(); ++j) {
-    SampleRec& r = *recs[j];
-    Deferred d;
-    d.pages = std::move(old_pages[j]);
-    const int64_t pl_bytes = align16(8 * (int64_t)r.pages.size());
-    if (r.pl_off >= 0) {
-      d.meta.emplace_back(r.pl_off, r.pl_len);
-    } else {
-      d.meta.emplace_back(r.meta_off, pl_bytes);     // the head of the main block
-      r.meta_off += pl_bytes;
-      r.meta_len -= pl_bytes;
-    }
-    r.pl_off = pl_off[j];
-    r.pl_len = pl_bytes;
-    r.page_off = pl_off[j];
-    r.pages = std::move(new_pages[j]);
-    fp_status ms = mark_readers(p, r.readers, &d.events);
-    if (ms != FP_OK) {
-      // Without an event on every reader, wait for the whole device instead.
-      (void)hipDeviceSynchronize();
-      if (st == FP_OK) st = ms;
-    }
-    p->events.ref(ev);
-    d.events.push_back(ev);
-    if (r.written >= 0) p->events.unref(r.written);
-    p->events.ref(ev);
-    r.written = ev;
-    r.write_stream = stream;
-    defer_or_release(p, std::move(d));
-  }
-  p->events.unref(ev);
-  return st;
+    p->events.unref(ev);
+    return st;
+  });
 }
 
 fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
                          int32_t capacity, int32_t n_mb, int32_t policy, int32_t* out_assign,
                          int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled,
                          int32_t* out_mb_max_len) {
-  if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28))
-    return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d", n, n_mb, capacity);
-  if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
-  if (n && (!lengths || !costs_scaled || !out_assign)) return fail(FP_EINVAL, "null array");
-  for (int32_t i = 0; i < n; ++i)
-    if (lengths[i] < 1 || costs_scaled[i] < 0) return fail(FP_EINVAL, "sample %d length/cost", i);
-  return greedy(lengths, costs_scaled, n, capacity, n_mb, policy, out_assign, out_mb_tokens, out_mb_cost_scaled,
-                out_mb_max_len);
+  return guarded([&]() -> fp_status {
+    if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28))
+      return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d", n, n_mb, capacity);
+    if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
+    if (n && (!lengths || !costs_scaled || !out_assign)) return fail(FP_EINVAL, "null array");
+    for (int32_t i = 0; i < n; ++i)
+      if (lengths[i] < 1 || costs_scaled[i] < 0) return fail(FP_EINVAL, "sample %d length/cost", i);
+    return greedy(lengths, costs_scaled, n, capacity, n_mb, policy, out_assign, out_mb_tokens, out_mb_cost_scaled,
+                  out_mb_max_len);
+  });
 }
 
 fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
                             int32_t n_mb, int32_t cost_k, int32_t policy, int32_t* out_assign,
                             int32_t* out_mb_tokens, int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
                             int64_t* out_sample_cost_scaled, void* stream) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  std::lock_guard<std::mutex> lock(p->mu);
-  if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28) || cost_k < 1 ||
-      cost_k > (1 << 24))
-    return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d, cost_k %d", n, n_mb, capacity, cost_k);
-  if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
-  if (n && (!sample_ids || !out_assign)) return fail(FP_EINVAL, "null array");
-  std::vector<int32_t> slots((size_t)n), lens((size_t)n);
-  std::vector<SampleRec*> recs((size_t)n);
-  std::unordered_set<uint64_t> seen;
-  seen.reserve((size_t)n * 2);
-  for (int32_t i = 0; i < n; ++i) {
-    auto it = p->samples.find(sample_ids[i]);
-    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-    if (!seen.insert(sample_ids[i]).second)
-      return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
-    slots[(size_t)i] = it->second.slot;
-    lens[(size_t)i] = it->second.len;
-    recs[(size_t)i] = &it->second;
-  }
-  std::vector<int64_t> costs((size_t)n);
-  if (n > 0) {
-    DeviceGuard guard(p->cfg.device);
-    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-    hipStream_t hs = (hipStream_t)stream;
-    if (capturing(hs)) return fail(FP_ESTATE, "plan_microbatches waits for its result and cannot be captured");
-    const size_t slot_bytes = align16(4ll * n);
-    Stage* s = nullptr;
-    fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, slot_bytes + 8 * (size_t)n, &s);
-    if (st != FP_OK) return st;
-    std::memcpy(s->host, slots.data(), 4 * (size_t)n);
-    FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
-    st = order_after_writes(p, recs, hs);   // the descriptors come from the writes
-    if (st != FP_OK) return st;
-    FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->dev, n, cost_k, (int64_t*)(s->dev + slot_bytes), hs));
-    FP_HIP(hipMemcpyAsync(s->host + slot_bytes, s->dev + slot_bytes, 8 * (size_t)n, hipMemcpyDeviceToHost, hs));
-    FP_HIP(hipStreamSynchronize(hs));
-    std::memcpy(costs.data(), s->host + slot_bytes, 8 * (size_t)n);
-    st = stage_release(s, hs);
-    if (st != FP_OK) return st;
-  }
-  if (out_sample_cost_scaled) std::memcpy(out_sample_cost_scaled, costs.data(), 8 * (size_t)n);
-  return greedy(lens.data(), costs.data(), n, capacity, n_mb, policy, out_assign, out_mb_tokens,
-                out_mb_cost_scaled, out_mb_max_len);
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    if (n < 0 || n_mb < 1 || n_mb > kMaxPlanMicrobatches || capacity < 1 || capacity > (1 << 28) || cost_k < 1 ||
+        cost_k > (1 << 24))
+      return fail(FP_EINVAL, "n %d, n_mb %d, capacity %d, cost_k %d", n, n_mb, capacity, cost_k);
+    if (policy != FP_PLAN_LPT && policy != FP_PLAN_ZIGZAG) return fail(FP_EINVAL, "policy %d", policy);
+    if (n && (!sample_ids || !out_assign)) return fail(FP_EINVAL, "null array");
+    std::vector<int32_t> slots((size_t)n), lens((size_t)n);
+    std::vector<SampleRec*> recs((size_t)n);
+    std::unordered_set<uint64_t> seen;
+    seen.reserve((size_t)n * 2);
+    for (int32_t i = 0; i < n; ++i) {
+      auto it = p->samples.find(sample_ids[i]);
+      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+      if (!seen.insert(sample_ids[i]).second)
+        return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
+      slots[(size_t)i] = it->second.slot;
+      lens[(size_t)i] = it->second.len;
+      recs[(size_t)i] = &it->second;
+    }
+    std::vector<int64_t> costs((size_t)n);
+    if (n > 0) {
+      DeviceGuard guard(p->cfg.device);
+      if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+      hipStream_t hs = (hipStream_t)stream;
+      if (capturing(hs)) return fail(FP_ESTATE, "plan_microbatches waits for its result and cannot be captured");
+      const size_t slot_bytes = align16(4ll * n);
+      Stage* s = nullptr;
+      fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, slot_bytes + 8 * (size_t)n, &s);
+      if (st != FP_OK) return st;
+      std::memcpy(s->host, slots.data(), 4 * (size_t)n);
+      FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
+      st = order_after_writes(p, recs, hs);   // the descriptors come from the writes
+      if (st != FP_OK) return st;
+      FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->dev, n, cost_k, (int64_t*)(s->dev + slot_bytes), hs));
+      FP_HIP(hipMemcpyAsync(s->host + slot_bytes, s->dev + slot_bytes, 8 * (size_t)n, hipMemcpyDeviceToHost, hs));
+      FP_HIP(hipStreamSynchronize(hs));
+      std::memcpy(costs.data(), s->host + slot_bytes, 8 * (size_t)n);
+      st = stage_release(s, hs);
+      if (st != FP_OK) return st;
+    }
+    if (out_sample_cost_scaled) std::memcpy(out_sample_cost_scaled, costs.data(), 8 * (size_t)n);
+    return greedy(lens.data(), costs.data(), n, capacity, n_mb, policy, out_assign, out_mb_tokens,
+                  out_mb_cost_scaled, out_mb_max_len);
+  });
 }
 
 namespace {
@@ -1143,7 +1180,7 @@ fp_status check_packing_args(int32_t n, int32_t capacity, int32_t n_ranks, int32
   if (n < 0) return fail(FP_EINVAL, "n %d", n);
   if (capacity < 1 || capacity > kMaxPackingCapacity)
     return fail(FP_EINVAL, "capacity %d outside [1, %d]", capacity, kMaxPackingCapacity);
-  if (n_ranks < 1) return fail(FP_EINVAL, "n_ranks %d", n_ranks);
+  if (n_ranks < 1 || n_ranks > (1 << 20)) return fail(FP_EINVAL, "n_ranks %d outside [1, 2^20]", n_ranks);
   if (n_buckets < 1) return fail(FP_EINVAL, "n_buckets %d", n_buckets);
   return FP_OK;
 }
@@ -1153,262 +1190,272 @@ fp_status check_packing_args(int32_t n, int32_t capacity, int32_t n_ranks, int32
 fp_status alloc_candidates(int32_t backbone, int32_t devices, int32_t per_node, int32_t global_batch,
                            int32_t layers, int32_t* out_dp, int32_t* out_tp, int32_t* out_pp, int32_t cap,
                            int32_t* out_n) {
-  if (devices < 1 || per_node < 1 || global_batch < 1 || layers < 1 || devices > (1 << 20) ||
-      per_node > 4096 || global_batch > (1 << 24) || layers > 65536)
-    return fail(FP_EINVAL, "devices %d, per_node %d, global_batch %d, layers %d", devices, per_node,
-                global_batch, layers);
-  if (!out_n) return fail(FP_EINVAL, "null out_n");
-  const std::vector<fp::Config> c = fp::prune_candidates(backbone != 0, devices, per_node, global_batch, layers);
-  *out_n = (int32_t)c.size();
-  if ((int64_t)c.size() > cap) return fail(FP_EINVAL, "%zu candidates, room for %d", c.size(), cap);
-  for (size_t i = 0; i < c.size(); ++i) {
-    if (out_dp) out_dp[i] = c[i].dp;
-    if (out_tp) out_tp[i] = c[i].tp;
-    if (out_pp) out_pp[i] = c[i].pp;
-  }
-  return FP_OK;
+  return guarded([&]() -> fp_status {
+    if (devices < 1 || per_node < 1 || global_batch < 1 || layers < 1 || devices > (1 << 20) ||
+        per_node > 4096 || global_batch > (1 << 24) || layers > 65536)
+      return fail(FP_EINVAL, "devices %d, per_node %d, global_batch %d, layers %d", devices, per_node,
+                  global_batch, layers);
+    if (!out_n) return fail(FP_EINVAL, "null out_n");
+    const std::vector<fp::Config> c = fp::prune_candidates(backbone != 0, devices, per_node, global_batch, layers);
+    *out_n = (int32_t)c.size();
+    if ((int64_t)c.size() > cap) return fail(FP_EINVAL, "%zu candidates, room for %d", c.size(), cap);
+    for (size_t i = 0; i < c.size(); ++i) {
+      if (out_dp) out_dp[i] = c[i].dp;
+      if (out_tp) out_tp[i] = c[i].tp;
+      if (out_pp) out_pp[i] = c[i].pp;
+    }
+    return FP_OK;
+  });
 }
 
 fp_status plan_allocation(int32_t n_modules, const int32_t* n_configs, const int64_t* tau, const int64_t* cost,
                           int64_t budget, int32_t* out_choice, int64_t* out_G, int64_t* out_F,
                           int64_t* out_devices) {
-  if (n_modules < 2 || n_modules > 64) return fail(FP_EINVAL, "n_modules %d (encoders + 1 backbone)", n_modules);
-  if (!n_configs || !tau || !cost) return fail(FP_EINVAL, "null array");
-  if (budget < 0) return fail(FP_EINVAL, "budget %lld", (long long)budget);
-  std::vector<std::vector<int64_t>> t((size_t)n_modules), c((size_t)n_modules);
-  double combos = 1;
-  size_t at = 0;
-  for (int32_t i = 0; i < n_modules; ++i) {
-    if (n_configs[i] < 1) return fail(FP_EINVAL, "module %d has %d configurations", i, n_configs[i]);
-    if (i < n_modules - 1) combos *= n_configs[i];
-    for (int32_t k = 0; k < n_configs[i]; ++k, ++at) {
-      if (tau[at] < 0 || tau[at] > (1ll << 50) || cost[at] < 0 || cost[at] > (1ll << 40))
-        return fail(FP_EINVAL, "module %d configuration %d: tau %lld, cost %lld", i, k, (long long)tau[at],
-                    (long long)cost[at]);
-      t[(size_t)i].push_back(tau[at]);
-      c[(size_t)i].push_back(cost[at]);
+  return guarded([&]() -> fp_status {
+    if (n_modules < 2 || n_modules > 64) return fail(FP_EINVAL, "n_modules %d (encoders + 1 backbone)", n_modules);
+    if (!n_configs || !tau || !cost) return fail(FP_EINVAL, "null array");
+    if (budget < 0) return fail(FP_EINVAL, "budget %lld", (long long)budget);
+    std::vector<std::vector<int64_t>> t((size_t)n_modules), c((size_t)n_modules);
+    double combos = 1;
+    size_t at = 0;
+    for (int32_t i = 0; i < n_modules; ++i) {
+      if (n_configs[i] < 1) return fail(FP_EINVAL, "module %d has %d configurations", i, n_configs[i]);
+      if (i < n_modules - 1) combos *= n_configs[i];
+      for (int32_t k = 0; k < n_configs[i]; ++k, ++at) {
+        if (tau[at] < 0 || tau[at] > (1ll << 50) || cost[at] < 0 || cost[at] > (1ll << 40))
+          return fail(FP_EINVAL, "module %d configuration %d: tau %lld, cost %lld", i, k, (long long)tau[at],
+                      (long long)cost[at]);
+        t[(size_t)i].push_back(tau[at]);
+        c[(size_t)i].push_back(cost[at]);
+      }
     }
-  }
-  if (combos > (double)(1 << 22)) return fail(FP_EINVAL, "%.0f encoder combinations (at most 2^22)", combos);
-  fp::FlowChoice best;
-  if (!fp::flow_match(t, c, budget, &best))
-    return fail(FP_ECAPACITY, "no choice of configurations fits %lld devices", (long long)budget);
-  if (out_choice) std::copy(best.choice.begin(), best.choice.end(), out_choice);
-  if (out_G) *out_G = best.G;
-  if (out_F) *out_F = best.F;
-  if (out_devices) *out_devices = best.devices;
-  return FP_OK;
+    if (combos > (double)(1 << 22)) return fail(FP_EINVAL, "%.0f encoder combinations (at most 2^22)", combos);
+    fp::FlowChoice best;
+    if (!fp::flow_match(t, c, budget, &best))
+      return fail(FP_ECAPACITY, "no choice of configurations fits %lld devices", (long long)budget);
+    if (out_choice) std::copy(best.choice.begin(), best.choice.end(), out_choice);
+    if (out_G) *out_G = best.G;
+    if (out_F) *out_F = best.F;
+    if (out_devices) *out_devices = best.devices;
+    return FP_OK;
+  });
 }
 
 fp_status plan_dynamic_packing(const int32_t* lengths, int32_t n, int32_t capacity, int32_t n_ranks,
                                int32_t n_buckets, int32_t* out_mb_of_seq, int32_t* out_n_mb,
                                int32_t* out_mb_tokens, int32_t* out_mb_max_len, int64_t* out_mb_cost_scaled,
                                int32_t* out_mb_bucket, int32_t* out_mb_rank, int32_t* out_mb_slot) {
-  fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
-  if (st != FP_OK) return st;
-  if (n > 0 && !lengths) return fail(FP_EINVAL, "null lengths");
-  for (int32_t i = 0; i < n; ++i)
-    if (lengths[i] < 1 || lengths[i] > capacity)
-      return fail(FP_EINVAL, "length %d of sequence %d outside [1, %d]", lengths[i], i, capacity);
-  fp::PackingPlan plan;
-  fp::dynamic_packing(lengths, n, capacity, n_ranks, n_buckets, &plan);
-  return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
-                         out_mb_bucket, out_mb_rank, out_mb_slot);
+  return guarded([&]() -> fp_status {
+    fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
+    if (st != FP_OK) return st;
+    if (n > 0 && !lengths) return fail(FP_EINVAL, "null lengths");
+    for (int32_t i = 0; i < n; ++i)
+      if (lengths[i] < 1 || lengths[i] > capacity)
+        return fail(FP_EINVAL, "length %d of sequence %d outside [1, %d]", lengths[i], i, capacity);
+    fp::PackingPlan plan;
+    fp::dynamic_packing(lengths, n, capacity, n_ranks, n_buckets, &plan);
+    return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
+                           out_mb_bucket, out_mb_rank, out_mb_slot);
+  });
 }
 
 fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
                             int32_t n_ranks, int32_t n_buckets, int32_t* out_mb_of_seq, int32_t* out_n_mb,
                             int32_t* out_mb_tokens, int32_t* out_mb_max_len, int64_t* out_mb_cost_scaled,
                             int32_t* out_mb_bucket, int32_t* out_mb_rank, int32_t* out_mb_slot) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
-  if (st != FP_OK) return st;
-  if (n > 0 && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
-  std::vector<int32_t> lens((size_t)n);
-  {
-    std::lock_guard<std::mutex> lock(p->mu);
-    for (int32_t i = 0; i < n; ++i) {
-      auto it = p->samples.find(sample_ids[i]);
-      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-      lens[(size_t)i] = it->second.len;
-      if (lens[(size_t)i] > capacity)
-        return fail(FP_EINVAL, "sample %llu of length %d exceeds capacity %d",
-                    (unsigned long long)sample_ids[i], lens[(size_t)i], capacity);
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    fp_status st = check_packing_args(n, capacity, n_ranks, n_buckets);
+    if (st != FP_OK) return st;
+    if (n > 0 && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
+    std::vector<int32_t> lens((size_t)n);
+    {
+      std::lock_guard<std::mutex> lock(p->mu);
+      for (int32_t i = 0; i < n; ++i) {
+        auto it = p->samples.find(sample_ids[i]);
+        if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+        lens[(size_t)i] = it->second.len;
+        if (lens[(size_t)i] > capacity)
+          return fail(FP_EINVAL, "sample %llu of length %d exceeds capacity %d",
+                      (unsigned long long)sample_ids[i], lens[(size_t)i], capacity);
+      }
     }
-  }
-  fp::PackingPlan plan;
-  fp::dynamic_packing(lens.data(), n, capacity, n_ranks, n_buckets, &plan);
-  return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
-                         out_mb_bucket, out_mb_rank, out_mb_slot);
+    fp::PackingPlan plan;
+    fp::dynamic_packing(lens.data(), n, capacity, n_ranks, n_buckets, &plan);
+    return packing_outputs(plan, out_mb_of_seq, out_n_mb, out_mb_tokens, out_mb_max_len, out_mb_cost_scaled,
+                           out_mb_bucket, out_mb_rank, out_mb_slot);
+  });
 }
 
 fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,
                           int64_t vocab, void* out_emb, int64_t out_rows_cap, int32_t* out_cu_seqlens,
                           int32_t* out_position_ids, int32_t* out_n_tokens, int32_t* out_max_seqlen,
                           int32_t tier_mask, void* stream) {
-  if (!p) return fail(FP_EINVAL, "null pool");
-  std::lock_guard<std::mutex> lock(p->mu);
-  if (n < 0 || n > fp::kMaxPackSamples) return fail(FP_EINVAL, "n %d outside [0, %d]", n, fp::kMaxPackSamples);
-  if (n && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
-  if (tier_mask < 1 || tier_mask > 3) return fail(FP_EINVAL, "tier_mask %d", tier_mask);
-  if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
-  if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
-  if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
-  std::vector<SampleRec*> recs((size_t)n);
-  int64_t total = 0, n_text = 0, n_imgs = 0;
-  int32_t mx = 0;
-  for (int32_t i = 0; i < n; ++i) {
-    auto it = p->samples.find(sample_ids[i]);
-    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-    SampleRec& r = it->second;
-    recs[(size_t)i] = &r;
-    total += r.len;
-    n_text += r.n_text;
-    n_imgs += r.n_img;
-    mx = std::max(mx, r.len);
-  }
-  if (n_imgs > fp::kMaxPackImages)
-    return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
-  if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
-  const int64_t vpr = p->rb / 16;
-  if (total * vpr > kMaxVectors)
-    return fail(FP_EINVAL, "microbatch of %lld rows of %lld bytes is too large", (long long)total, (long long)p->rb);
-  if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
-  if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
-    if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
-    if (vocab < p->cfg.vocab) return fail(FP_EINVAL, "table vocab %lld < pool vocab %lld", (long long)vocab, (long long)p->cfg.vocab);
-  }
-  DeviceGuard guard(p->cfg.device);
-  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-  hipStream_t hs = (hipStream_t)stream;
-  fp::PackArgs a{};
-  a.meta = p->meta_dev;
-  a.pte = p->pte_dev;
-  a.gva_start = p->gva_start;
-  a.page_bytes = (uint64_t)p->pb;
-  a.table = (const uint8_t*)embed_table;
-  a.out = (uint8_t*)out_emb;
-  a.cu = out_cu_seqlens;
-  a.pos = out_position_ids;
-  a.n = n;
-  a.n_tokens = (int32_t)total;
-  a.row_bytes = (int32_t)p->rb;
-  a.page_tokens = p->cfg.page_tokens;
-  a.tier_mask = tier_mask;
-  a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
-  fp::pack_chunks(&a, p->n_cu);
-  a.div_mul = p->dv.div_mul;
-  a.div_shift = p->dv.div_shift;
-  a.pt_mul = p->dv.pt_mul;
-  a.pt_shift = p->dv.pt_shift;
-  a.pb_mul = p->dv.pb_mul;
-  a.pb_shift = p->dv.pb_shift;
-  // The run table: sample lengths, then the runs of every sample in row
-  // order (a text run per nonempty stretch of text rows, an image run per
-  // stretch of images with no text row between them), then the bucket index.
-  std::vector<int32_t> lens((size_t)n), run_start;
-  std::vector<fp::PackRun> runs;
-  {
-    int32_t row = 0;
-    auto close_run = [&]() {
-      if (!runs.empty()) runs.back().end = row;
-    };
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    if (n < 0 || n > fp::kMaxPackSamples) return fail(FP_EINVAL, "n %d outside [0, %d]", n, fp::kMaxPackSamples);
+    if (n && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
+    if (tier_mask < 1 || tier_mask > 3) return fail(FP_EINVAL, "tier_mask %d", tier_mask);
+    if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
+    if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
+    if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
+    std::vector<SampleRec*> recs((size_t)n);
+    int64_t total = 0, n_text = 0, n_imgs = 0;
+    int32_t mx = 0;
     for (int32_t i = 0; i < n; ++i) {
-      const SampleRec& r = *recs[(size_t)i];
-      const int32_t s0 = row;
-      lens[(size_t)i] = r.len;
-      int32_t ti = 0, vis = 0;
-      bool in_image = false;
-      auto text_to = [&](int32_t upto) {
-        if (upto <= ti) return;
-        close_run();
-        run_start.push_back(row);
-        runs.push_back(fp::PackRun{0, s0 | fp::kTextRun, 0, (int32_t)(r.text_off / 4 + ti - row)});
-        row += upto - ti;
-        ti = upto;
-        in_image = false;
+      auto it = p->samples.find(sample_ids[i]);
+      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+      SampleRec& r = it->second;
+      recs[(size_t)i] = &r;
+      total += r.len;
+      n_text += r.n_text;
+      n_imgs += r.n_img;
+      mx = std::max(mx, r.len);
+    }
+    if (n_imgs > fp::kMaxPackImages)
+      return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
+    if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
+    const int64_t vpr = p->rb / 16;
+    if (total * vpr > kMaxVectors)
+      return fail(FP_EINVAL, "microbatch of %lld rows of %lld bytes is too large", (long long)total, (long long)p->rb);
+    if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
+    if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
+      if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
+      if (vocab < p->cfg.vocab) return fail(FP_EINVAL, "table vocab %lld < pool vocab %lld", (long long)vocab, (long long)p->cfg.vocab);
+    }
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    hipStream_t hs = (hipStream_t)stream;
+    fp::PackArgs a{};
+    a.meta = p->meta_dev;
+    a.pte = p->pte_dev;
+    a.gva_start = p->gva_start;
+    a.page_bytes = (uint64_t)p->pb;
+    a.table = (const uint8_t*)embed_table;
+    a.out = (uint8_t*)out_emb;
+    a.cu = out_cu_seqlens;
+    a.pos = out_position_ids;
+    a.n = n;
+    a.n_tokens = (int32_t)total;
+    a.row_bytes = (int32_t)p->rb;
+    a.page_tokens = p->cfg.page_tokens;
+    a.tier_mask = tier_mask;
+    a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
+    fp::pack_chunks(&a, p->n_cu);
+    a.div_mul = p->dv.div_mul;
+    a.div_shift = p->dv.div_shift;
+    a.pt_mul = p->dv.pt_mul;
+    a.pt_shift = p->dv.pt_shift;
+    a.pb_mul = p->dv.pb_mul;
+    a.pb_shift = p->dv.pb_shift;
+    // The run table: sample lengths, then the runs of every sample in row
+    // order (a text run per nonempty stretch of text rows, an image run per
+    // stretch of images with no text row between them), then the bucket index.
+    std::vector<int32_t> lens((size_t)n), run_start;
+    std::vector<fp::PackRun> runs;
+    {
+      int32_t row = 0;
+      auto close_run = [&]() {
+        if (!runs.empty()) runs.back().end = row;
       };
-      for (int32_t j = 0; j < r.n_img; ++j) {
-        text_to(r.img[2 * (size_t)j]);
-        const int32_t nt = r.img[2 * (size_t)j + 1];
-        if (nt <= 0) continue;
-        if (!in_image) {
+      for (int32_t i = 0; i < n; ++i) {
+        const SampleRec& r = *recs[(size_t)i];
+        const int32_t s0 = row;
+        lens[(size_t)i] = r.len;
+        int32_t ti = 0, vis = 0;
+        bool in_image = false;
+        auto text_to = [&](int32_t upto) {
+          if (upto <= ti) return;
           close_run();
           run_start.push_back(row);
-          runs.push_back(fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)});
-          in_image = true;
+          runs.push_back(fp::PackRun{0, s0 | fp::kTextRun, 0, (int32_t)(r.text_off / 4 + ti - row)});
+          row += upto - ti;
+          ti = upto;
+          in_image = false;
+        };
+        for (int32_t j = 0; j < r.n_img; ++j) {
+          text_to(r.img[2 * (size_t)j]);
+          const int32_t nt = r.img[2 * (size_t)j + 1];
+          if (nt <= 0) continue;
+          if (!in_image) {
+            close_run();
+            run_start.push_back(row);
+            runs.push_back(fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)});
+            in_image = true;
+          }
+          row += nt;
+          vis += nt;
         }
-        row += nt;
-        vis += nt;
+        text_to(r.n_text);
       }
-      text_to(r.n_text);
+      close_run();
     }
-    close_run();
-  }
-  const int32_t n_runs = (int32_t)runs.size();
-  int32_t shift = 0;
-  while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
-  const int32_t n_buckets = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
-  std::vector<uint16_t> bucket((size_t)(n_buckets + (n_buckets & 1)), 0);
-  for (int32_t b = 0, sidx = 0; b < n_buckets; ++b) {
-    const int64_t first = (int64_t)b << shift;
-    while (sidx + 1 < n_runs && run_start[(size_t)sidx + 1] <= first) ++sidx;
-    bucket[(size_t)b] = (uint16_t)sidx;
-  }
-  a.n_runs = n_runs;
-  a.bucket_shift = shift;
-  const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;
-  if (capturing(hs)) {
-    // A captured pack is one kernel whose arguments hold the whole
-    // microbatch, so a replay packs the same samples again.
-    if (staged)
-      return fail(FP_ESTATE, "a pack of more than %d samples or %d runs cannot be captured into a graph",
-                  fp::kInlineSamples, fp::kInlineRuns);
-    // No event queries during capture: the writes must already be known complete.
+    const int32_t n_runs = (int32_t)runs.size();
+    int32_t shift = 0;
+    while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
+    const int32_t n_buckets = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
+    std::vector<uint16_t> bucket((size_t)(n_buckets + (n_buckets & 1)), 0);
+    for (int32_t b = 0, sidx = 0; b < n_buckets; ++b) {
+      const int64_t first = (int64_t)b << shift;
+      while (sidx + 1 < n_runs && run_start[(size_t)sidx + 1] <= first) ++sidx;
+      bucket[(size_t)b] = (uint16_t)sidx;
+    }
+    a.n_runs = n_runs;
+    a.bucket_shift = shift;
+    const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;
+    if (capturing(hs)) {
+      // A captured pack is one kernel whose arguments hold the whole
+      // microbatch, so a replay packs the same samples again.
+      if (staged)
+        return fail(FP_ESTATE, "a pack of more than %d samples or %d runs cannot be captured into a graph",
+                    fp::kInlineSamples, fp::kInlineRuns);
+      // No event queries during capture: the writes must already be known complete.
+      for (SampleRec* r : recs)
+        if (r->written >= 0)
+          return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
+                                 "before capturing its pack");
+    }
+    Stage* s = nullptr;
+    if (!staged) {
+      if (n) std::memcpy(a.lens, lens.data(), 4 * lens.size());
+      if (n_runs) std::memcpy(a.runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
+      if (n_buckets) std::memcpy(a.bucket, bucket.data(), 2 * (size_t)n_buckets);
+      a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
+      a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
+    } else {
+      const size_t o_runs = (4 * lens.size() + 15) & ~(size_t)15;
+      const size_t o_b = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
+      const size_t bytes = o_b + 2 * bucket.size();
+      fp_status st = stage_acquire(p, bytes, bytes, &s);
+      if (st != FP_OK) return st;
+      std::memset(s->host, 0, bytes);
+      if (n) std::memcpy(s->host, lens.data(), 4 * lens.size());
+      if (n_runs) std::memcpy(s->host + o_runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
+      if (!bucket.empty()) std::memcpy(s->host + o_b, bucket.data(), 2 * bucket.size());
+      FP_HIP(hipMemcpyAsync(s->dev, s->host, bytes, hipMemcpyHostToDevice, hs));
+      a.staged = s->dev;
+      a.off_runs = (int32_t)o_runs;
+      a.off_bucket = (int32_t)o_b;
+    }
+    {
+      fp_status st = order_after_writes(p, recs, hs);
+      if (st != FP_OK) return st;
+    }
+    hipError_t e = fp::launch_pack(a, hs);
+    if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
+    if (s) {
+      fp_status st = stage_release(s, hs);
+      if (st != FP_OK) return st;
+    }
+    // Remember the stream as a reader of each sample; a free records its event
+    // there (no event per pack: events between back-to-back packs slow them).
     for (SampleRec* r : recs)
-      if (r->written >= 0)
-        return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
-                               "before capturing its pack");
-  }
-  Stage* s = nullptr;
-  if (!staged) {
-    if (n) std::memcpy(a.lens, lens.data(), 4 * lens.size());
-    if (n_runs) std::memcpy(a.runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
-    if (n_buckets) std::memcpy(a.bucket, bucket.data(), 2 * (size_t)n_buckets);
-    a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
-    a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
-  } else {
-    const size_t o_runs = (4 * lens.size() + 15) & ~(size_t)15;
-    const size_t o_b = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
-    const size_t bytes = o_b + 2 * bucket.size();
-    fp_status st = stage_acquire(p, bytes, bytes, &s);
-    if (st != FP_OK) return st;
-    std::memset(s->host, 0, bytes);
-    if (n) std::memcpy(s->host, lens.data(), 4 * lens.size());
-    if (n_runs) std::memcpy(s->host + o_runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
-    if (!bucket.empty()) std::memcpy(s->host + o_b, bucket.data(), 2 * bucket.size());
-    FP_HIP(hipMemcpyAsync(s->dev, s->host, bytes, hipMemcpyHostToDevice, hs));
-    a.staged = s->dev;
-    a.off_runs = (int32_t)o_runs;
-    a.off_bucket = (int32_t)o_b;
-  }
-  {
-    fp_status st = order_after_writes(p, recs, hs);
-    if (st != FP_OK) return st;
-  }
-  hipError_t e = fp::launch_pack(a, hs);
-  if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
-  if (s) {
-    fp_status st = stage_release(s, hs);
-    if (st != FP_OK) return st;
-  }
-  // Remember the stream as a reader of each sample; a free records its event
-  // there (no event per pack: events between back-to-back packs slow them).
-  for (SampleRec* r : recs)
-    if (std::find(r->readers.begin(), r->readers.end(), stream) == r->readers.end()) r->readers.push_back(stream);
-  if (out_n_tokens) *out_n_tokens = (int32_t)total;
-  if (out_max_seqlen) *out_max_seqlen = mx;
-  return FP_OK;
+      if (std::find(r->readers.begin(), r->readers.end(), stream) == r->readers.end()) r->readers.push_back(stream);
+    if (out_n_tokens) *out_n_tokens = (int32_t)total;
+    if (out_max_seqlen) *out_max_seqlen = mx;
+    return FP_OK;
+  });
 }
 
 fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages, int64_t* n_samples) {

@@ -69,6 +69,9 @@ def test_plan_partition_errors():
         fp.plan_partition([0], [0], 10, 1)
     assert e.value.code == "EINVAL"
     assert fp.plan_partition([], [], 10, 2)["mb_tokens"].tolist() == [0, 0]
+    with pytest.raises(fp.FlowPoolError) as e:
+        fp.plan_dynamic_packing([5, 6], 10, (1 << 20) + 1, 2)
+    assert e.value.code == "EINVAL"
     for bad in (dict(policy=2), dict(policy=-1), dict(n_mb=(1 << 20) + 1)):
         args = dict(lengths=[1], costs_scaled=[1], capacity=10, n_mb=2)
         args.update(bad)
