@@ -32,6 +32,20 @@ def test_exports_every_declared_symbol():
     assert fp.fp_abi_version() == fp.ABI_VERSION == 4
 
 
+def test_constants_match_header():
+    """Every FP_* enumerator of the header has the same value in the bindings."""
+    src = open(os.path.join(ROOT, "include", "flowpool.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    consts = {}
+    for body in re.findall(r"enum\s*\{(.*?)\}", src, flags=re.S):
+        for name, val in re.findall(r"(FP_\w+)\s*=\s*(-?\d+)", body):
+            consts[name] = int(val)
+    assert len(consts) == 17
+    for name, val in consts.items():
+        assert getattr(fp, name) == val, name
+    assert int(re.search(r"#define FP_ABI_VERSION (\d+)", src).group(1)) == fp.ABI_VERSION
+
+
 def test_config_struct_matches_header():
     # fp_pool_config: 2*i32, 2*i64, 2*i32, i64, u64, 2*i32, 2*i64, u64, i64, 2 ptrs, 2*i32
     assert ctypes.sizeof(fp.fp_pool_config) == 8 + 16 + 8 + 8 + 8 + 8 + 16 + 8 + 8 + 16 + 8
