@@ -746,6 +746,9 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
       }
       if (attr.type == hipMemoryTypeUnregistered || !attr.devicePointer)
         return fail(FP_EINVAL, "vis_emb is ordinary host memory, not device-accessible");
+      if (attr.type == hipMemoryTypeDevice && attr.device != p->cfg.device)
+        return fail(FP_EINVAL, "vis_emb is memory of device %d, the pool is on device %d", attr.device,
+                    p->cfg.device);
       vis_dev = (const uint8_t*)attr.devicePointer;
     }
     const int64_t meta_len = align16(8 * n_pages) + align16(8ll * n_img) + align16(4ll * n_text);

@@ -140,14 +140,18 @@ def _ptr(x) -> Optional[int]:
 # Hidden size of each pool created through these bindings, to check buffer
 # sizes before the kernels touch them (pools created elsewhere are not checked).
 _HIDDEN = {}
+_DEVICE = {}
 # Caller-provided tier backings, kept alive while their pool exists.
 _BACKING = {}
 
 
-def _buf(x, nbytes: int, name: str) -> Optional[int]:
-    """Like ``_ptr``; a tensor must also be contiguous and hold ``nbytes``."""
+def _buf(x, nbytes: int, name: str, device: Optional[int] = None) -> Optional[int]:
+    """Like ``_ptr``; a tensor must also be contiguous, hold ``nbytes`` and,
+    if on a GPU, be on ``device`` (when given)."""
     if x is None or isinstance(x, int):
         return _ptr(x)
+    if device is not None and x.is_cuda and x.device.index != device:
+        raise ValueError(f"{name} is on cuda:{x.device.index}, the pool on cuda:{device}")
     if not x.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if x.numel() * x.element_size() < nbytes:
@@ -198,6 +202,7 @@ def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int =
     out = _P()
     _check(_lib.pool_create(C.byref(cfg), C.byref(out)), "pool_create")
     _HIDDEN[int(out.value)] = hidden
+    _DEVICE[int(out.value)] = device
     _BACKING[int(out.value)] = (hbm_backing, host_backing)
     return int(out.value)
 
@@ -205,6 +210,7 @@ def pool_create(hidden: int, page_tokens: int, hbm_pages: int, host_pages: int =
 def pool_destroy(pool: int) -> None:
     _check(_lib.pool_destroy(pool), "pool_destroy")
     _HIDDEN.pop(pool, None)
+    _DEVICE.pop(pool, None)
     _BACKING.pop(pool, None)
 
 
@@ -216,7 +222,7 @@ def pool_write_sample(pool: int, text_ids, img_pos, img_ntok, vis_emb=None, page
     w, wp = _arr(page_tier_wish, np.uint8, _u8p)
     sid = C.c_uint64()
     rb = 2 * _HIDDEN.get(pool, 0)
-    vis = _buf(vis_emb, int(v.sum(dtype=np.int64)) * rb if v is not None else 0, "vis_emb")
+    vis = _buf(vis_emb, int(v.sum(dtype=np.int64)) * rb if v is not None else 0, "vis_emb", _DEVICE.get(pool))
     _check(_lib.pool_write_sample(pool, tp, len(t), pp, vp, len(p), vis, wp, _stream(stream),
                                   C.byref(sid)), "pool_write_sample")
     return int(sid.value)
@@ -341,10 +347,11 @@ def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out
     mx = C.c_int32()
     rb = 2 * _HIDDEN.get(pool, 0)
     cap = max(int(out_rows_cap), 0)
-    _check(_lib.pack_microbatch(pool, idp, len(ids), _buf(embed_table, max(int(vocab), 0) * rb, "embed_table"), vocab,
-                                _buf(out_emb, cap * rb, "out_emb"), out_rows_cap,
-                                _buf(out_cu_seqlens, 4 * (len(ids) + 1), "out_cu_seqlens"),
-                                _buf(out_position_ids, 4 * cap, "out_position_ids"), C.byref(n_tok), C.byref(mx),
+    dev = _DEVICE.get(pool)
+    _check(_lib.pack_microbatch(pool, idp, len(ids), _buf(embed_table, max(int(vocab), 0) * rb, "embed_table", dev),
+                                vocab, _buf(out_emb, cap * rb, "out_emb", dev), out_rows_cap,
+                                _buf(out_cu_seqlens, 4 * (len(ids) + 1), "out_cu_seqlens", dev),
+                                _buf(out_position_ids, 4 * cap, "out_position_ids", dev), C.byref(n_tok), C.byref(mx),
                                 tier_mask, _stream(stream)), "pack_microbatch")
     return int(n_tok.value), int(mx.value)
 
