@@ -36,7 +36,7 @@
  *  - Calls from several threads are serialised internally by a mutex, so a
  *    producer thread and a consumer thread may share one pool.
  *  - HIP graphs: pack_microbatch may be captured on a capturing stream when
- *    its row table travels in the kernel arguments (at most 64 samples whose
+ *    its row table travels in the kernel arguments (at most 32 samples whose
  *    rows form at most 160 runs, a run being a stretch of one sample's text
  *    rows, or of its image rows with no text row between them) and its
  *    samples' writes are known complete (a pack, plan or

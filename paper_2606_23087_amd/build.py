@@ -14,9 +14,9 @@ HIPCC_FLAGS = [
     "-Wall", "-Wno-unused-result",
     # keep the compiler from emitting packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # the pack kernel's ten leading scalar arguments arrive preloaded in
+    # the pack kernel's eleven leading scalar arguments arrive preloaded in
     # scalar registers (the hardware fills them at wave launch)
-    "-mllvm", "-amdgpu-kernarg-preload-count=10",
+    "-mllvm", "-amdgpu-kernarg-preload-count=11",
 ]
 
 

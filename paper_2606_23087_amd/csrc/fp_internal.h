@@ -45,9 +45,9 @@ constexpr int kSmallChunkRowBytes = 10240;
 constexpr int kPackPerCU = 8;        // k_pack workgroups resident per CU (occupancy 8)
 constexpr int kTail1Vecs = 512;
 constexpr int kTail2Vecs = 256;
-constexpr int kInlineSamples = 64;   // sample lengths passed by value to k_pack
+constexpr int kInlineSamples = 32;   // sample lengths passed by value to k_pack
 constexpr int kInlineRuns = 160;     // runs passed by value to k_pack
-constexpr int kBuckets = 256;        // row buckets of the run index
+constexpr int kBuckets = 64;         // row buckets of the run index
 constexpr int kWaveRows = 16;        // rows per wave resolved with scalar loads in k_pack
 constexpr int kMaxPackSamples = 1024;  // per microbatch (bounds the staged run table)
 constexpr int kMaxPackImages = 1024;
@@ -74,8 +74,10 @@ constexpr int64_t kMaxMetaBytes = 1ll << 33;
 // lengths, runs, bucket index) follows the scalar fields; kernel arguments are
 // captured at launch, so a microbatch of up to kInlineSamples samples and
 // kInlineRuns runs needs no staging copy. A larger one points `staged` at a
-// device copy of the table laid out at the given offsets. bucket[b] is the
-// last run starting at or before row b << bucket_shift.
+// device copy of the table laid out at the given offsets. For each row
+// bucket b, brun[b] is a copy of the run holding row b << bucket_shift and
+// bucket[b] that run's index, so a row of the same run is resolved with one
+// load, and a later row steps on from there.
 struct PackArgs {
   const uint8_t* meta;        // device metadata arena
   const uint64_t* pte;        // device page table, index = (gva - gva_start) / page_bytes
@@ -87,6 +89,7 @@ struct PackArgs {
   int32_t* pos;               // position ids or null
   const uint8_t* staged;      // staged run table, or null = the arrays below
   int32_t off_runs;           // byte offsets of the arrays from the table's start
+  int32_t off_brun;
   int32_t off_bucket;
   int32_t n;                  // samples
   int32_t n_runs;
@@ -107,9 +110,12 @@ struct PackArgs {
   int32_t pb_shift;
   alignas(16) int32_t lens[kInlineSamples];   // sample lengths (rows), in pack order
   alignas(16) PackRun runs[kInlineRuns];
+  alignas(16) PackRun brun[kBuckets];
   uint16_t bucket[kBuckets];
 };
-static_assert(sizeof(PackArgs) <= 4096, "kernel arguments stay within 4 KiB");
+// The pack's kernel arguments, 64 bytes of leading scalars (preloaded into
+// registers) and this struct, stay within 4 KiB.
+static_assert(sizeof(PackArgs) + 64 <= 4096, "kernel arguments stay within 4 KiB");
 
 // Division constants of a pool (host-computed once): for e < 2^31,
 // e / (row_bytes / 16) == (e * div_mul) >> div_shift and

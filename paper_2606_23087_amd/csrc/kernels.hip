@@ -68,7 +68,8 @@ struct PackHead {
   int32_t div_shift;
   int32_t bucket_shift;
   const uint8_t* tb;        // run table: staged copy, or null = the one in PackArgs
-  int32_t off_bucket;       // byte offset of the bucket index in the run table
+  int32_t off_brun;         // byte offsets of the bucket runs and the bucket index in the run table
+  int32_t off_bucket;
   int32_t total;            // vectors of the microbatch
 };
 
@@ -86,20 +87,34 @@ __device__ __forceinline__ PackRun ld_run(const PackRun* rp) {
 
 // Run holding packed row `row`: the bucket of the row names a run starting
 // at or before it; runs that end at or before the row are stepped over.
-template <bool kScalar>
-__device__ __forceinline__ uint32_t bucket_word(const PackHead& h, const uint8_t* tb, int row) {
-  return ld<kScalar, uint32_t>(tb + h.off_bucket + 4 * ((row >> h.bucket_shift) >> 1));
-}
+// The first two loads of a row's lookup, independent of each other: its
+// bucket's run (the run holding the bucket's first row) and the word of the
+// bucket index that holds that run's number.
+struct BucketHit {
+  PackRun r;
+  uint32_t w;
+};
 
 template <bool kScalar>
-__device__ __forceinline__ PackRun run_of(const PackHead& h, const PackArgs& a, const uint8_t* tb, int row,
-                                          uint32_t w, int* s_out = nullptr) {
+__device__ __forceinline__ BucketHit bucket_of(const PackHead& h, const uint8_t* tb, int row) {
   const int b = row >> h.bucket_shift;
-  int s = (int)((b & 1) ? (w >> 16) : (w & 0xffffu));
-  const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
-  PackRun r = ld_run<kScalar>(runs + s);
-  while (r.end <= row) r = ld_run<kScalar>(runs + ++s);
-  if (s_out) *s_out = s;
+  return BucketHit{ld_run<kScalar>(reinterpret_cast<const PackRun*>(tb + h.off_brun) + b),
+                   ld<kScalar, uint32_t>(tb + h.off_bucket + 4 * (b >> 1))};
+}
+
+// Run holding packed row `row`: its bucket's run, or a later one, stepped to
+// from that run's number when the bucket's run ends at or before the row.
+template <bool kScalar>
+__device__ __forceinline__ PackRun run_of(const PackHead& h, const PackArgs& a, const uint8_t* tb, int row,
+                                          const BucketHit& hit, int* s_out = nullptr) {
+  PackRun r = hit.r;
+  if (r.end <= row || s_out) {
+    const int b = row >> h.bucket_shift;
+    int s = (int)((b & 1) ? (hit.w >> 16) : (hit.w & 0xffffu));
+    const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
+    while (r.end <= row) r = ld_run<kScalar>(runs + ++s);
+    if (s_out) *s_out = s;
+  }
   return r;
 }
 
@@ -138,12 +153,12 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
 template <int VPT>
 __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int32_t t1, int32_t t2,
                                                       uint64_t div_mul, int32_t div_shift, int32_t bucket_shift,
-                                                      const uint8_t* staged, int32_t off_bucket, int32_t total,
-                                                      PackArgs a) {
+                                                      const uint8_t* staged, int32_t off_brun, int32_t off_bucket,
+                                                      int32_t total, PackArgs a) {
   constexpr int kChunk = kPackBlock * VPT;       // vectors of a full chunk
   extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
-  const PackHead h{g0, g1, t1, t2, div_mul, div_shift, bucket_shift, staged, off_bucket, total};
+  const PackHead h{g0, g1, t1, t2, div_mul, div_shift, bucket_shift, staged, off_brun, off_bucket, total};
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const uint8_t* tb = h.tb ? h.tb : reinterpret_cast<const uint8_t*>(a.lens);
@@ -169,8 +184,8 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   // together with it (the compiler would otherwise split the batch and load
   // it first).
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t w0 = bucket_word<true>(h, tb, r0 + min(wave, max(rows - 1, 0)));
-  asm volatile("" : : "s"(w0), "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start),
+  const BucketHit w0 = bucket_of<true>(h, tb, r0 + min(wave, max(rows - 1, 0)));
+  asm volatile("" : : "s"(w0.w), "s"(w0.r.end), "s"(w0.r.head), "s"(w0.r.vdelta), "s"(w0.r.word), "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start),
                "s"(a.pt_mul), "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
                "s"(a.tier_mask), "s"(a.row_bytes));
   const bool write_meta = (a.tier_mask & 1) != 0;
@@ -181,7 +196,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
     // chains of different rows overlap.
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
-      const uint32_t w = t == wave ? w0 : bucket_word<true>(h, tb, row);
+      const BucketHit w = t == wave ? w0 : bucket_of<true>(h, tb, row);
       const uint64_t src = row_source<true>(a, run_of<true>(h, a, tb, row, w), row);
       if (lane == 0) {
         s_src[t] = src;
@@ -191,7 +206,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   } else {
     for (int t = tid; t < rows; t += kPackBlock) {
       const int row = r0 + t;
-      const uint64_t src = row_source<false>(a, run_of<false>(h, a, tb, row, bucket_word<false>(h, tb, row)), row);
+      const uint64_t src = row_source<false>(a, run_of<false>(h, a, tb, row, bucket_of<false>(h, tb, row)), row);
       s_src[t] = src;
       if (!src) my_skip = 1;
     }
@@ -268,7 +283,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
         const int first = blk * 64, row = first + lane;
         const int last = min(first + 63, a.n_tokens - 1);
         int s;
-        PackRun r = run_of<true>(h, a, tb, first, bucket_word<true>(h, tb, first), &s);
+        PackRun r = run_of<true>(h, a, tb, first, bucket_of<true>(h, tb, first), &s);
         int start = r.head & 0x7fffffff;
         while (r.end <= last) {
           const int next = r.end;
@@ -384,10 +399,11 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
   const int32_t total = (int32_t)vecs;               // the host keeps this below 2^31
   if (a.vpt == 2)
     hipLaunchKernelGGL(k_pack<2>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1, a.t1, a.t2,
-                       a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_bucket, total, a);
+                       a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_brun, a.off_bucket, total, a);
   else
     hipLaunchKernelGGL(k_pack<kVecsPerThread>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1,
-                       a.t1, a.t2, a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_bucket, total, a);
+                       a.t1, a.t2, a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_brun, a.off_bucket, total,
+                       a);
   return hipGetLastError();
 }
 

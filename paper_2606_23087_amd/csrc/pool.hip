@@ -1399,10 +1399,12 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
     while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
     const int32_t n_buckets = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
     std::vector<uint16_t> bucket((size_t)(n_buckets + (n_buckets & 1)), 0);
+    std::vector<fp::PackRun> brun((size_t)n_buckets);
     for (int32_t b = 0, sidx = 0; b < n_buckets; ++b) {
       const int64_t first = (int64_t)b << shift;
       while (sidx + 1 < n_runs && run_start[(size_t)sidx + 1] <= first) ++sidx;
       bucket[(size_t)b] = (uint16_t)sidx;
+      brun[(size_t)b] = runs[(size_t)sidx];
     }
     a.n_runs = n_runs;
     a.bucket_shift = shift;
@@ -1424,21 +1426,26 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
       if (n) std::memcpy(a.lens, lens.data(), 4 * lens.size());
       if (n_runs) std::memcpy(a.runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
       if (n_buckets) std::memcpy(a.bucket, bucket.data(), 2 * (size_t)n_buckets);
+      if (n_buckets) std::memcpy(a.brun, brun.data(), sizeof(fp::PackRun) * (size_t)n_buckets);
       a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
+      a.off_brun = (int32_t)(offsetof(fp::PackArgs, brun) - offsetof(fp::PackArgs, lens));
       a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
     } else {
       const size_t o_runs = (4 * lens.size() + 15) & ~(size_t)15;
-      const size_t o_b = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
+      const size_t o_br = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
+      const size_t o_b = o_br + sizeof(fp::PackRun) * brun.size();
       const size_t bytes = o_b + 2 * bucket.size();
       fp_status st = stage_acquire(p, bytes, bytes, &s);
       if (st != FP_OK) return st;
       std::memset(s->host, 0, bytes);
       if (n) std::memcpy(s->host, lens.data(), 4 * lens.size());
       if (n_runs) std::memcpy(s->host + o_runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
+      if (!brun.empty()) std::memcpy(s->host + o_br, brun.data(), sizeof(fp::PackRun) * brun.size());
       if (!bucket.empty()) std::memcpy(s->host + o_b, bucket.data(), 2 * bucket.size());
       FP_HIP(hipMemcpyAsync(s->dev, s->host, bytes, hipMemcpyHostToDevice, hs));
       a.staged = s->dev;
       a.off_runs = (int32_t)o_runs;
+      a.off_brun = (int32_t)o_br;
       a.off_bucket = (int32_t)o_b;
     }
     {

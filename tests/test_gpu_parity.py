@@ -328,10 +328,10 @@ def _head_specs(rng, n, max_img, vocab):
 def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
     """Row resolution at every chunk shape: many rows per chunk (small H,
     one row per lane) down to chunks inside one row (large H); page sizes
-    that are not powers of two; 17..64 samples with an inline run table,
+    that are not powers of two; 17..32 samples with an inline run table,
     samples with eleven images, empty images and adjacent images (merged
-    runs), the 64-sample and 160-run limits of the inline table and
-    microbatches just past them (staged table). pack_cus=1 sizes the chunk
+    runs), the 32-sample and 160-run limits of the inline table and
+    microbatches just past them (staged table), and 64 or more samples. pack_cus=1 sizes the chunk
     geometry for one compute unit, so these small packs also take full
     chunks and both shrinking tail stages; with the device's count they are
     all in the last stage."""
@@ -354,9 +354,10 @@ def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
         cu = torch.full((150,), -1, dtype=torch.int32, device="cuda")
         runs = np.cumsum([_runs(s) for s in specs])
         r160 = int(np.searchsorted(runs, 160, side="right"))     # first r160 samples form <= 160 runs
-        assert runs[r160 - 1] <= 160 < runs[r160] and r160 < 64
+        assert runs[r160 - 1] <= 160 < runs[r160] and r160 < 32
+        assert runs[101] - runs[69] <= 160                         # samples 70..101 fit the inline table
         groups = [list(range(17)), list(range(r160)), list(range(r160 + 1)),
-                  list(range(70, 134)), list(range(70, 135)), list(range(70)),
+                  list(range(70, 102)), list(range(70, 103)), list(range(70, 134)), list(range(70)),
                   [11, 23, 11, 35, 140 - 1]]
         for g in groups:
             say(f"  group of {len(g)} samples, {sum(_runs(specs[i]) for i in g)} runs")

@@ -7,9 +7,9 @@
   so it does not insert them).
 - The pack kernels spill nothing to scratch and stay within the registers
   that keep 8 waves per SIMD resident.
-- The pack kernels' leading scalar arguments (12 dwords) arrive preloaded in
-  scalar registers, and the first load of the row lookup (the bucket entry)
-  is issued before the wait for the other kernel arguments, so the two are in
+- The pack kernels' leading scalar arguments (13 dwords) arrive preloaded in
+  scalar registers, and the first loads of the row lookup (the bucket's run and
+  index entry) are issued before the wait for the other kernel arguments, so the two are in
   flight together.
 """
 
@@ -78,7 +78,7 @@ def test_pack_kernels_preload_their_head_arguments(isa):
     packs = {k: v for k, v in _kernels(isa).items() if "k_pack" in k}
     assert len(packs) == 2
     for name, (lines, meta) in packs.items():
-        assert re.search(r"\.amdhsa_user_sgpr_kernarg_preload_length 12\b", meta), name
+        assert re.search(r"\.amdhsa_user_sgpr_kernarg_preload_length 13\b", meta), name
         # Entry with preloaded arguments: 256 bytes past the kernel symbol,
         # after the compatibility prologue that loads them for firmware that
         # does not preload. There, the first scalar load that is not a
