@@ -58,9 +58,9 @@ __device__ __forceinline__ T ld(const void* p) {
 }
 
 // The pack's leading kernel arguments: everything a wave needs to address its
-// row's bucket entry. They are separate scalar arguments, ahead of PackArgs,
+// row's bucket run and bucket-index entry. They are separate scalar arguments, ahead of PackArgs,
 // so that the hardware preloads them into scalar registers at wave launch
-// (kernarg preloading); the first load of the row lookup then leaves at once,
+// (kernarg preloading); the first loads of the row lookup then leave at once,
 // alongside the kernel-argument loads of the rest.
 struct PackHead {
   int32_t g0, g1, t1, t2;   // chunk geometry (as in PackArgs)
@@ -85,8 +85,6 @@ __device__ __forceinline__ PackRun ld_run(const PackRun* rp) {
   return PackRun{(int32_t)d.x, (int32_t)d.y, (int32_t)d.z, (int32_t)d.w};
 }
 
-// Run holding packed row `row`: the bucket of the row names a run starting
-// at or before it; runs that end at or before the row are stepped over.
 // The first two loads of a row's lookup, independent of each other: its
 // bucket's run (the run holding the bucket's first row) and the word of the
 // bucket index that holds that run's number.
@@ -178,15 +176,15 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   }
   const int r0 = div_vpr(h, v0);
   const int rows = v1 > v0 ? div_vpr(h, v1 - 1) - r0 + 1 : 0;
-  // The bucket entry of the wave's first row (a row of the chunk; row 0 of an
-  // empty pack, whose inline index always has an entry), then the other kernel
+  // The bucket run and index entry of the wave's first row (a row of the
+  // chunk; row 0 of an empty pack, whose inline table always has them), then the other kernel
   // arguments the row resolution uses in one batch of scalar loads, in flight
   // together with it (the compiler would otherwise split the batch and load
   // it first).
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const BucketHit w0 = bucket_of<true>(h, tb, r0 + min(wave, max(rows - 1, 0)));
-  asm volatile("" : : "s"(w0.w), "s"(w0.r.end), "s"(w0.r.head), "s"(w0.r.vdelta), "s"(w0.r.word), "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start),
-               "s"(a.pt_mul), "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
+  asm volatile("" : : "s"(w0.w), "s"(w0.r.end), "s"(w0.r.head), "s"(w0.r.vdelta), "s"(w0.r.word),
+               "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start), "s"(a.pt_mul), "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
                "s"(a.tier_mask), "s"(a.row_bytes));
   const bool write_meta = (a.tier_mask & 1) != 0;
   const int vpr = a.row_bytes >> 4;
