@@ -193,3 +193,82 @@ def test_producer_and_consumer_threads(fp):
         t.join()
         torch.cuda.synchronize()
         fp.pool_destroy(pool)
+
+
+def test_two_producers_and_a_planning_consumer(fp):
+    """Two producer threads, each on its own stream, write and free samples
+    while the consumer plans (zig-zag policy) and packs resident samples on a
+    third stream: the pool's lock serialises the calls and its events order
+    the streams. Every pack is checked after all threads finish, and all
+    pages come back at the end."""
+    say("case two producers, planning consumer")
+    rng = np.random.default_rng(4)
+    table = tagged_table(VOCAB, H, 4)
+    t_dev = to_dev(table)
+    pool = _pool(fp, 400)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    lock = threading.Lock()
+    resident = {}            # id -> (spec, host rows, device rows)
+    done = [threading.Event(), threading.Event()]
+    errors = []
+
+    def producer(k):
+        prng = np.random.default_rng(40 + k)
+        st = streams[k]
+        try:
+            for i in range(100):
+                s = _spec(prng, VOCAB, int(prng.integers(1, 40)),
+                          [int(x) for x in prng.integers(0, 3 * P, size=int(prng.integers(0, 3)))])
+                v = tagged_vis(1000 * k + i, s.n_vis, H, 4)
+                with torch.cuda.stream(st):
+                    d = to_dev(v) if s.n_vis else None
+                    sid = fp.pool_write_sample(pool, s.text_ids, s.img_pos, s.img_ntok, d, stream=st)
+                with lock:
+                    resident[sid] = (s, v, d, k)
+                    mine = sorted(x for x, r in resident.items() if r[3] == k)
+                    if len(mine) > 8:
+                        fp.pool_free_sample(pool, mine[0])
+                        resident.pop(mine[0])
+        except Exception as e:  # surfaced by the main thread
+            errors.append(e)
+        finally:
+            done[k].set()
+
+    threads = [threading.Thread(target=producer, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    packs = []
+    try:
+        while not all(d.is_set() for d in done) or len(packs) < 20:
+            with lock:
+                ids = sorted(resident)
+                if len(ids) < 2:
+                    continue
+                plan = fp.plan_microbatches(pool, ids, 200, 2, 64, stream=streams[2], policy=fp.FP_PLAN_ZIGZAG)
+                pick = [ids[i] for i in range(len(ids)) if plan["assign"][i] == 0][:6]
+                if not pick:
+                    continue
+                items = [resident[i][:2] for i in pick]
+                n = sum(sp.length for sp, _ in items)
+                out = torch.empty((n, H), dtype=torch.int16, device="cuda")
+                fp.pack_microbatch(pool, pick, t_dev, VOCAB, out, n, stream=streams[2])
+            packs.append((items, out))
+            if len(packs) >= 300:
+                break
+        for t in threads:
+            t.join()
+        torch.cuda.synchronize()
+        assert not errors, errors
+        say(f"  {len(packs)} packs checked")
+        for items, out in packs:
+            want = definitional_pack([sp for sp, _ in items], [v for _, v in items], table)
+            assert np.array_equal(to_host(out), want[0])
+        for sid in list(resident):
+            fp.pool_free_sample(pool, sid)
+        torch.cuda.synchronize()
+        assert fp.pool_reclaim(pool, True) == 0 and fp.pool_stats(pool)["n_samples"] == 0
+    finally:
+        for t in threads:
+            t.join()
+        torch.cuda.synchronize()
+        fp.pool_destroy(pool)
