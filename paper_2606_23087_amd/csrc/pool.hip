@@ -57,6 +57,9 @@ constexpr int64_t kDefaultMetaBytes = 64ll << 20;
 constexpr int64_t kDefaultChunkBytes = 1ll << 30;
 constexpr int64_t kMaxSampleRows = 1 << 24;
 constexpr int32_t kMaxPlanMicrobatches = 1 << 20;
+// A tail chunk must fit the smallest full chunk (2 vectors per thread): the
+// pack kernel's threads cover at most that many vectors of a chunk.
+static_assert(fp::kTail2Vecs <= fp::kTail1Vecs && fp::kTail1Vecs <= 2 * fp::kPackBlock, "tail chunk sizes");
 // 16-byte vectors one pack or one write may move. The kernels index vectors
 // with 32-bit integers, and a thread forms the indices of its vectors (up to
 // 767 past its chunk's start) before testing them against the chunk's end,
