@@ -18,7 +18,8 @@ Plain, slow, obviously correct Python + numpy:
   allocators, producer write / free, and a consumer pack that resolves every
   visual row through the page table.
 - ``oracle.plan``   the per-sample cost l + l^2/K, the per-microbatch cost of
-  Eq. 3, the greedy balanced partition, and brute-force optimal partitions.
+  Eq. 3, the greedy balanced partition, the zig-zag partition, and
+  brute-force optimal partitions.
 - ``oracle.allocate`` the heterogeneous parallel allocator of Eq. 1-2:
   pruned candidate configurations and the lexmax (G, -F) flow matching,
   solved by enumerating every combination.
