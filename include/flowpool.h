@@ -354,7 +354,10 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
  *                    and writes cu_seqlens/position ids; FP_TIER_MASK_HOST
  *                    copies rows on host-tier pages; FP_TIER_MASK_ALL both.
  *                    Two launches with the two masks write what one ALL does.
- * Asynchronous on `stream`. Duplicated ids are packed twice.
+ * Asynchronous on `stream`. Duplicated ids are packed twice. The row table
+ * travels in the kernel arguments for up to 32 samples and 160 runs; a larger
+ * microbatch's table is first copied to the device on `stream` from one of
+ * the pool's pinned staging buffers.
  * Errors: EINVAL (also more than 1024 samples or images, or a microbatch of
  * more than 2^31 - 1024 16-byte vectors, i.e. n_tokens * 2H / 16), ENOENT,
  * ECAPACITY (sum of l > out_rows_cap), EALIGN, EHIP. */
