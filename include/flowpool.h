@@ -270,12 +270,19 @@ fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, in
 /* Heterogeneous parallel allocator, first step (Sec. 3.3): the pruned
  * parallelism configurations of one module. Encoders (backbone = 0) use data
  * and tensor parallelism, DP x TP devices; the backbone (backbone != 0) also
- * pipeline parallelism, DP x TP x PP devices. Kept: DP divides global_batch,
- * TP divides per_node (no tensor parallelism across nodes), PP divides
- * layers (backbone only; PP = 1 for encoders), DP*TP*PP <= devices. Listed in
- * increasing (DP, TP, PP) order into host int32 out_dp/out_tp/out_pp[cap]
- * (any may be NULL); *out_n (host) receives the count even when it exceeds
- * cap (then EINVAL). Host only. Errors: EINVAL. */
+ * pipeline parallelism, DP x TP x PP devices. The section prunes
+ * configurations whose DP does not divide the global batch, whose TP/PP
+ * degrees do not factorize the module's resource budget, or whose tensor
+ * parallelism crosses nodes; kept here:
+ *  - DP divides global_batch;
+ *  - DP*TP*PP <= devices (the module's budget, which its degrees factorize,
+ *    fits the cluster); for the backbone with layers > 0, PP also divides
+ *    layers (pipeline stages of equal depth); layers = 0 drops that rule;
+ *    PP = 1 for encoders;
+ *  - TP divides per_node (TP groups on consecutive devices stay in one node).
+ * Listed in increasing (DP, TP, PP) order into host int32
+ * out_dp/out_tp/out_pp[cap] (any may be NULL); *out_n (host) receives the
+ * count even when it exceeds cap (then EINVAL). Host only. Errors: EINVAL. */
 fp_status alloc_candidates(int32_t backbone, int32_t devices, int32_t per_node, int32_t global_batch,
                            int32_t layers, int32_t* out_dp, int32_t* out_tp, int32_t* out_pp,
                            int32_t cap, int32_t* out_n);

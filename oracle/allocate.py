@@ -8,15 +8,25 @@ the throughput and r_i(c) the device count of configuration c of module i:
     lexmax (G, -F)  with  G = min(T_enc, T_bb),  F = |T_enc - T_bb|,
     one configuration per module, sum of r_i(c_i) <= R                    (Eq. 2)
 
-First the candidate configurations are pruned: encoders use data and tensor
-parallelism (DP x TP devices), the backbone also pipeline parallelism
-(DP x TP x PP devices); DP must divide the global batch, TP must divide the
-devices of one node (no tensor parallelism across nodes) and PP must divide
-the backbone's layers.
+First the candidate configurations are pruned (Sec. 3.3, first step):
+encoders use data and tensor parallelism (DP x TP devices), the backbone also
+pipeline parallelism (DP x TP x PP devices). The paper prunes three kinds of
+configuration; each is read here as one rule:
+- the global batch is not divisible by DP: kept iff DP divides it;
+- TP/PP degrees that do not factorize the per-module resource budget: a
+  module's budget is the device count of its configuration, which the three
+  degrees factorize by construction, so the rule bounds that count by the
+  cluster's devices (DP x TP x PP <= devices); where the caller gives the
+  backbone's layer count (layers > 0), PP must also divide it, so that every
+  pipeline stage holds the same number of layers (a low-efficiency pruning
+  the paper does not spell out; layers = 0 leaves it out);
+- cross-node tensor parallelism: TP must divide the devices of one node, the
+  condition under which TP groups laid over consecutive devices from any
+  multiple of TP never straddle a node boundary.
 
 Here the problem is solved by enumerating every combination (the paper
 solves the same problem as a MILP). Readings where the paper leaves a
-detail open (listed with the others in the design notes):
+detail open:
 - throughputs and device counts are integers, so G and F are exact;
 - among combinations with the best (G, F), fewer devices win, then the
   lexicographically smallest choice vector (encoders in order, then the
@@ -35,11 +45,18 @@ def divisors(n: int) -> List[int]:
 
 
 def candidates(backbone: bool, devices: int, per_node: int, global_batch: int, layers: int):
-    """Pruned (DP, TP, PP) configurations of one module, in increasing order."""
+    """Pruned (DP, TP, PP) configurations of one module, in increasing order.
+    layers = 0: no layer rule for the backbone's PP."""
     out = []
+    if not backbone:
+        pps = [1]
+    elif layers:
+        pps = divisors(layers)
+    else:
+        pps = list(range(1, devices + 1))
     for dp in divisors(global_batch):
         for tp in divisors(per_node):
-            for pp in (divisors(layers) if backbone else [1]):
+            for pp in pps:
                 if dp * tp * pp <= devices:
                     out.append((dp, tp, pp))
     return sorted(out)

@@ -1,9 +1,11 @@
 // Heterogeneous parallel allocator of the paper (Sec. 3.3, Eq. 1-2), host side.
 //
-// Candidate pruning: encoders run DP x TP, the backbone DP x TP x PP; DP
-// divides the global batch, TP divides the devices of a node (no tensor
-// parallelism across nodes), PP divides the backbone's layers, and a
-// configuration fits the device budget.
+// Candidate pruning: encoders run DP x TP, the backbone DP x TP x PP. The
+// paper's three pruning conditions become: DP divides the global batch; the
+// configuration's device count DP x TP x PP (its module budget) fits the
+// cluster, and PP divides the backbone's layers when a layer count is given
+// (layers = 0: no layer rule); TP divides the devices of a node, so TP groups
+// on consecutive devices never straddle two nodes.
 //
 // Flow matching: one configuration per module, total devices <= R,
 // lexmax (G, -F) with G = min(T_enc, T_bb) and F = |T_enc - T_bb|. For a
@@ -68,13 +70,17 @@ class MinTree {
 std::vector<Config> prune_candidates(bool backbone, int32_t devices, int32_t per_node, int32_t global_batch,
                                      int32_t layers) {
   std::vector<Config> out;
+  // PP ranges over the divisors of the layer count, or (layers = 0) over
+  // every degree the device budget allows; encoders have PP = 1.
+  const int32_t pp_max = !backbone ? 1 : (layers > 0 ? layers : devices);
   for (int32_t dp = 1; dp <= global_batch; ++dp) {
     if (global_batch % dp) continue;
     for (int32_t tp = 1; tp <= per_node; ++tp) {
       if (per_node % tp) continue;
-      for (int32_t pp = 1; pp <= (backbone ? layers : 1); ++pp) {
-        if (layers % pp && backbone) continue;
-        if ((int64_t)dp * tp * pp <= devices) out.push_back(Config{dp, tp, pp});
+      for (int32_t pp = 1; pp <= pp_max; ++pp) {
+        if (layers > 0 && layers % pp) continue;
+        if ((int64_t)dp * tp * pp > devices) break;   // larger pp only grows the product
+        out.push_back(Config{dp, tp, pp});
       }
     }
   }

@@ -1197,7 +1197,7 @@ fp_status alloc_candidates(int32_t backbone, int32_t devices, int32_t per_node, 
                            int32_t layers, int32_t* out_dp, int32_t* out_tp, int32_t* out_pp, int32_t cap,
                            int32_t* out_n) {
   return guarded([&]() -> fp_status {
-    if (devices < 1 || per_node < 1 || global_batch < 1 || layers < 1 || devices > (1 << 20) ||
+    if (devices < 1 || per_node < 1 || global_batch < 1 || layers < 0 || devices > (1 << 20) ||
         per_node > 4096 || global_batch > (1 << 24) || layers > 65536)
       return fail(FP_EINVAL, "devices %d, per_node %d, global_batch %d, layers %d", devices, per_node,
                   global_batch, layers);

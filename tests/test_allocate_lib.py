@@ -15,7 +15,8 @@ from paper_2606_23087_amd.workloads import allocator_tables
 fp = pytest.importorskip("paper_2606_23087_amd.flowpool")
 
 
-@pytest.mark.parametrize("cluster", [(8, 4, 8, 4), (24, 8, 48, 12), (64, 8, 256, 28), (3, 2, 5, 7)])
+@pytest.mark.parametrize("cluster", [(8, 4, 8, 4), (24, 8, 48, 12), (64, 8, 256, 28), (3, 2, 5, 7),
+                                     (8, 4, 4, 0), (64, 8, 512, 0), (6, 4, 6, 0)])
 def test_candidates_match(cluster):
     for bb in (False, True):
         assert fp.alloc_candidates(bb, *cluster) == candidates(bb, *cluster)
@@ -56,3 +57,5 @@ def test_errors():
         fp.plan_allocation([[(1, 1)], []], 5)
     with pytest.raises(fp.FlowPoolError, match="EINVAL"):
         fp.alloc_candidates(True, 0, 8, 8, 8)
+    with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+        fp.alloc_candidates(True, 8, 8, 8, -1)

@@ -5,8 +5,12 @@
 - closed form: with an unlimited budget, G = min(best encoder sum, best
   backbone throughput), and F follows from the closest encoder sum;
 - monotonicity: a larger budget never lowers G;
-- the candidate rules hold for every listed configuration and no valid one
-  is missing.
+- the candidate rules, checked by simulating what each prunes (an even
+  batch split, TP groups inside one node, equal pipeline stages, the device
+  budget) over every configuration in range, plus hand-worked lists that tell
+  the rules apart (a TP degree that fits a node without dividing it, a PP
+  degree that fits the budget without dividing the layers, a budget below the
+  product of the largest degrees).
 """
 
 import itertools
@@ -78,15 +82,50 @@ def test_budget_monotone():
         last = g
 
 
+def _batch_splits_evenly(batch, dp):
+    """Deal the global batch's samples to dp replicas round-robin; equal shares?"""
+    share = [0] * dp
+    for i in range(batch):
+        share[i % dp] += 1
+    return len(set(share)) == 1
+
+
+def _tp_groups_stay_in_nodes(tp, per_node, span):
+    """TP groups of tp consecutive devices, laid from every multiple of tp
+    below ``span``: does any group hold devices of two nodes?"""
+    for start in range(0, span, tp):
+        if len({d // per_node for d in range(start, start + tp)}) > 1:
+            return False
+    return True
+
+
+def _stages_equal(layers, pp):
+    """Cut the layers into pp contiguous stages, as evenly as possible; equal?"""
+    cuts = [round(k * layers / pp) for k in range(pp + 1)]
+    return len({b - a for a, b in zip(cuts, cuts[1:])}) == 1
+
+
 @pytest.mark.parametrize("backbone", [False, True])
-def test_candidate_rules(backbone):
-    devices, per_node, batch, layers = 24, 8, 48, 12
+@pytest.mark.parametrize("cluster", [(24, 8, 48, 12), (12, 6, 30, 10), (16, 4, 16, 0), (5, 8, 12, 7)])
+def test_candidate_rules_by_simulation(backbone, cluster):
+    """Each kept configuration splits the batch evenly, keeps every TP group
+    inside one node, cuts the layers into equal stages (if a layer count is
+    given) and fits the devices; every configuration in range that is left
+    out breaks one of these, checked by simulating the split, the placement
+    and the stage cut rather than by the divisibility formulas."""
+    devices, per_node, batch, layers = cluster
     got = candidates(backbone, devices, per_node, batch, layers)
-    for dp, tp, pp in got:
-        assert batch % dp == 0 and per_node % tp == 0 and layers % pp == 0 and dp * tp * pp <= devices
-        assert backbone or pp == 1
-    every = [(dp, tp, pp) for dp in range(1, 49) for tp in range(1, 9) for pp in range(1, 13)
-             if batch % dp == 0 and per_node % tp == 0 and layers % pp == 0 and dp * tp * pp <= devices
-             and (backbone or pp == 1)]
-    assert got == sorted(every)
+    assert got == sorted(set(got))
+    span = 2 * per_node * per_node     # every TP alignment against the node size repeats within this span
+    ok = set()
+    for dp in range(1, batch + 1):
+        for tp in range(1, per_node + 1):
+            for pp in range(1, (devices if backbone else 1) + 1):
+                if (dp * tp * pp <= devices and _batch_splits_evenly(batch, dp)
+                        and _tp_groups_stay_in_nodes(tp, per_node, span)
+                        and (not backbone or not layers or (pp <= layers and _stages_equal(layers, pp)))):
+                    ok.add((dp, tp, pp))
+    assert set(got) == ok
+    # a TP degree above the node size always straddles nodes
+    assert not _tp_groups_stay_in_nodes(per_node + 1, per_node, span)
     assert divisors(12) == [1, 2, 3, 4, 6, 12]
