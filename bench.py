@@ -375,6 +375,8 @@ def concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
     th.join()
     torch.cuda.synchronize()
     del graph
+    for mb in mbs:                          # the graph is gone: its packs no longer hold their samples
+        fp.pool_release_captured(w.pool, mb)
     alone = mb_bytes * passes / t_alone / 1e9
     busy = mb_bytes * passes / t_busy / 1e9
     prod = (b1 - b0) / wall / 1e9
@@ -689,6 +691,8 @@ def main() -> int:
             g1.record(pack_stream)
             torch.cuda.synchronize()
             del g
+            for mb in mbs:
+                fp.pool_release_captured(w.pool, mb)
             return g0.elapsed_time(g1) * 1e-3 / args.steps
 
         graph_s = replay_s(1)

@@ -39,13 +39,15 @@
  *    its row table travels in the kernel arguments (at most 32 samples whose
  *    rows form at most 160 runs, a run being a stretch of one sample's text
  *    rows, or of its image rows with no text row between them) and its
- *    samples' writes are known complete (a pack, plan or
- *    pool_reclaim after they finished has seen them; the capture makes no
- *    event queries); each replay packs the same samples into the same
- *    buffers. The samples must stay resident
- *    while the graph may be replayed. pool_write_sample, pool_migrate and
- *    plan_microbatches return ESTATE on a capturing stream, as does a pack
- *    that cannot be captured.
+ *    samples' writes are known complete (a pack, plan or pool_reclaim after they finished has seen
+ *    them; the capture makes no event queries); each replay packs the same
+ *    samples into the same buffers, through the page lists they had at
+ *    capture. A captured pack therefore holds its samples: pool_free_sample
+ *    and pool_migrate return ESTATE for them until the caller, once the
+ *    graph will not be replayed again, hands the same sample id list to
+ *    pool_release_captured (once per captured pack). pool_write_sample,
+ *    pool_migrate and plan_microbatches return ESTATE on a capturing stream,
+ *    as does a pack that cannot be captured.
  */
 #ifndef FLOWPOOL_H
 #define FLOWPOOL_H
@@ -56,7 +58,7 @@
 extern "C" {
 #endif
 
-#define FP_ABI_VERSION 4
+#define FP_ABI_VERSION 5
 
 typedef struct fp_pool fp_pool;   /* opaque; created and owned by the library */
 typedef int32_t fp_status;
@@ -187,14 +189,17 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
                             const void* vis_emb, const uint8_t* page_tier_wish,
                             void* stream, uint64_t* out_sample_id);
 
-/* Release a sample; its id becomes invalid at once. Its pages, metadata and
- * slot return to the free lists as soon as the work enqueued before this call
- * on every stream that packed the sample has completed: at once if those
- * streams are idle, otherwise later (an event recorded on each busy one;
- * event-deferred reclamation, checked by the next write or by pool_reclaim).
- * If the sample's own write has not finished, the call waits for it. Pages
- * freed while no pack is pending return in free order.
- * Errors: ENOENT, EHIP. */
+/* Release a sample; its id becomes invalid at once. The paper's pool
+ * (Sec. 3.2) describes writing and consuming samples but defines no release;
+ * this is the library's, so that the pool can be reused over a run. Its
+ * pages, metadata and slot return to the free lists as soon as the work
+ * enqueued before this call on every stream that packed the sample has
+ * completed: at once if those streams are idle, otherwise later (an event
+ * recorded on each busy one; event-deferred reclamation, checked by the next
+ * write or by pool_reclaim). If the sample's own write has not finished, the
+ * call waits for it. Pages freed while no pack is pending return in free
+ * order.
+ * Errors: ENOENT, ESTATE (a captured pack still holds the sample), EHIP. */
 fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
 
 /* Returns the resources of deferred frees whose packs have completed (with
@@ -220,7 +225,8 @@ fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages);
  * samples to the host tier. SCATTER pools only; a sample may be listed once.
  * All-or-nothing. *out_pages_moved (host, may be NULL) receives the number of
  * pages moved. Errors: EINVAL, ENOENT, ENOMEM (not enough free pages in
- * `tier`, or metadata arena full), EHIP. */
+ * `tier`, or metadata arena full), ESTATE (a captured pack holds a listed
+ * sample, or `stream` is capturing), EHIP. */
 fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t tier,
                        void* stream, int64_t* out_pages_moved);
 
@@ -374,6 +380,14 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n,
                           int32_t* out_cu_seqlens, int32_t* out_position_ids,
                           int32_t* out_n_tokens, int32_t* out_max_seqlen,
                           int32_t tier_mask, void* stream);
+
+/* Ends the hold that captured packs have on their samples (see HIP graphs
+ * above): call it with a captured pack's sample id list (host uint64[n], in
+ * any order; an id listed twice releases two captures of it) once no graph
+ * holding that pack will be replayed again. Afterwards the samples may be
+ * freed or migrated. All-or-nothing. Errors: ENOENT, EINVAL (an id holds
+ * fewer captured packs than listed). */
+fp_status pool_release_captured(fp_pool* p, const uint64_t* sample_ids, int32_t n);
 
 /* Introspection (tests, benchmarks); host outputs, any may be NULL. */
 fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages,

@@ -70,42 +70,33 @@ static_assert(sizeof(PackRun) == 16, "PackRun layout");
 constexpr int32_t kTextRun = INT32_MIN;
 constexpr int64_t kMaxMetaBytes = 1ll << 33;
 
-// Everything one pack launch needs, passed by value. The run table (sample
-// lengths, runs, bucket index) follows the scalar fields; kernel arguments are
-// captured at launch, so a microbatch of up to kInlineSamples samples and
-// kInlineRuns runs needs no staging copy. A larger one points `staged` at a
-// device copy of the table laid out at the given offsets. For each row
-// bucket b, brun[b] is a copy of the run holding row b << bucket_shift and
-// bucket[b] that run's index, so a row of the same run is resolved with one
-// load, and a later row steps on from there.
+// What the pack kernel reads, passed by value. The run table (sample
+// lengths, runs, bucket index) follows the scalar fields; kernel arguments
+// are captured at launch, so a microbatch of up to kInlineSamples samples and
+// kInlineRuns runs needs no staging copy. A larger one is copied to device
+// memory first, laid out at the given byte offsets. For each row bucket b,
+// brun[b] is a copy of the run holding row b << bucket_shift and bucket[b]
+// that run's index, so a row of the same run is resolved with one load, and a
+// later row steps on from there.
 struct PackArgs {
   const uint8_t* meta;        // device metadata arena
   const uint64_t* pte;        // device page table, index = (gva - gva_start) / page_bytes
   uint64_t gva_start;
-  uint64_t page_bytes;
   const uint8_t* table;       // embedding table (may be null when no text row is copied)
   uint8_t* out;               // packed rows
   int32_t* cu;                // cu_seqlens or null
   int32_t* pos;               // position ids or null
-  const uint8_t* staged;      // staged run table, or null = the arrays below
-  int32_t off_runs;           // byte offsets of the arrays from the table's start
-  int32_t off_brun;
+  int32_t off_runs;           // byte offsets from the table's start: the runs,
+  int32_t off_brun;           // the bucket runs and the bucket index
   int32_t off_bucket;
+  int32_t bucket_shift;       // buckets hold 2^bucket_shift rows
   int32_t n;                  // samples
-  int32_t n_runs;
   int32_t n_tokens;           // total rows
   int32_t row_bytes;
   int32_t page_tokens;
   int32_t tier_mask;
-  int32_t max_chunk_rows;     // rows one chunk can touch
-  int32_t g0, g1;             // workgroups [0, g0): full chunks; [g0, g1): kTail1Vecs; then kTail2Vecs
-  int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * full chunk)
-  int32_t vpt;                // vectors per thread of a full chunk (2 or kVecsPerThread)
-  int32_t bucket_shift;
-  uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
   uint64_t pt_mul;            // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
   uint64_t pb_mul;            // d / page_bytes == umulhi64(d, pb_mul) >> pb_shift for d < 2^52
-  int32_t div_shift;
   int32_t pt_shift;
   int32_t pb_shift;
   alignas(16) int32_t lens[kInlineSamples];   // sample lengths (rows), in pack order
@@ -116,6 +107,18 @@ struct PackArgs {
 // The pack's kernel arguments, 64 bytes of leading scalars (preloaded into
 // registers) and this struct, stay within 4 KiB.
 static_assert(sizeof(PackArgs) + 64 <= 4096, "kernel arguments stay within 4 KiB");
+
+// A pack launch: the kernel's arguments and, host side, its geometry.
+struct PackPlan {
+  PackArgs a;
+  const uint8_t* staged;      // staged run table, or null = the arrays in `a`
+  int32_t max_chunk_rows;     // rows one chunk can touch
+  int32_t g0, g1;             // workgroups [0, g0): full chunks; [g0, g1): kTail1Vecs; then kTail2Vecs
+  int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * full chunk)
+  int32_t vpt;                // vectors per thread of a full chunk (2 or kVecsPerThread)
+  uint64_t div_mul;           // e / (row_bytes/16) == (e * div_mul) >> div_shift for e < 2^31
+  int32_t div_shift;
+};
 
 // Division constants of a pool (host-computed once): for e < 2^31,
 // e / (row_bytes / 16) == (e * div_mul) >> div_shift and
@@ -148,11 +151,11 @@ struct WriteArgs {
   Divisors dv;
 };
 
-size_t pack_lds_bytes(const PackArgs& a);
+size_t pack_lds_bytes(const PackPlan& pl);
 Divisors make_divisors(int64_t row_bytes, int64_t page_tokens, uint64_t page_bytes);
 // Chunk geometry of a pack (g0, g1, t1, t2) for a device with n_cu compute units.
-void pack_chunks(PackArgs* a, int n_cu);
-hipError_t launch_pack(const PackArgs& a, hipStream_t stream);
+void pack_chunks(PackPlan* pl, int n_cu);
+hipError_t launch_pack(const PackPlan& pl, hipStream_t stream);
 hipError_t launch_write(const WriteArgs& a, hipStream_t stream);
 hipError_t launch_cost(const SampleDesc* desc, const int32_t* slots, int32_t n, int64_t k,
                        int64_t* out_cost, hipStream_t stream);

@@ -63,7 +63,7 @@ __device__ __forceinline__ T ld(const void* p) {
 // (kernarg preloading); the first loads of the row lookup then leave at once,
 // alongside the kernel-argument loads of the rest.
 struct PackHead {
-  int32_t g0, g1, t1, t2;   // chunk geometry (as in PackArgs)
+  int32_t g0, g1, t1, t2;   // chunk geometry (as in PackPlan)
   uint64_t div_mul;         // e / (row_bytes / 16) == (e * div_mul) >> div_shift
   int32_t div_shift;
   int32_t bucket_shift;
@@ -71,6 +71,12 @@ struct PackHead {
   int32_t off_brun;         // byte offsets of the bucket runs and the bucket index in the run table
   int32_t off_bucket;
   int32_t total;            // vectors of the microbatch
+};
+
+// A run index: bucket size and where its bucket runs and bucket entries sit
+// in the run table.
+struct RunIndex {
+  int32_t shift, off_brun, off_bucket;
 };
 
 // e / (row_bytes / 16) as a multiply and a shift (host-computed constants).
@@ -94,47 +100,60 @@ struct BucketHit {
 };
 
 template <bool kScalar>
-__device__ __forceinline__ BucketHit bucket_of(const PackHead& h, const uint8_t* tb, int row) {
-  const int b = row >> h.bucket_shift;
-  return BucketHit{ld_run<kScalar>(reinterpret_cast<const PackRun*>(tb + h.off_brun) + b),
-                   ld<kScalar, uint32_t>(tb + h.off_bucket + 4 * (b >> 1))};
+__device__ __forceinline__ BucketHit bucket_of(const RunIndex& x, const uint8_t* tb, int row) {
+  const int b = row >> x.shift;
+  return BucketHit{ld_run<kScalar>(reinterpret_cast<const PackRun*>(tb + x.off_brun) + b),
+                   ld<kScalar, uint32_t>(tb + x.off_bucket + 4 * (b >> 1))};
 }
 
-// Run holding packed row `row`: its bucket's run, or a later one, stepped to
-// from that run's number when the bucket's run ends at or before the row.
+// Run holding row `row`: its bucket's run, or a later one, stepped to from
+// that run's number when the bucket's run ends at or before the row.
 template <bool kScalar>
-__device__ __forceinline__ PackRun run_of(const PackHead& h, const PackArgs& a, const uint8_t* tb, int row,
+__device__ __forceinline__ PackRun run_of(const RunIndex& x, int32_t off_runs, const uint8_t* tb, int row,
                                           const BucketHit& hit, int* s_out = nullptr) {
   PackRun r = hit.r;
   if (r.end <= row || s_out) {
-    const int b = row >> h.bucket_shift;
+    const int b = row >> x.shift;
     int s = (int)((b & 1) ? (hit.w >> 16) : (hit.w & 0xffffu));
-    const PackRun* runs = reinterpret_cast<const PackRun*>(tb + a.off_runs);
+    const PackRun* runs = reinterpret_cast<const PackRun*>(tb + off_runs);
     while (r.end <= row) r = ld_run<kScalar>(runs + ++s);
     if (s_out) *s_out = s;
   }
   return r;
 }
 
+// Row of physical memory holding visual row `vidx` of the sample whose page
+// GVAs start at 64-bit word `word` of the arena: visual index -> page GVA
+// (the sample's page list) -> page-table entry (the GVA's page number) -> row
+// in the physical page. Returns the page-table entry's flags in *flags.
+template <bool kScalar>
+__device__ __forceinline__ uint64_t walk(const PackArgs& a, int32_t word, uint32_t vidx, uint64_t* flags) {
+  const int lp = (int)(((uint64_t)vidx * a.pt_mul) >> a.pt_shift);
+  const int in_page = (int)vidx - lp * a.page_tokens;
+  const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)word + lp));
+  const uint64_t vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
+  const uint64_t pte = ld<kScalar, uint64_t>(a.pte + vpn);
+  *flags = pte;
+  return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
+}
+
+__device__ __forceinline__ uint64_t text_row(const PackArgs& a, int32_t id) {
+  return reinterpret_cast<uint64_t>(a.table) + (uint64_t)(uint32_t)id * (uint64_t)a.row_bytes;
+}
+
 // Source address of packed row `row` of run r, or 0 when the tier mask
 // leaves the row out. A text row's id selects an embedding-table row; an
-// image row walks the page table: visual index -> page GVA (the sample's page
-// list) -> page-table entry (the GVA's page number) -> row in the physical page.
+// image row walks the page table.
 template <bool kScalar>
 __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun& run, int row) {
   if (run.head < 0) {
     if (!(a.tier_mask & 1)) return 0;
-    const int32_t id = ld<kScalar, int32_t>(a.meta + 4 * ((int64_t)run.word + row));
-    return reinterpret_cast<uint64_t>(a.table) + (uint64_t)(uint32_t)id * (uint64_t)a.row_bytes;
+    return text_row(a, ld<kScalar, int32_t>(a.meta + 4 * ((int64_t)run.word + row)));
   }
-  const uint32_t vidx = (uint32_t)(row + run.vdelta);
-  const int lp = (int)(((uint64_t)vidx * a.pt_mul) >> a.pt_shift);
-  const int in_page = (int)vidx - lp * a.page_tokens;
-  const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)run.word + lp));
-  const uint64_t vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
-  const uint64_t pte = ld<kScalar, uint64_t>(a.pte + vpn);
-  if (!(a.tier_mask & ((pte & PTE_HOST) ? 2 : 1))) return 0;
-  return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
+  uint64_t flags = 0;
+  const uint64_t src = walk<kScalar>(a, run.word, (uint32_t)(row + run.vdelta), &flags);
+  if (!(a.tier_mask & ((flags & PTE_HOST) ? 2 : 1))) return 0;
+  return src;
 }
 
 // One workgroup packs one chunk of 256 * VPT 16-byte vectors of the output
@@ -157,6 +176,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
   const PackHead h{g0, g1, t1, t2, div_mul, div_shift, bucket_shift, staged, off_brun, off_bucket, total};
+  const RunIndex cx{h.bucket_shift, h.off_brun, h.off_bucket};
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const uint8_t* tb = h.tb ? h.tb : reinterpret_cast<const uint8_t*>(a.lens);
@@ -177,12 +197,12 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   const int r0 = div_vpr(h, v0);
   const int rows = v1 > v0 ? div_vpr(h, v1 - 1) - r0 + 1 : 0;
   // The bucket run and index entry of the wave's first row (a row of the
-  // chunk; row 0 of an empty pack, whose inline table always has them), then the other kernel
+  // chunk; row 0 of an empty pack, whose table always has them), then the other kernel
   // arguments the row resolution uses in one batch of scalar loads, in flight
   // together with it (the compiler would otherwise split the batch and load
   // it first).
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const BucketHit w0 = bucket_of<true>(h, tb, r0 + min(wave, max(rows - 1, 0)));
+  const BucketHit w0 = bucket_of<true>(cx, tb, r0 + min(wave, max(rows - 1, 0)));
   asm volatile("" : : "s"(w0.w), "s"(w0.r.end), "s"(w0.r.head), "s"(w0.r.vdelta), "s"(w0.r.word),
                "s"(a.off_runs), "s"(a.meta), "s"(a.table), "s"(a.pte), "s"(a.gva_start), "s"(a.pt_mul), "s"(a.pt_shift), "s"(a.pb_mul), "s"(a.pb_shift), "s"(a.page_tokens),
                "s"(a.tier_mask), "s"(a.row_bytes));
@@ -194,8 +214,8 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
     // chains of different rows overlap.
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
-      const BucketHit w = t == wave ? w0 : bucket_of<true>(h, tb, row);
-      const uint64_t src = row_source<true>(a, run_of<true>(h, a, tb, row, w), row);
+      const BucketHit w = t == wave ? w0 : bucket_of<true>(cx, tb, row);
+      const uint64_t src = row_source<true>(a, run_of<true>(cx, a.off_runs, tb, row, w), row);
       if (lane == 0) {
         s_src[t] = src;
         if (!src) my_skip = 1;
@@ -204,7 +224,8 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   } else {
     for (int t = tid; t < rows; t += kPackBlock) {
       const int row = r0 + t;
-      const uint64_t src = row_source<false>(a, run_of<false>(h, a, tb, row, bucket_of<false>(h, tb, row)), row);
+      const uint64_t src =
+          row_source<false>(a, run_of<false>(cx, a.off_runs, tb, row, bucket_of<false>(cx, tb, row)), row);
       s_src[t] = src;
       if (!src) my_skip = 1;
     }
@@ -281,7 +302,7 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
         const int first = blk * 64, row = first + lane;
         const int last = min(first + 63, a.n_tokens - 1);
         int s;
-        PackRun r = run_of<true>(h, a, tb, first, bucket_of<true>(h, tb, first), &s);
+        PackRun r = run_of<true>(cx, a.off_runs, tb, first, bucket_of<true>(cx, tb, first), &s);
         int start = r.head & 0x7fffffff;
         while (r.end <= last) {
           const int next = r.end;
@@ -375,33 +396,35 @@ __global__ __launch_bounds__(kBlock) void k_cost(const SampleDesc* __restrict__ 
   }
 }
 
-size_t pack_lds_bytes(const PackArgs& a) { return sizeof(uint64_t) * (size_t)a.max_chunk_rows; }
+size_t pack_lds_bytes(const PackPlan& pl) { return sizeof(uint64_t) * (size_t)std::max(pl.max_chunk_rows, 1); }
 
-void pack_chunks(PackArgs* a, int n_cu) {
-  a->vpt = a->row_bytes >= kSmallChunkRowBytes ? 2 : kVecsPerThread;
-  const int64_t chunk = (int64_t)kPackBlock * a->vpt;
-  const int64_t vecs = (int64_t)a->n_tokens * (a->row_bytes >> 4);
+void pack_chunks(PackPlan* pl, int n_cu) {
+  pl->vpt = pl->a.row_bytes >= kSmallChunkRowBytes ? 2 : kVecsPerThread;
+  const int64_t chunk = (int64_t)kPackBlock * pl->vpt;
+  const int64_t vecs = (int64_t)pl->a.n_tokens * (pl->a.row_bytes >> 4);
   const int64_t wave = (int64_t)std::max(n_cu, 1) * kPackPerCU;
   const int64_t t2 = std::max<int64_t>(vecs - (wave / 2) * kTail2Vecs, 0);
   const int64_t t1 = (std::max<int64_t>(t2 - wave * kTail1Vecs, 0) / chunk) * chunk;
-  a->g0 = (int32_t)(t1 / chunk);
-  a->g1 = (int32_t)(a->g0 + (t2 - t1 + kTail1Vecs - 1) / kTail1Vecs);
-  a->t1 = (int32_t)t1;
-  a->t2 = (int32_t)t2;
+  pl->g0 = (int32_t)(t1 / chunk);
+  pl->g1 = (int32_t)(pl->g0 + (t2 - t1 + kTail1Vecs - 1) / kTail1Vecs);
+  pl->t1 = (int32_t)t1;
+  pl->t2 = (int32_t)t2;
 }
 
-hipError_t launch_pack(const PackArgs& a, hipStream_t stream) {
-  const int64_t vecs = (int64_t)a.n_tokens * (a.row_bytes >> 4);
-  const int64_t grid64 = a.g1 + (vecs - a.t2 + kTail2Vecs - 1) / kTail2Vecs;
+template <int VPT>
+static void launch_pack_as(const PackPlan& pl, int grid, int32_t total, hipStream_t stream) {
+  hipLaunchKernelGGL(k_pack<VPT>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(pl), stream, pl.g0, pl.g1, pl.t1,
+                     pl.t2, pl.div_mul, pl.div_shift, pl.a.bucket_shift, pl.staged, pl.a.off_brun, pl.a.off_bucket,
+                     total, pl.a);
+}
+
+hipError_t launch_pack(const PackPlan& pl, hipStream_t stream) {
+  const int64_t vecs = (int64_t)pl.a.n_tokens * (pl.a.row_bytes >> 4);
+  const int64_t grid64 = pl.g1 + (vecs - pl.t2 + kTail2Vecs - 1) / kTail2Vecs;
   const int grid = grid64 > 0 ? (int)grid64 : 1;
   const int32_t total = (int32_t)vecs;               // the host keeps this below 2^31
-  if (a.vpt == 2)
-    hipLaunchKernelGGL(k_pack<2>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1, a.t1, a.t2,
-                       a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_brun, a.off_bucket, total, a);
-  else
-    hipLaunchKernelGGL(k_pack<kVecsPerThread>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(a), stream, a.g0, a.g1,
-                       a.t1, a.t2, a.div_mul, a.div_shift, a.bucket_shift, a.staged, a.off_brun, a.off_bucket, total,
-                       a);
+  if (pl.vpt == 2) launch_pack_as<2>(pl, grid, total, stream);
+  else launch_pack_as<kVecsPerThread>(pl, grid, total, stream);
   return hipGetLastError();
 }
 

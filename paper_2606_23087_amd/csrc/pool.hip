@@ -66,6 +66,14 @@ static_assert(fp::kTail2Vecs <= fp::kTail1Vecs && fp::kTail1Vecs <= 2 * fp::kPac
 // so the count stays that far below 2^31.
 constexpr int64_t kMaxVectors = (1ll << 31) - 1024;
 constexpr int kRing = 8;
+// Pinned staging buffers are at least this large; pool_create allocates them
+// all, so a call that stages no more than this never allocates.
+constexpr size_t kStageHostMin = 1 << 20;
+// Runs of one pack at most: per sample, a text run before each image and one
+// after the last, and an image run per image.
+constexpr int kMaxPackRuns = fp::kMaxPackSamples + 2 * fp::kMaxPackImages;
+// Streams remembered per sample as its readers without growing host memory.
+constexpr size_t kReaders = 8;
 
 // Restores the caller's current device on scope exit.
 struct DeviceGuard {
@@ -117,6 +125,7 @@ struct RangeAlloc {
 // Pinned host buffer + device buffer + completion event, reused round-robin.
 struct Stage {
   uint8_t* host = nullptr;
+  uint8_t* host_dev = nullptr;   // the same pinned buffer as the GPU addresses it
   size_t host_cap = 0;
   uint8_t* dev = nullptr;
   size_t dev_cap = 0;
@@ -136,7 +145,8 @@ struct SampleRec {
   int32_t written = -1;          // event after its write (metadata upload +
                                  // k_write), -1 once seen complete
   void* write_stream = nullptr;  // stream of that write
-  std::vector<void*> readers;    // streams that have packed it
+  std::vector<void*> readers;    // streams that have packed it (capacity kReaders reserved)
+  int32_t captured = 0;          // packs of it captured into HIP graphs and not yet released
 };
 
 // A freed sample whose pages, metadata and slot wait for packs still in
@@ -235,6 +245,13 @@ struct fp_pool {
   Stage ring[kRing];
   int ring_next = 0;
   fp::Divisors dv{};                  // division constants of the row, page and GVA sizes
+  // Host arrays a pack builds its run table in, sized at creation for the
+  // largest pack (kMaxPackSamples samples, kMaxPackRuns runs), so a pack
+  // allocates no host memory. Used under `mu`.
+  std::vector<SampleRec*> pk_recs;
+  std::vector<int32_t> pk_lens;
+  std::vector<fp::PackRun> pk_runs, pk_brun;
+  std::vector<uint16_t> pk_bucket;
 
   uint64_t page_gva(int tier, int64_t idx) const { return seg_start[tier] + (uint64_t)idx * (uint64_t)pb; }
   int page_index(uint64_t gva, int64_t* idx) const {
@@ -260,10 +277,14 @@ fp_status stage_acquire(fp_pool* p, size_t host_bytes, size_t dev_bytes, Stage**
   if (host_bytes > s.host_cap) {
     if (s.host) FP_HIP(hipHostFree(s.host));
     s.host = nullptr;
+    s.host_dev = nullptr;
     s.host_cap = 0;
-    size_t cap = std::max<size_t>(host_bytes, 1 << 20);
+    size_t cap = std::max<size_t>(host_bytes, kStageHostMin);
     FP_HIP(hipHostMalloc((void**)&s.host, cap, hipHostMallocDefault));
     s.host_cap = cap;
+    void* dptr = nullptr;
+    FP_HIP(hipHostGetDevicePointer(&dptr, s.host, 0));
+    s.host_dev = (uint8_t*)dptr;
   }
   if (dev_bytes > s.dev_cap) {
     if (s.dev) FP_HIP(hipFree(s.dev));
@@ -420,8 +441,9 @@ void reclaim(fp_pool* p, bool wait) {
 
 // Makes `stream` wait for the writes of the given samples that may still be
 // running on another stream (host-side check first: usually they are done).
-fp_status order_after_writes(fp_pool* p, const std::vector<SampleRec*>& recs, hipStream_t stream) {
-  for (SampleRec* r : recs) {
+fp_status order_after_writes(fp_pool* p, SampleRec* const* recs, size_t n, hipStream_t stream) {
+  for (size_t i = 0; i < n; ++i) {
+    SampleRec* r = recs[i];
     if (r->written < 0) continue;
     if (p->events.done(r->written)) {
       p->events.unref(r->written);
@@ -683,6 +705,18 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
     for (int i = 0; e == hipSuccess && i < kRing; ++i)
       e = hipEventCreateWithFlags(&p->ring[i].ev, hipEventDisableTiming);
     if (e != hipSuccess) return fail(FP_EHIP, "pool metadata allocation: %s", hipGetErrorString(e));
+    // Every staging slot's pinned buffer now, so that calls staging at most
+    // kStageHostMin bytes (plans, pack run tables) never allocate one.
+    for (int i = 0; i < kRing; ++i) {
+      Stage* sg = nullptr;
+      fp_status ss = stage_acquire(p, kStageHostMin, 0, &sg);
+      if (ss != FP_OK) return ss;
+    }
+    p->pk_recs.resize(fp::kMaxPackSamples);
+    p->pk_lens.resize(fp::kMaxPackSamples);
+    p->pk_runs.resize(kMaxPackRuns);
+    p->pk_brun.resize(fp::kBuckets);
+    p->pk_bucket.resize(fp::kBuckets);
     p->meta.init(c.meta_bytes);
     p->free_slots.resize((size_t)c.max_samples);
     for (int64_t i = 0; i < c.max_samples; ++i) p->free_slots[(size_t)i] = (int32_t)(c.max_samples - 1 - i);
@@ -845,6 +879,7 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
     rec.meta_len = meta_len;
     rec.text_off = d.text_off;
     rec.page_off = d.page_off;
+    rec.readers.reserve(kReaders);
     rec.img.resize(2 * (size_t)n_img);
     for (int32_t j = 0; j < n_img; ++j) {
       rec.img[2 * (size_t)j] = img_pos[j];
@@ -864,6 +899,9 @@ fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
     auto it = p->samples.find(sample_id);
     if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_id);
     SampleRec& r = it->second;
+    if (r.captured > 0)
+      return fail(FP_ESTATE, "sample %llu is read by %d captured pack(s): release them with pool_release_captured first",
+                  (unsigned long long)sample_id, r.captured);
     DeviceGuard guard(p->cfg.device);
     if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
     // The sample's own write is waited for here, so that reuse of its pages
@@ -933,6 +971,9 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
       if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
       if (!seen.insert(sample_ids[i]).second)
         return fail(FP_EINVAL, "sample %llu listed twice", (unsigned long long)sample_ids[i]);
+      if (it->second.captured > 0)
+        return fail(FP_ESTATE, "sample %llu is read by %d captured pack(s): its pages cannot move until "
+                               "pool_release_captured", (unsigned long long)sample_ids[i], it->second.captured);
       std::vector<int32_t> mv;
       for (size_t k = 0; k < it->second.pages.size(); ++k) {
         int64_t idx = 0;
@@ -970,7 +1011,7 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
       unreserve();
       return fail(FP_ESTATE, "pool_migrate cannot be captured into a graph (it moves pages now)");
     }
-    fp_status st = order_after_writes(p, recs, hs);   // the copies read what the writes wrote
+    fp_status st = order_after_writes(p, recs.data(), recs.size(), hs);   // the copies read what the writes wrote
     if (st != FP_OK) {
       unreserve();
       return st;
@@ -1142,16 +1183,18 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
       if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
       hipStream_t hs = (hipStream_t)stream;
       if (capturing(hs)) return fail(FP_ESTATE, "plan_microbatches waits for its result and cannot be captured");
+      // The cost kernel reads the slots from, and writes the costs to, a
+      // pinned staging buffer directly: no copy kernels run beside the packs
+      // of other streams.
       const size_t slot_bytes = align16(4ll * n);
       Stage* s = nullptr;
-      fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, slot_bytes + 8 * (size_t)n, &s);
+      fp_status st = stage_acquire(p, slot_bytes + 8 * (size_t)n, 0, &s);
       if (st != FP_OK) return st;
       std::memcpy(s->host, slots.data(), 4 * (size_t)n);
-      FP_HIP(hipMemcpyAsync(s->dev, s->host, 4 * (size_t)n, hipMemcpyHostToDevice, hs));
-      st = order_after_writes(p, recs, hs);   // the descriptors come from the writes
+      st = order_after_writes(p, recs.data(), recs.size(), hs);   // the descriptors come from the writes
       if (st != FP_OK) return st;
-      FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->dev, n, cost_k, (int64_t*)(s->dev + slot_bytes), hs));
-      FP_HIP(hipMemcpyAsync(s->host + slot_bytes, s->dev + slot_bytes, 8 * (size_t)n, hipMemcpyDeviceToHost, hs));
+      FP_HIP(fp::launch_cost(p->desc_dev, (const int32_t*)s->host_dev, n, cost_k,
+                             (int64_t*)(s->host_dev + slot_bytes), hs));
       FP_HIP(hipStreamSynchronize(hs));
       std::memcpy(costs.data(), s->host + slot_bytes, 8 * (size_t)n);
       st = stage_release(s, hs);
@@ -1293,180 +1336,243 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
   });
 }
 
+// Bucket index of runs covering rows [0, total) (run k starts where run k-1
+// ends): at most kBuckets buckets of 2^shift rows; bucket b gets the run
+// holding its first row and that run's number. Returns the bucket count.
+static int32_t build_buckets(const fp::PackRun* runs, int32_t n_runs, int64_t total, int32_t* shift_out,
+                             fp::PackRun* brun, uint16_t* bucket) {
+  int32_t shift = 0;
+  while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
+  const int32_t nb = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
+  for (int32_t b = 0, k = 0; b < nb; ++b) {
+    const int64_t first = (int64_t)b << shift;
+    while (k + 1 < n_runs && runs[k].end <= first) ++k;
+    bucket[b] = (uint16_t)k;
+    brun[b] = runs[k];
+  }
+  *shift_out = shift;
+  return nb;
+}
+
+// pack_microbatch, and (scratch_dev != null) its variant that stages a large
+// run table into the caller-supplied device scratch instead of the pool's
+// staging buffers and allocates nothing.
+static fp_status pack_impl(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,
+                           int64_t vocab, void* out_emb, int64_t out_rows_cap, int32_t* out_cu_seqlens,
+                           int32_t* out_position_ids, int32_t* out_n_tokens, int32_t* out_max_seqlen,
+                           int32_t tier_mask, void* stream, uint8_t* scratch_dev, size_t scratch_bytes) {
+  const bool noalloc = scratch_dev != nullptr;
+  if (!p) return fail(FP_EINVAL, "null pool");
+  std::lock_guard<std::mutex> lock(p->mu);
+  if (n < 0 || n > fp::kMaxPackSamples) return fail(FP_EINVAL, "n %d outside [0, %d]", n, fp::kMaxPackSamples);
+  if (n && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
+  if (tier_mask < 1 || tier_mask > 3) return fail(FP_EINVAL, "tier_mask %d", tier_mask);
+  if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
+  if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
+  if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
+  SampleRec** recs = p->pk_recs.data();
+  int64_t total = 0, n_text = 0, n_imgs = 0;
+  int32_t mx = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    auto it = p->samples.find(sample_ids[i]);
+    if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
+    SampleRec& r = it->second;
+    recs[i] = &r;
+    total += r.len;
+    n_text += r.n_text;
+    n_imgs += r.n_img;
+    mx = std::max(mx, r.len);
+  }
+  if (n_imgs > fp::kMaxPackImages)
+    return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
+  if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
+  const int64_t vpr = p->rb / 16;
+  if (total * vpr > kMaxVectors)
+    return fail(FP_EINVAL, "microbatch of %lld rows of %lld bytes is too large", (long long)total, (long long)p->rb);
+  if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
+  if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
+    if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
+    if (vocab < p->cfg.vocab) return fail(FP_EINVAL, "table vocab %lld < pool vocab %lld", (long long)vocab, (long long)p->cfg.vocab);
+  }
+  if (noalloc) {
+    // Remembering a new reader stream must not grow a sample's list.
+    for (int32_t i = 0; i < n; ++i) {
+      const SampleRec& r = *recs[i];
+      if (std::find(r.readers.begin(), r.readers.end(), stream) == r.readers.end() &&
+          r.readers.size() >= r.readers.capacity())
+        return fail(FP_ESTATE, "sample %llu was packed on %zu other streams, the most this call can record "
+                               "without allocating", (unsigned long long)sample_ids[i], r.readers.size());
+    }
+  }
+  DeviceGuard guard(p->cfg.device);
+  if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+  hipStream_t hs = (hipStream_t)stream;
+  fp::PackPlan pl{};
+  fp::PackArgs& a = pl.a;
+  a.meta = p->meta_dev;
+  a.pte = p->pte_dev;
+  a.gva_start = p->gva_start;
+  a.table = (const uint8_t*)embed_table;
+  a.out = (uint8_t*)out_emb;
+  a.cu = out_cu_seqlens;
+  a.pos = out_position_ids;
+  a.n = n;
+  a.n_tokens = (int32_t)total;
+  a.row_bytes = (int32_t)p->rb;
+  a.page_tokens = p->cfg.page_tokens;
+  a.tier_mask = tier_mask;
+  a.pt_mul = p->dv.pt_mul;
+  a.pt_shift = p->dv.pt_shift;
+  a.pb_mul = p->dv.pb_mul;
+  a.pb_shift = p->dv.pb_shift;
+  pl.div_mul = p->dv.div_mul;
+  pl.div_shift = p->dv.div_shift;
+  // The run table: sample lengths, then the runs of every sample in row
+  // order (a text run per nonempty stretch of text rows, an image run per
+  // stretch of images with no text row between them), then the bucket index.
+  int32_t* lens = p->pk_lens.data();
+  fp::PackRun* runs = p->pk_runs.data();
+  int32_t n_runs = 0;
+  {
+    int32_t row = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      const SampleRec& r = *recs[i];
+      const int32_t s0 = row;
+      lens[i] = r.len;
+      int32_t ti = 0, vis = 0;
+      bool in_image = false;
+      auto text_to = [&](int32_t upto) {
+        if (upto <= ti) return;
+        if (n_runs) runs[n_runs - 1].end = row;
+        runs[n_runs++] = fp::PackRun{0, s0 | fp::kTextRun, 0, (int32_t)(r.text_off / 4 + ti - row)};
+        row += upto - ti;
+        ti = upto;
+        in_image = false;
+      };
+      for (int32_t j = 0; j < r.n_img; ++j) {
+        text_to(r.img[2 * (size_t)j]);
+        const int32_t nt = r.img[2 * (size_t)j + 1];
+        if (nt <= 0) continue;
+        if (!in_image) {
+          if (n_runs) runs[n_runs - 1].end = row;
+          runs[n_runs++] = fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)};
+          in_image = true;
+        }
+        row += nt;
+        vis += nt;
+      }
+      text_to(r.n_text);
+    }
+    if (n_runs) runs[n_runs - 1].end = row;
+  }
+  int32_t shift = 0;
+  const int32_t n_buckets = build_buckets(runs, n_runs, total, &shift, p->pk_brun.data(), p->pk_bucket.data());
+  const int32_t bucket_len = n_buckets + (n_buckets & 1);
+  a.bucket_shift = shift;
+
+  pl.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
+  fp::pack_chunks(&pl, p->n_cu);
+
+  const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;
+  const bool captured = capturing(hs);
+  if (captured) {
+    // A captured pack is one kernel whose arguments hold the whole
+    // microbatch, so a replay packs the same samples again.
+    if (staged)
+      return fail(FP_ESTATE, "a pack of more than %d samples or %d runs cannot be captured into a graph",
+                  fp::kInlineSamples, fp::kInlineRuns);
+    // No event queries during capture: the writes must already be known complete.
+    for (int32_t i = 0; i < n; ++i)
+      if (recs[i]->written >= 0)
+        return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
+                               "before capturing its pack");
+  }
+  Stage* s = nullptr;
+  if (!staged) {
+    if (n) std::memcpy(a.lens, lens, 4 * (size_t)n);
+    if (n_runs) std::memcpy(a.runs, runs, sizeof(fp::PackRun) * (size_t)n_runs);
+    if (n_buckets) std::memcpy(a.bucket, p->pk_bucket.data(), 2 * (size_t)n_buckets);
+    if (n_buckets) std::memcpy(a.brun, p->pk_brun.data(), sizeof(fp::PackRun) * (size_t)n_buckets);
+    a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
+    a.off_brun = (int32_t)(offsetof(fp::PackArgs, brun) - offsetof(fp::PackArgs, lens));
+    a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
+    pl.staged = nullptr;
+  } else {
+    const size_t o_runs = ((size_t)4 * n + 15) & ~(size_t)15;
+    const size_t o_br = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
+    const size_t o_b = o_br + sizeof(fp::PackRun) * (size_t)n_buckets;
+    const size_t bytes = o_b + 2 * (size_t)bucket_len;
+    uint8_t* dest = nullptr;
+    if (noalloc) {
+      if (bytes > scratch_bytes)
+        return fail(FP_ECAPACITY, "run table of %zu bytes exceeds the %zu-byte scratch", bytes, scratch_bytes);
+      fp_status st = stage_acquire(p, bytes, 0, &s);        // never allocates: buffers hold kStageHostMin
+      if (st != FP_OK) return st;
+      dest = scratch_dev;
+    } else {
+      fp_status st = stage_acquire(p, bytes, bytes, &s);
+      if (st != FP_OK) return st;
+      dest = s->dev;
+    }
+    std::memset(s->host, 0, bytes);
+    if (n) std::memcpy(s->host, lens, 4 * (size_t)n);
+    if (n_runs) std::memcpy(s->host + o_runs, runs, sizeof(fp::PackRun) * (size_t)n_runs);
+    if (n_buckets) std::memcpy(s->host + o_br, p->pk_brun.data(), sizeof(fp::PackRun) * (size_t)n_buckets);
+    if (n_buckets) std::memcpy(s->host + o_b, p->pk_bucket.data(), 2 * (size_t)n_buckets);
+    FP_HIP(hipMemcpyAsync(dest, s->host, bytes, hipMemcpyHostToDevice, hs));
+    pl.staged = dest;
+    a.off_runs = (int32_t)o_runs;
+    a.off_brun = (int32_t)o_br;
+    a.off_bucket = (int32_t)o_b;
+  }
+  {
+    fp_status st = order_after_writes(p, recs, (size_t)n, hs);
+    if (st != FP_OK) return st;
+  }
+  hipError_t e = fp::launch_pack(pl, hs);
+  if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
+  if (s) {
+    fp_status st = stage_release(s, hs);
+    if (st != FP_OK) return st;
+  }
+  // Remember the stream as a reader of each sample; a free records its event
+  // there (no event per pack: events between back-to-back packs slow them).
+  for (int32_t i = 0; i < n; ++i) {
+    SampleRec* r = recs[i];
+    if (std::find(r->readers.begin(), r->readers.end(), stream) == r->readers.end()) r->readers.push_back(stream);
+    if (captured) ++r->captured;
+  }
+  if (out_n_tokens) *out_n_tokens = (int32_t)total;
+  if (out_max_seqlen) *out_max_seqlen = mx;
+  return FP_OK;
+}
+
 fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,
                           int64_t vocab, void* out_emb, int64_t out_rows_cap, int32_t* out_cu_seqlens,
                           int32_t* out_position_ids, int32_t* out_n_tokens, int32_t* out_max_seqlen,
                           int32_t tier_mask, void* stream) {
   return guarded([&]() -> fp_status {
+    return pack_impl(p, sample_ids, n, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens, out_position_ids,
+                     out_n_tokens, out_max_seqlen, tier_mask, stream, nullptr, 0);
+  });
+}
+
+fp_status pool_release_captured(fp_pool* p, const uint64_t* sample_ids, int32_t n) {
+  return guarded([&]() -> fp_status {
     if (!p) return fail(FP_EINVAL, "null pool");
+    if (n < 0 || (n > 0 && !sample_ids)) return fail(FP_EINVAL, "n %d / null sample_ids", n);
     std::lock_guard<std::mutex> lock(p->mu);
-    if (n < 0 || n > fp::kMaxPackSamples) return fail(FP_EINVAL, "n %d outside [0, %d]", n, fp::kMaxPackSamples);
-    if (n && !sample_ids) return fail(FP_EINVAL, "null sample_ids");
-    if (tier_mask < 1 || tier_mask > 3) return fail(FP_EINVAL, "tier_mask %d", tier_mask);
-    if (out_rows_cap < 0) return fail(FP_EINVAL, "out_rows_cap");
-    if ((uintptr_t)out_emb % 16 || (uintptr_t)embed_table % 16) return fail(FP_EALIGN, "out_emb/embed_table alignment");
-    if ((uintptr_t)out_cu_seqlens % 4 || (uintptr_t)out_position_ids % 4) return fail(FP_EALIGN, "cu/pos alignment");
-    std::vector<SampleRec*> recs((size_t)n);
-    int64_t total = 0, n_text = 0, n_imgs = 0;
-    int32_t mx = 0;
-    for (int32_t i = 0; i < n; ++i) {
-      auto it = p->samples.find(sample_ids[i]);
-      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)sample_ids[i]);
-      SampleRec& r = it->second;
-      recs[(size_t)i] = &r;
-      total += r.len;
-      n_text += r.n_text;
-      n_imgs += r.n_img;
-      mx = std::max(mx, r.len);
+    // All-or-nothing: every listed occurrence must hold a capture.
+    std::unordered_map<uint64_t, int32_t> want;
+    for (int32_t i = 0; i < n; ++i) ++want[sample_ids[i]];
+    for (const auto& kv : want) {
+      auto it = p->samples.find(kv.first);
+      if (it == p->samples.end()) return fail(FP_ENOENT, "sample %llu", (unsigned long long)kv.first);
+      if (it->second.captured < kv.second)
+        return fail(FP_EINVAL, "sample %llu holds %d captured pack(s), %d released", (unsigned long long)kv.first,
+                    it->second.captured, kv.second);
     }
-    if (n_imgs > fp::kMaxPackImages)
-      return fail(FP_EINVAL, "%lld images in one microbatch (at most %d)", (long long)n_imgs, fp::kMaxPackImages);
-    if (total > out_rows_cap) return fail(FP_ECAPACITY, "%lld rows > capacity %lld", (long long)total, (long long)out_rows_cap);
-    const int64_t vpr = p->rb / 16;
-    if (total * vpr > kMaxVectors)
-      return fail(FP_EINVAL, "microbatch of %lld rows of %lld bytes is too large", (long long)total, (long long)p->rb);
-    if (total > 0 && !out_emb) return fail(FP_EINVAL, "null out_emb");
-    if (n_text > 0 && (tier_mask & FP_TIER_MASK_HBM)) {
-      if (!embed_table) return fail(FP_EINVAL, "null embed_table with text rows");
-      if (vocab < p->cfg.vocab) return fail(FP_EINVAL, "table vocab %lld < pool vocab %lld", (long long)vocab, (long long)p->cfg.vocab);
-    }
-    DeviceGuard guard(p->cfg.device);
-    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
-    hipStream_t hs = (hipStream_t)stream;
-    fp::PackArgs a{};
-    a.meta = p->meta_dev;
-    a.pte = p->pte_dev;
-    a.gva_start = p->gva_start;
-    a.page_bytes = (uint64_t)p->pb;
-    a.table = (const uint8_t*)embed_table;
-    a.out = (uint8_t*)out_emb;
-    a.cu = out_cu_seqlens;
-    a.pos = out_position_ids;
-    a.n = n;
-    a.n_tokens = (int32_t)total;
-    a.row_bytes = (int32_t)p->rb;
-    a.page_tokens = p->cfg.page_tokens;
-    a.tier_mask = tier_mask;
-    a.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
-    fp::pack_chunks(&a, p->n_cu);
-    a.div_mul = p->dv.div_mul;
-    a.div_shift = p->dv.div_shift;
-    a.pt_mul = p->dv.pt_mul;
-    a.pt_shift = p->dv.pt_shift;
-    a.pb_mul = p->dv.pb_mul;
-    a.pb_shift = p->dv.pb_shift;
-    // The run table: sample lengths, then the runs of every sample in row
-    // order (a text run per nonempty stretch of text rows, an image run per
-    // stretch of images with no text row between them), then the bucket index.
-    std::vector<int32_t> lens((size_t)n), run_start;
-    std::vector<fp::PackRun> runs;
-    {
-      int32_t row = 0;
-      auto close_run = [&]() {
-        if (!runs.empty()) runs.back().end = row;
-      };
-      for (int32_t i = 0; i < n; ++i) {
-        const SampleRec& r = *recs[(size_t)i];
-        const int32_t s0 = row;
-        lens[(size_t)i] = r.len;
-        int32_t ti = 0, vis = 0;
-        bool in_image = false;
-        auto text_to = [&](int32_t upto) {
-          if (upto <= ti) return;
-          close_run();
-          run_start.push_back(row);
-          runs.push_back(fp::PackRun{0, s0 | fp::kTextRun, 0, (int32_t)(r.text_off / 4 + ti - row)});
-          row += upto - ti;
-          ti = upto;
-          in_image = false;
-        };
-        for (int32_t j = 0; j < r.n_img; ++j) {
-          text_to(r.img[2 * (size_t)j]);
-          const int32_t nt = r.img[2 * (size_t)j + 1];
-          if (nt <= 0) continue;
-          if (!in_image) {
-            close_run();
-            run_start.push_back(row);
-            runs.push_back(fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)});
-            in_image = true;
-          }
-          row += nt;
-          vis += nt;
-        }
-        text_to(r.n_text);
-      }
-      close_run();
-    }
-    const int32_t n_runs = (int32_t)runs.size();
-    int32_t shift = 0;
-    while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
-    const int32_t n_buckets = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
-    std::vector<uint16_t> bucket((size_t)(n_buckets + (n_buckets & 1)), 0);
-    std::vector<fp::PackRun> brun((size_t)n_buckets);
-    for (int32_t b = 0, sidx = 0; b < n_buckets; ++b) {
-      const int64_t first = (int64_t)b << shift;
-      while (sidx + 1 < n_runs && run_start[(size_t)sidx + 1] <= first) ++sidx;
-      bucket[(size_t)b] = (uint16_t)sidx;
-      brun[(size_t)b] = runs[(size_t)sidx];
-    }
-    a.n_runs = n_runs;
-    a.bucket_shift = shift;
-    const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;
-    if (capturing(hs)) {
-      // A captured pack is one kernel whose arguments hold the whole
-      // microbatch, so a replay packs the same samples again.
-      if (staged)
-        return fail(FP_ESTATE, "a pack of more than %d samples or %d runs cannot be captured into a graph",
-                    fp::kInlineSamples, fp::kInlineRuns);
-      // No event queries during capture: the writes must already be known complete.
-      for (SampleRec* r : recs)
-        if (r->written >= 0)
-          return fail(FP_ESTATE, "a sample's write is not known complete: synchronize and call pool_reclaim "
-                                 "before capturing its pack");
-    }
-    Stage* s = nullptr;
-    if (!staged) {
-      if (n) std::memcpy(a.lens, lens.data(), 4 * lens.size());
-      if (n_runs) std::memcpy(a.runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
-      if (n_buckets) std::memcpy(a.bucket, bucket.data(), 2 * (size_t)n_buckets);
-      if (n_buckets) std::memcpy(a.brun, brun.data(), sizeof(fp::PackRun) * (size_t)n_buckets);
-      a.off_runs = (int32_t)(offsetof(fp::PackArgs, runs) - offsetof(fp::PackArgs, lens));
-      a.off_brun = (int32_t)(offsetof(fp::PackArgs, brun) - offsetof(fp::PackArgs, lens));
-      a.off_bucket = (int32_t)(offsetof(fp::PackArgs, bucket) - offsetof(fp::PackArgs, lens));
-    } else {
-      const size_t o_runs = (4 * lens.size() + 15) & ~(size_t)15;
-      const size_t o_br = o_runs + sizeof(fp::PackRun) * (size_t)n_runs;
-      const size_t o_b = o_br + sizeof(fp::PackRun) * brun.size();
-      const size_t bytes = o_b + 2 * bucket.size();
-      fp_status st = stage_acquire(p, bytes, bytes, &s);
-      if (st != FP_OK) return st;
-      std::memset(s->host, 0, bytes);
-      if (n) std::memcpy(s->host, lens.data(), 4 * lens.size());
-      if (n_runs) std::memcpy(s->host + o_runs, runs.data(), sizeof(fp::PackRun) * (size_t)n_runs);
-      if (!brun.empty()) std::memcpy(s->host + o_br, brun.data(), sizeof(fp::PackRun) * brun.size());
-      if (!bucket.empty()) std::memcpy(s->host + o_b, bucket.data(), 2 * bucket.size());
-      FP_HIP(hipMemcpyAsync(s->dev, s->host, bytes, hipMemcpyHostToDevice, hs));
-      a.staged = s->dev;
-      a.off_runs = (int32_t)o_runs;
-      a.off_brun = (int32_t)o_br;
-      a.off_bucket = (int32_t)o_b;
-    }
-    {
-      fp_status st = order_after_writes(p, recs, hs);
-      if (st != FP_OK) return st;
-    }
-    hipError_t e = fp::launch_pack(a, hs);
-    if (e != hipSuccess) return fail(FP_EHIP, "pack kernel: %s", hipGetErrorString(e));
-    if (s) {
-      fp_status st = stage_release(s, hs);
-      if (st != FP_OK) return st;
-    }
-    // Remember the stream as a reader of each sample; a free records its event
-    // there (no event per pack: events between back-to-back packs slow them).
-    for (SampleRec* r : recs)
-      if (std::find(r->readers.begin(), r->readers.end(), stream) == r->readers.end()) r->readers.push_back(stream);
-    if (out_n_tokens) *out_n_tokens = (int32_t)total;
-    if (out_max_seqlen) *out_max_seqlen = mx;
+    for (const auto& kv : want) p->samples.find(kv.first)->second.captured -= kv.second;
     return FP_OK;
   });
 }

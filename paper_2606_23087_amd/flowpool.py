@@ -33,7 +33,7 @@ except ImportError:
     pass
 
 _lib = C.CDLL(LIB_PATH)
-ABI_VERSION = 4   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
+ABI_VERSION = 5   # FP_ABI_VERSION of include/flowpool.h that these bindings follow
 if _lib.fp_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI version {_lib.fp_abi_version()}, the bindings expect {ABI_VERSION}; rebuild it")
 
@@ -94,6 +94,7 @@ _SIGS = {
     "pool_translate": (C.c_int32, [_P, C.c_uint64, _i32p, _u64p]),
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
     "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
+    "pool_release_captured": (C.c_int32, [_P, _u64p, C.c_int32]),
     "pool_migrate": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, _P, _i64p]),
     "alloc_candidates": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i32p,
                                      C.c_int32, _i32p]),
@@ -238,6 +239,12 @@ def pool_reclaim(pool: int, wait: bool = False) -> int:
     n = C.c_int64()
     _check(_lib.pool_reclaim(pool, 1 if wait else 0, C.byref(n)), "pool_reclaim")
     return int(n.value)
+
+
+def pool_release_captured(pool: int, sample_ids) -> None:
+    """End a captured pack's hold on its samples (once its graph will not be replayed again)."""
+    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    _check(_lib.pool_release_captured(pool, idp, len(ids)), "pool_release_captured")
 
 
 def pool_migrate(pool: int, sample_ids, tier: int, stream=None) -> int:

@@ -105,3 +105,60 @@ def test_uncapturable_calls_refuse(fp):
     finally:
         torch.cuda.synchronize()
         w.close()
+
+
+def test_captured_samples_are_held(fp):
+    """A captured pack holds its samples: freeing or migrating one returns
+    ESTATE (its page list stays where the graph reads it), replays still
+    give the eager result, and after pool_release_captured the samples move
+    and free as usual (the graph is not replayed after that)."""
+    from paper_2606_23087_amd.harness import GpuWorkload
+    say("case captured samples are held")
+    cfg = scaled(CONFIGS["tiered"], hbm_pages=400, host_pages=400, vocab=3000, capacity=16384, n_mb=1)
+    w = GpuWorkload(cfg, 4, specs=gen_samples(cfg, 4, count=3), mode="tagged")
+    try:
+        torch.cuda.synchronize()
+        fp.pool_reclaim(w.pool, True)
+        ids = list(w.ids)
+        eager, ec, ep = w.alloc_outputs(fill=0x2222)
+        w.pack(ids, eager, ec, ep)
+        torch.cuda.synchronize()
+        out, cu, pos = w.alloc_outputs(fill=0x2222)
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                w.pack(ids, out, cu, pos)
+        torch.cuda.synchronize()
+        pages_before = [fp.pool_sample_pages(w.pool, s).tolist() for s in ids]
+        with pytest.raises(fp.FlowPoolError, match="ESTATE"):
+            fp.pool_migrate(w.pool, [ids[0]], fp.FP_TIER_HBM)
+        with pytest.raises(fp.FlowPoolError, match="ESTATE"):
+            fp.pool_free_sample(w.pool, ids[1])
+        assert [fp.pool_sample_pages(w.pool, s).tolist() for s in ids] == pages_before
+        for rep in range(2):
+            out.fill_(0x2222)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, eager) and torch.equal(cu, ec) and torch.equal(pos, ep), f"replay {rep}"
+        del g
+        with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+            fp.pool_release_captured(w.pool, ids + ids)        # each was captured once
+        with pytest.raises(fp.FlowPoolError, match="ENOENT"):
+            fp.pool_release_captured(w.pool, [10 ** 9])
+        fp.pool_release_captured(w.pool, ids[::-1])
+        with pytest.raises(fp.FlowPoolError, match="EINVAL"):
+            fp.pool_release_captured(w.pool, ids[:1])          # already released
+        moved = fp.pool_migrate(w.pool, ids, fp.FP_TIER_HBM)
+        assert moved > 0
+        torch.cuda.synchronize()
+        again, ac, ap = w.alloc_outputs(fill=0x2222)
+        w.pack(ids, again, ac, ap)
+        torch.cuda.synchronize()
+        assert torch.equal(again, eager)
+        fp.pool_free_sample(w.pool, ids[1])
+    finally:
+        torch.cuda.synchronize()
+        w.close()

@@ -10,7 +10,7 @@
 - The pack kernels' leading scalar arguments (13 dwords) arrive preloaded in
   scalar registers, and the first loads of the row lookup (the bucket's run and
   index entry) are issued before the wait for the other kernel arguments, so the two are in
-  flight together.
+  flight together (for the all-rows kernels, ahead of every kernel-argument load).
 """
 
 import os
@@ -87,4 +87,11 @@ def test_pack_kernels_preload_their_head_arguments(isa):
         body = [l.strip() for l in lines[entry:]]
         first_wait = next(i for i, l in enumerate(body) if l.startswith("s_waitcnt"))
         loads = [l for l in body[:first_wait] if l.startswith("s_load")]
-        assert loads and not loads[0].split(",")[1].strip().startswith("s[0:1]"), (name, loads[:3])
+        table_loads = [l for l in loads if not l.split(",")[1].strip().startswith("s[0:1]")]
+        if "Lb0E" in name:
+            # the row-lookup loads leave first
+            assert loads and loads[0] in table_loads, (name, loads[:3])
+        else:
+            # compact packs (tier-masked): the row-lookup loads at least leave
+            # before the first wait, in flight with the argument loads
+            assert table_loads, (name, loads[:3])

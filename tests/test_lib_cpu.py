@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(fp.EXPORTED)
-    assert fp.fp_abi_version() == fp.ABI_VERSION == 4
+    assert fp.fp_abi_version() == fp.ABI_VERSION == 5
 
 
 def test_constants_match_header():
