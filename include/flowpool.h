@@ -381,6 +381,27 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n,
                           int32_t* out_n_tokens, int32_t* out_max_seqlen,
                           int32_t tier_mask, void* stream);
 
+/* pack_microbatch for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same arguments, result and errors, but the call allocates nothing, host or
+ * device, on success. A microbatch whose row table does not fit the kernel
+ * arguments (more than 32 samples or 160 runs) has it copied, from one of the
+ * staging buffers pool_create allocated, into a 64 KiB device scratch array
+ * of the library, one per GPU, which holds the largest table a pack can have;
+ * a larger table returns ECAPACITY (it cannot occur within the limits of
+ * pack_microbatch). Every call on one GPU shares that array and leaves its
+ * table there: calls that overlap on one GPU (on different streams, or
+ * through different pools, with neither ordered after the other) race and
+ * may read each other's table; calls in order on one stream do not. A sample
+ * already packed on 8 other streams returns ESTATE when packed on a new one
+ * (recording a 9th reader stream would grow a host list). */
+fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_t n,
+                                  const void* embed_table, int64_t vocab,
+                                  void* out_emb, int64_t out_rows_cap,
+                                  int32_t* out_cu_seqlens, int32_t* out_position_ids,
+                                  int32_t* out_n_tokens, int32_t* out_max_seqlen,
+                                  int32_t tier_mask, void* stream);
+
 /* Ends the hold that captured packs have on their samples (see HIP graphs
  * above): call it with a captured pack's sample id list (host uint64[n], in
  * any order; an id listed twice releases two captures of it) once no graph

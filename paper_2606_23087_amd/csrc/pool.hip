@@ -75,6 +75,38 @@ constexpr int kMaxPackRuns = fp::kMaxPackSamples + 2 * fp::kMaxPackImages;
 // Streams remembered per sample as its readers without growing host memory.
 constexpr size_t kReaders = 8;
 
+// Device scratch of pack_microbatch_noalloc: the staged run table of a pack
+// too large for its kernel arguments goes here instead of into a staging
+// buffer the pool allocates. One array per GPU, shared by every pool and
+// call on that GPU; each pool records its device's address of it at
+// creation. The largest run table (kMaxPackSamples lengths, kMaxPackRuns
+// runs, kBuckets bucket runs and entries) fits.
+constexpr size_t kScratchBytes = 64 << 10;
+static_assert(((4 * (size_t)fp::kMaxPackSamples + 15) & ~(size_t)15) + 16 * (size_t)kMaxPackRuns +
+                      18 * (size_t)fp::kBuckets <= kScratchBytes,
+              "the largest run table fits the scratch");
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+// Device address of `scratch` on a device, looked up once per device with the
+// device current (the array's name is a host-side stand-in; only this
+// address is valid on the GPU). Null and the HIP error on failure.
+uint8_t* scratch_address(int device, hipError_t* err) {
+  static std::mutex mu;
+  static std::unordered_map<int, uint8_t*> addr;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(device);
+  if (it != addr.end()) return it->second;
+  void* ptr = nullptr;
+  *err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (*err != hipSuccess || !ptr) return nullptr;
+  addr.emplace(device, (uint8_t*)ptr);
+  return (uint8_t*)ptr;
+}
+
 // Restores the caller's current device on scope exit.
 struct DeviceGuard {
   int prev = -1;
@@ -244,6 +276,7 @@ struct fp_pool {
   // staging
   Stage ring[kRing];
   int ring_next = 0;
+  uint8_t* scratch_dev = nullptr;     // this device's address of `scratch`
   fp::Divisors dv{};                  // division constants of the row, page and GVA sizes
   // Host arrays a pack builds its run table in, sized at creation for the
   // largest pack (kMaxPackSamples samples, kMaxPackRuns runs), so a pack
@@ -711,6 +744,11 @@ fp_status pool_create(const fp_pool_config* cfg_in, fp_pool** out) {
       Stage* sg = nullptr;
       fp_status ss = stage_acquire(p, kStageHostMin, 0, &sg);
       if (ss != FP_OK) return ss;
+    }
+    {
+      hipError_t se = hipSuccess;
+      p->scratch_dev = scratch_address(c.device, &se);     // the device is current here
+      if (!p->scratch_dev) return fail(FP_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(se));
     }
     p->pk_recs.resize(fp::kMaxPackSamples);
     p->pk_lens.resize(fp::kMaxPackSamples);
@@ -1554,6 +1592,17 @@ fp_status pack_microbatch(fp_pool* p, const uint64_t* sample_ids, int32_t n, con
   return guarded([&]() -> fp_status {
     return pack_impl(p, sample_ids, n, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens, out_position_ids,
                      out_n_tokens, out_max_seqlen, tier_mask, stream, nullptr, 0);
+  });
+}
+
+fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_t n, const void* embed_table,
+                                  int64_t vocab, void* out_emb, int64_t out_rows_cap, int32_t* out_cu_seqlens,
+                                  int32_t* out_position_ids, int32_t* out_n_tokens, int32_t* out_max_seqlen,
+                                  int32_t tier_mask, void* stream) {
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    return pack_impl(p, sample_ids, n, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens, out_position_ids,
+                     out_n_tokens, out_max_seqlen, tier_mask, stream, p->scratch_dev, kScratchBytes);
   });
 }
 

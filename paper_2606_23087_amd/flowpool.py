@@ -88,6 +88,8 @@ _SIGS = {
                                    _i32p]),
     "pack_microbatch": (C.c_int32, [_P, _u64p, C.c_int32, _P, C.c_int64, _P, C.c_int64, _P, _P,
                                     _i32p, _i32p, C.c_int32, _P]),
+    "pack_microbatch_noalloc": (C.c_int32, [_P, _u64p, C.c_int32, _P, C.c_int64, _P, C.c_int64, _P, _P,
+                                    _i32p, _i32p, C.c_int32, _P]),
     "pool_stats": (C.c_int32, [_P, _i64p, _i64p, _i64p]),
     "pool_sample_pages": (C.c_int32, [_P, C.c_uint64, _u64p, C.c_int32, _i32p]),
     "pool_sample_info": (C.c_int32, [_P, C.c_uint64, _i32p, _i32p, _i32p]),
@@ -347,7 +349,7 @@ def plan_pool_packing(pool: int, sample_ids, capacity: int, n_ranks: int, n_buck
 
 def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out_rows_cap: int,
                     out_cu_seqlens=None, out_position_ids=None, tier_mask: int = FP_TIER_MASK_ALL,
-                    stream=None):
+                    stream=None, _entry=None):
     """Enqueue the pack of ``sample_ids`` into ``out_emb``. Returns (n_tokens, max_seqlen)."""
     ids, idp = _arr(sample_ids, np.uint64, _u64p)
     n_tok = C.c_int32()
@@ -355,12 +357,21 @@ def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out
     rb = 2 * _HIDDEN.get(pool, 0)
     cap = max(int(out_rows_cap), 0)
     dev = _DEVICE.get(pool)
-    _check(_lib.pack_microbatch(pool, idp, len(ids), _buf(embed_table, max(int(vocab), 0) * rb, "embed_table", dev),
-                                vocab, _buf(out_emb, cap * rb, "out_emb", dev), out_rows_cap,
-                                _buf(out_cu_seqlens, 4 * (len(ids) + 1), "out_cu_seqlens", dev),
-                                _buf(out_position_ids, 4 * cap, "out_position_ids", dev), C.byref(n_tok), C.byref(mx),
-                                tier_mask, _stream(stream)), "pack_microbatch")
+    entry = _lib.pack_microbatch if _entry is None else _entry
+    _check(entry(pool, idp, len(ids), _buf(embed_table, max(int(vocab), 0) * rb, "embed_table", dev),
+                 vocab, _buf(out_emb, cap * rb, "out_emb", dev), out_rows_cap,
+                 _buf(out_cu_seqlens, 4 * (len(ids) + 1), "out_cu_seqlens", dev),
+                 _buf(out_position_ids, 4 * cap, "out_position_ids", dev), C.byref(n_tok), C.byref(mx),
+                 tier_mask, _stream(stream)), entry.__name__)
     return int(n_tok.value), int(mx.value)
+
+
+def pack_microbatch_noalloc(pool: int, sample_ids, embed_table, vocab: int, out_emb, out_rows_cap: int,
+                            out_cu_seqlens=None, out_position_ids=None, tier_mask: int = FP_TIER_MASK_ALL,
+                            stream=None):
+    """pack_microbatch through the entry point that allocates nothing. Returns (n_tokens, max_seqlen)."""
+    return pack_microbatch(pool, sample_ids, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens,
+                           out_position_ids, tier_mask, stream, _entry=_lib.pack_microbatch_noalloc)
 
 
 def pool_stats(pool: int):
