@@ -2,8 +2,7 @@
 benchmark times (same pool, same pack entry point, a non-default stream,
 rotating output buffers).
 
-The oracle cannot materialise every byte here, so each microbatch is checked
-by properties that hold at any size plus sampled rows:
+Every microbatch is checked by properties that hold at any size:
 - the plan (assignment, tokens, cost per microbatch) equals the oracle's;
 - every sample's page GVAs equal the oracle pool's (same churn history);
 - cu_seqlens and position ids equal the oracle's, in full;
@@ -11,6 +10,11 @@ by properties that hold at any size plus sampled rows:
   layout gives (sample, visual index or text id);
 - sampled rows (first, last, and random ones) equal, in all H words, the
   input row the oracle names for them.
+Two whole microbatches per workload, the first and the one with the most
+tokens, are compared element by element with the oracle pool's pack: their
+samples' visual rows (and the table rows their text names) are copied from
+the seeded generators to the host and written into the oracle pool, which
+packs them through its own page table.
 """
 
 import numpy as np
@@ -58,12 +62,22 @@ def test_full_size(fp, name):
     say(f"full-size {name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}")
     w = GpuWorkload(cfg, seed, mode="tagged", log=say)
     try:
-        say(f"  {len(w.ids)} samples written; replaying in the oracle pool")
-        opool, oids = oracle_pool_for(cfg, seed, w.specs, None, with_bytes=False)
+        assign, tok, cst, mem = oracle_plan(cfg, w.specs)
+        whole = sorted({0, int(np.argmax(tok))})          # microbatches compared element by element
+        members = {i for j in whole for i in mem[j]}
+        say(f"  {len(w.ids)} samples written; replaying in the oracle pool, with the rows of microbatches "
+            f"{whole} ({len(members)} samples)")
+        vis_np = [to_host(vis_rows(cfg, seed, i, s.n_vis, "tagged")) if i in members and s.n_vis else None
+                  for i, s in enumerate(w.specs)]
+        opool, oids = oracle_pool_for(cfg, seed, w.specs, vis_np, with_bytes=True)
+        del vis_np
         for gid, oid in zip(w.ids, oids):
             assert fp.pool_sample_pages(w.pool, gid).tolist() == opool.sample_pages(oid)
+        text_ids = np.unique(np.concatenate([w.specs[i].text_ids for i in members] + [np.zeros(0, np.int32)]))
+        host_table = np.zeros((cfg.vocab, cfg.hidden), np.uint16)     # only the named rows are filled
+        if text_ids.size:
+            host_table[text_ids] = to_host(w.table[torch.from_numpy(text_ids.astype(np.int64)).cuda()])
         plan = w.plan()
-        assign, tok, cst, mem = oracle_plan(cfg, w.specs)
         assert plan["assign"].tolist() == assign
         assert plan["mb_tokens"].tolist() == tok and plan["mb_cost_scaled"].tolist() == cst
         mbs = w.microbatches(plan)
@@ -71,7 +85,6 @@ def test_full_size(fp, name):
         stream = torch.cuda.Stream()
         outs = [w.alloc_outputs() for _ in range(4)]
         rng = np.random.default_rng(11)
-        host_table = None
         for j, idx in enumerate(mem):
             out, cu, pos = outs[j % 4]
             n, mx = w.pack([w.ids[i] for i in idx], out, cu, pos, stream=stream)
@@ -97,6 +110,16 @@ def test_full_size(fp, name):
                         vis_cache[g] = vis_rows(cfg, seed, g, w.specs[g].n_vis, "tagged")
                     want = to_host(vis_cache[g][x])
                 assert np.array_equal(to_host(out[r]), want), f"microbatch {j} row {r} ({kind})"
+            if j in whole:
+                rows_o, cu_o, pos_o, n_o, mx_o = opool.pack([oids[i] for i in idx], host_table)
+                assert (n_o, mx_o) == (n, mx)
+                got = to_host(out[:n])
+                bad = np.nonzero(np.any(got != rows_o, axis=1))[0]
+                assert bad.size == 0, f"microbatch {j}: {bad.size} of {n} rows differ from the oracle, first {bad[:5]}"
+                assert cu[:len(idx) + 1].cpu().numpy().tolist() == cu_o.tolist()
+                assert np.array_equal(pos[:n].cpu().numpy(), pos_o)
+                say(f"  microbatch {j}: all {n} x {cfg.hidden} words equal the oracle pool's pack")
+                del got, rows_o
         say(f"  {len(mem)} microbatches checked")
         if cfg.host_pages:
             say("  tier-mask split at full size")

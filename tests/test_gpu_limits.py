@@ -7,9 +7,11 @@ them (Sec. 3.1 consumer pack; the limits are the library's own):
 - the most samples (1024) and the most images (1024) in one microbatch.
 
 The oracle's layout names the source of every row of the large pack: the
-tag words of every row, all cu_seqlens and position ids, and sampled whole
-rows (both ends, the shrinking tail chunks, random ones) are checked, and the
-guard rows past the microbatch must be untouched.
+tag words of every row, all cu_seqlens and position ids, sampled whole rows
+(both ends, the shrinking tail chunks, random ones), and then every word of
+every row, slice by slice, against the rows the generators wrote (the host
+twin of the device pattern and the host table) are checked, and the guard
+rows past the microbatch must be untouched.
 Bar: bit-exact.
 """
 
@@ -19,7 +21,7 @@ import pytest
 from gpu_common import say, to_dev, to_host
 from oracle.pack import definitional_pack, row_sources
 from paper_2606_23087_amd.workloads import TAG_TEXT, TAG_VIS, SampleSpec
-from tagging import pattern_base, pattern_row, pattern_rows_dev, tagged_table, tagged_vis
+from tagging import PATTERN_BASE_ROWS, pattern_base, pattern_row, pattern_rows_dev, tagged_table, tagged_vis
 
 pytestmark = pytest.mark.gpu
 
@@ -95,6 +97,24 @@ def test_largest_microbatch(fp):
             kind, g, x = src[r]
             want = table_np[x] if kind == "text" else pattern_row(g, x, H, SEED, base)
             assert np.array_equal(to_host(out[r]), want), f"row {r} ({kind})"
+        say("  every word of every row, in slices of 65536 rows")
+        g = np.fromiter((s for _, s, _ in src), np.int64, m)
+        x = np.fromiter((v for _, _, v in src), np.int64, m)
+        for a in range(0, m, 1 << 16):
+            b = min(a + (1 << 16), m)
+            want = np.empty((b - a, H), np.uint16)
+            t = text[a:b]
+            want[t] = table_np[x[a:b][t]]
+            gv, xv = g[a:b][~t], x[a:b][~t]
+            rows = base[(7 * xv + gv) % PATTERN_BASE_ROWS]
+            rows[:, 0] = TAG_VIS
+            rows[:, 1] = gv & 0xFFFF
+            rows[:, 2] = xv & 0xFFFF
+            rows[:, 3] = (xv >> 16) & 0xFFFF
+            want[~t] = rows
+            got = to_host(out[a:b])
+            assert np.array_equal(got, want), f"rows {a}..{b}: first differing row " \
+                f"{a + int(np.nonzero(np.any(got != want, axis=1))[0][0])}"
         say("  one row more, or one visual row more in a write, is refused")
         extra = fp.pool_write_sample(pool, [3], [], [])
         before = fp.pool_stats(pool)
