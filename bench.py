@@ -188,30 +188,119 @@ def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
     t_all = timed([(fp.FP_TIER_MASK_ALL, stream)])
     hbm_bytes = 2 * (sum(tot_rows) - sum(host_rows)) * rb
     pcie_bytes = sum(host_rows) * rb
+    # Gather ceiling of the HBM-tier part: the same HBM-side rows (text rows
+    # and rows on HBM pages) gathered by the plain measurement kernel.
+    import numpy as np
+    lists = []
+    for mb in mbs:
+        a, t = row_sources(cfg, w, mb, spec_of, tiers=True)
+        lists.append(torch.from_numpy(a[t == 0].view(np.int64)).to("cuda"))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for rep in range(reps + 1):
+        if rep == 1:
+            e0.record(stream)
+        for j, lst in enumerate(lists):
+            fp.fp_gather_rows(lst, lst.numel(), rb, outs[j % len(outs)][0], stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_gather = e0.elapsed_time(e1) * 1e-3 / reps
+    del lists
     return {"host_tier_row_fraction": round(sum(host_rows) / sum(tot_rows), 4),
+            "text_row_fraction_of_hbm_part": round(sum(spec_of[x].n_text for mb in mbs for x in mb)
+                                                   / (sum(tot_rows) - sum(host_rows)), 4),
             "hbm_tier": {"GBps": round(hbm_bytes / t_hbm / 1e9, 1), "peak": HBM_PEAK_GBPS,
-                         "bytes": hbm_bytes, "ms": round(t_hbm * 1e3, 3)},
+                         "bytes": hbm_bytes, "ms": round(t_hbm * 1e3, 3),
+                         "gather_ceiling_GBps": round(hbm_bytes / t_gather / 1e9, 1),
+                         "gather_ceiling_ms": round(t_gather * 1e3, 3)},
             "host_tier": {"GBps": round(pcie_bytes / t_host / 1e9, 2), "peak": PCIE_PEAK_GBPS,
                           "bytes_over_pcie": pcie_bytes, "ms": round(t_host * 1e3, 3)},
             "both_masks_two_streams_ms": round(t_both * 1e3, 3),
             "one_full_pack_ms": round(t_all * 1e3, 3)}
 
 
-def d2d_ceiling(nbytes: int = 1 << 30, iters: int = 10) -> float:
+def row_sources(cfg, w, mb, spec_of, tiers=False):
+    """Device address of the source of every row of microbatch ``mb``, in
+    pack order (text rows: their table row; image rows: their row in the
+    physical page, from the pool's page table), for the gather ceiling; with
+    ``tiers``, also each row's tier (text rows count as HBM)."""
+    import numpy as np
+    from paper_2606_23087_amd import flowpool as fp
+    rb, P = cfg.row_bytes, cfg.page_tokens
+    table = np.uint64(w.table.data_ptr())
+    addr, tier = [], []
+    for sid in mb:
+        sp = spec_of[sid]
+        phys, ptier = [], []
+        for g in fp.pool_sample_pages(w.pool, sid).tolist():
+            t, a = fp.pool_translate(w.pool, int(g))
+            phys.append(a)
+            ptier.append(t)
+        phys = np.array(phys, np.uint64)
+        v = np.arange(sp.n_vis, dtype=np.uint64)
+        vis = phys[(v // np.uint64(P)).astype(np.int64)] + (v % np.uint64(P)) * np.uint64(rb) if sp.n_vis \
+            else np.zeros(0, np.uint64)
+        vtier = np.array(ptier, np.int8)[(np.arange(sp.n_vis) // P)] if sp.n_vis else np.zeros(0, np.int8)
+        text = table + sp.text_ids.astype(np.uint64) * np.uint64(rb)
+        ti = vi = 0
+        for p_, nt in zip(sp.img_pos.tolist(), sp.img_ntok.tolist()):
+            addr += [text[ti:p_], vis[vi:vi + nt]]
+            tier += [np.zeros(p_ - ti, np.int8), vtier[vi:vi + nt]]
+            ti, vi = p_, vi + nt
+        addr.append(text[ti:])
+        tier.append(np.zeros(sp.n_text - ti, np.int8))
+    a = np.concatenate(addr)
+    return (a, np.concatenate(tier)) if tiers else a
+
+
+def ceilings(cfg, w, mbs, spec_of, outs, stream, passes: int):
+    """Same-run ceilings for the pack of these microbatches, from the
+    library's measurement kernels (the pack's chunk geometry and cache
+    policy, nothing else):
+    - copy: one plain copy per microbatch, of its rows' bytes, from a 2 GiB
+      source walked forward (cache-cold) into the rotating output buffers;
+    - gather: each microbatch's rows gathered from the same source addresses
+      the pack reads (table rows and page rows), into the same buffers.
+    Each is timed like the pack: one event pair around all launches of
+    ``passes`` passes over the microbatches."""
+    import numpy as np
     import torch
-    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    b = torch.empty_like(a)
-    b.copy_(a)
+    from paper_2606_23087_amd import flowpool as fp
+    rb = cfg.row_bytes
+    rows = [sum(spec_of[x].length for x in mb) for mb in mbs]
+    src_lists = [torch.from_numpy(row_sources(cfg, w, mb, spec_of).view(np.int64)).to("cuda") for mb in mbs]
+    pool_bytes = 2 << 30
+    src = torch.empty(pool_bytes, dtype=torch.uint8, device="cuda")
+    offs, at = [], 0
+    for n in rows:
+        if at + n * rb > pool_bytes:
+            at = 0
+        offs.append(at)
+        at += n * rb
+
+    def run(kind: str) -> float:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for rep in range(passes + 1):
+            if rep == 1:
+                e0.record(stream)
+            for j, n in enumerate(rows):
+                out = outs[j % len(outs)][0]
+                if kind == "copy":
+                    fp.fp_copy_bytes(src.data_ptr() + offs[j], out, n * rb, rb, stream)
+                else:
+                    fp.fp_gather_rows(src_lists[j], n, rb, out, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / (passes * len(rows))
+
     torch.cuda.synchronize()
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s.record()
-    for _ in range(iters):
-        b.copy_(a)
-    e.record()
-    torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / iters
-    del a, b
-    return 2 * nbytes / (ms * 1e-3) / 1e9
+    t_copy = run("copy")
+    t_gather = run("gather")
+    mean_row_bytes = 2 * rb * float(np.mean(rows))
+    del src, src_lists
+    return {"what": "plain copy and plain gather of the same microbatch rows, library measurement kernels",
+            "copy_us": round(t_copy * 1e6, 3), "copy_GBps": round(mean_row_bytes / t_copy / 1e9, 1),
+            "gather_us": round(t_gather * 1e6, 3), "gather_GBps": round(mean_row_bytes / t_gather / 1e9, 1)}
 
 
 def h2d_ceiling(nbytes: int = 1 << 30, iters: int = 5) -> float:
@@ -521,7 +610,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen", choices=["tiny", "qwen", "frag70b", "video", "tiered"])
-    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--seed", type=int, default=0, help="seed of the --prefetch, --concurrent, --scheduler "
+                    "and --allocator legs")
+    ap.add_argument("--seeds", default="0,1,2", help="seeds whose workloads the timed steps cycle through")
     ap.add_argument("--buffers", type=int, default=4, help="rotating output buffers")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -561,11 +652,17 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = CONFIGS[args.workload]
-    t_setup = time.perf_counter()
-    log(f"workload {cfg.name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}")
-    w = GpuWorkload(cfg, args.seed, mode="normal", log=log)
-    log(f"pool built: {len(w.ids)} samples in {time.perf_counter() - t_setup:.1f} s, {fp.pool_stats(w.pool)}")
-    spec_of = {sid: s for sid, s in zip(w.ids, w.specs)}
+    seeds = [int(x) for x in str(args.seeds).split(",")] if not (args.prefetch or args.concurrent) else [args.seed]
+    log(f"workload {cfg.name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}, seeds {seeds}")
+    works = {}
+    for sd in seeds:
+        t_setup = time.perf_counter()
+        works[sd] = GpuWorkload(cfg, sd, mode="normal", log=log)
+        log(f"seed {sd}: pool built, {len(works[sd].ids)} samples in {time.perf_counter() - t_setup:.1f} s, "
+            f"{fp.pool_stats(works[sd].pool)}")
+    s0 = seeds[0]
+    w = works[s0]
+    spec_of = {sd: {sid: sp for sid, sp in zip(wk.ids, wk.specs)} for sd, wk in works.items()}
 
     if args.calibrate_copy:
         a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -580,34 +677,39 @@ def main() -> int:
     plan_stream = torch.cuda.Stream()
     outs = [w.alloc_outputs() for _ in range(max(1, args.buffers))]
 
-    region = {}
-
-    def one_step(events=None, mark_start=False):
-        plan = w.plan(stream=plan_stream)
-        mbs = w.microbatches(plan)
+    def one_step(sd, events=None, mark=None):
+        """Plan seed sd's resident samples, then pack every microbatch on the
+        pack stream; `mark` is recorded on the pack stream before the first pack."""
+        wk = works[sd]
+        plan = wk.plan(stream=plan_stream)
+        mbs = wk.microbatches(plan)
         for j, mb in enumerate(mbs):
             out, cu, pos = outs[j % len(outs)]
-            if j == 0 and mark_start:
-                region["start"].record(pack_stream)
+            if j == 0 and mark is not None:
+                mark.record(pack_stream)
             if events is not None:
                 events[j][0].record(pack_stream)
-            w.pack(mb, out, cu, pos, stream=pack_stream)
+            wk.pack(mb, out, cu, pos, stream=pack_stream)
             if events is not None:
                 events[j][1].record(pack_stream)
         return plan, mbs
 
-    plan, mbs = one_step()
-    step_bytes = sum(pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs)
-    step_tokens = int(plan["mb_tokens"].sum())
-    deferred = int((plan["assign"] < 0).sum())
-    for _ in range(args.warmup):
-        one_step()
+    info = {}
+    for sd in seeds:
+        plan, mbs = one_step(sd)
+        info[sd] = dict(plan=plan, mbs=mbs,
+                        mb_bytes=[pack_bytes(cfg, [spec_of[sd][x] for x in mb]) for mb in mbs],
+                        tokens=int(plan["mb_tokens"].sum()), deferred=int((plan["assign"] < 0).sum()))
+        info[sd]["step_bytes"] = sum(info[sd]["mb_bytes"])
+    for k in range(args.warmup):
+        one_step(seeds[k % len(seeds)])
     torch.cuda.synchronize()
-    log(f"warmup done: {len(mbs)} microbatches, {step_tokens} tokens, {step_bytes / 1e6:.1f} MB per step, "
-        f"{deferred} samples deferred")
+    plan, mbs = info[s0]["plan"], info[s0]["mbs"]
+    log(f"warmup done: seed {s0}: {len(mbs)} microbatches, {info[s0]['tokens']} tokens, "
+        f"{info[s0]['step_bytes'] / 1e6:.1f} MB per step, {info[s0]['deferred']} samples deferred")
 
     if args.prefetch:
-        res = prefetch_bench(args, cfg, w, mbs, spec_of, outs, pack_stream)
+        res = prefetch_bench(args, cfg, w, mbs, spec_of[s0], outs, pack_stream)
         print(json.dumps({
             "metric": "tiered pack: zero-copy host-tier reads vs host-tier pages promoted into HBM first",
             "value": res["pipelined_ms"], "unit": "ms per 16 microbatches (pipelined promote + pack)",
@@ -618,7 +720,7 @@ def main() -> int:
         return 0
 
     if args.concurrent:
-        res = concurrent_bench(args, cfg, w, mbs, spec_of, outs, pack_stream)
+        res = concurrent_bench(args, cfg, w, mbs, spec_of[s0], outs, pack_stream)
         print(json.dumps({
             "metric": "pack_microbatch GB/s with a concurrent producer writing on another stream",
             "value": res["pack_with_producer_GBps"], "unit": "GB/s", "higher_is_better": True,
@@ -629,33 +731,56 @@ def main() -> int:
         w.close()
         return 0 if res["producer_error"] is None else 1
 
-    # Timed region: K whole steps back to back. One event pair on the pack
-    # stream brackets every pack launch of the region (from the first pack of
-    # the first step to the last pack of the last step); the wall clock
-    # brackets the whole region, planning included.
-    n_packs = len(mbs)
-    region["start"] = torch.cuda.Event(enable_timing=True)
-    region["end"] = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    gc.collect()
-    gc.disable()          # no collector pauses between enqueues inside the timed region
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        one_step(mark_start=(k == 0))
-    region["end"].record(pack_stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gc.enable()
-    mb_bytes = np.array([pack_bytes(cfg, [spec_of[s] for s in mb]) for mb in mbs], dtype=np.float64)
-    launch_s = region["start"].elapsed_time(region["end"]) * 1e-3 / (args.steps * n_packs)
+    def timed(order):
+        """Whole steps for the seeds in `order`, back to back. Returns the wall
+        time, the pack-stream time from the first pack to the last, and the
+        launches, bytes and tokens. One event pair brackets all pack launches;
+        the wall clock brackets everything, planning included."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        gc.collect()
+        gc.disable()          # no collector pauses between enqueues inside the timed region
+        t0 = time.perf_counter()
+        for k, sd in enumerate(order):
+            one_step(sd, mark=e0 if k == 0 else None)
+        e1.record(pack_stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        gc.enable()
+        return dict(wall=wall, packs=e0.elapsed_time(e1) * 1e-3, launches=sum(len(info[sd]["mbs"]) for sd in order),
+                    bytes=sum(info[sd]["step_bytes"] for sd in order), tokens=sum(info[sd]["tokens"] for sd in order))
 
-    # Per-call spread, from one extra step with an event pair around every
-    # launch (outside the timed region: per-call event records perturb the
-    # stream they time).
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_packs)]
-    one_step(events)
+    # Timed region: K whole steps, the seeds' workloads in turn.
+    order = [seeds[k % len(seeds)] for k in range(args.steps)]
+    main_t = timed(order)
+    launch_s = main_t["packs"] / main_t["launches"]
+    mean_bytes = main_t["bytes"] / main_t["launches"]
+    kernel_gbps = mean_bytes / launch_s / 1e9
+    value = main_t["bytes"] / main_t["wall"] / 1e9
+
+    # Each seed alone, K steps, measured the same way (outside the timed region).
+    per_seed = []
+    for sd in seeds:
+        t = timed([sd] * args.steps)
+        g = t["bytes"] / t["packs"] / 1e9
+        per_seed.append({"seed": sd, "samples": len(works[sd].ids), "step_bytes": info[sd]["step_bytes"],
+                         "deferred_samples": info[sd]["deferred"],
+                         "mean_us": round(t["packs"] / t["launches"] * 1e6, 3), "GBps": round(g, 2),
+                         "frac": round(g / HBM_PEAK_GBPS, 4), "step_GBps": round(t["bytes"] / t["wall"] / 1e9, 2)})
+        log(f"seed {sd}: {per_seed[-1]}")
+
+    # Per-call spread, from one extra step of the first seed with an event
+    # pair around every launch (per-call event records perturb the stream
+    # they time: each launch reads about 1.5 us longer than back to back).
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(len(mbs))]
+    one_step(s0, events)
     torch.cuda.synchronize()
     durs = np.array([s_.elapsed_time(e_) * 1e-3 for s_, e_ in events])   # seconds
+
+    ceiling = ceilings(cfg, w, mbs, spec_of[s0], outs, pack_stream, args.steps)
+    pack_s0 = [x for x in per_seed if x["seed"] == s0][0]
+    ceiling["pack_over_gather"] = round(ceiling["gather_us"] / pack_s0["mean_us"], 4)
+    ceiling["pack_over_copy"] = round(ceiling["copy_us"] / pack_s0["mean_us"], 4)
 
     graph_s = None
     graph2_s = None
@@ -699,11 +824,9 @@ def main() -> int:
         graph2_s = replay_s(2)
         del gouts
 
-    value = step_bytes * args.steps / wall / 1e9
-    kernel_gbps = float(mb_bytes.mean()) / launch_s / 1e9
-    per_call = mb_bytes / durs / 1e9
+    per_call = np.array(info[s0]["mb_bytes"], dtype=np.float64) / durs / 1e9
     traffic = counter_traffic(cfg.name)
-    mean_bytes = float(mb_bytes.mean())
+    fracs = [x["frac"] for x in per_seed]
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -711,7 +834,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "ms_per_step": round(main_t["wall"] / args.steps * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -719,14 +842,15 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}-h{cfg.hidden}", "hidden": cfg.hidden, "page_tokens": cfg.page_tokens,
                    "pool_pages": cfg.hbm_pages + cfg.host_pages, "alloc": cfg.alloc, "capacity": cfg.capacity,
-                   "n_mb": cfg.n_mb, "cost_k": cfg.cost_k, "samples": len(w.ids), "seed": args.seed,
-                   "parallelism": "none (1 GPU)"},
+                   "n_mb": cfg.n_mb, "cost_k": cfg.cost_k, "samples": len(w.ids),
+                   "seeds": seeds, "steps_cycle_seeds": True, "parallelism": "none (1 GPU)"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "tokens_per_s": round(step_tokens * args.steps / wall, 1),
-        "step_tokens": step_tokens,
-        "step_bytes": step_bytes,
-        "deferred_samples": deferred,
-        "pack_kernel": {"launches": args.steps * n_packs, "mean_us": round(launch_s * 1e6, 3),
+        "tokens_per_s": round(main_t["tokens"] / main_t["wall"], 1),
+        "step_tokens": info[s0]["tokens"],
+        "step_bytes": info[s0]["step_bytes"],
+        "deferred_samples": info[s0]["deferred"],
+        "pack_kernel": {"launches": main_t["launches"], "mean_us": round(launch_s * 1e6, 3),
+                        "mean_bytes": round(mean_bytes),
                         "timing": "pack-stream event pair around all launches of the timed steps",
                         "GBps": round(kernel_gbps, 2),
                         "single_call_events_us_p10_p50_p90_max": [round(float(np.percentile(durs, q)) * 1e6, 2)
@@ -736,27 +860,32 @@ def main() -> int:
                      "frac": round(kernel_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": (round(traffic) if traffic else None),
                      "traffic_over_algorithmic": (round(traffic / mean_bytes, 4) if traffic else None)},
+        "per_seed": per_seed,
+        "median_over_seeds": {"frac": float(np.median(fracs)),
+                              "GBps": float(np.median([x["GBps"] for x in per_seed])),
+                              "mean_us": float(np.median([x["mean_us"] for x in per_seed]))},
+        "ceiling": ceiling,
     }
     if graph_s is not None:
+        step_bytes = info[s0]["step_bytes"]
         result["graph_pack_two_chains"] = {"replay_ms": round(graph2_s * 1e3, 4),
                                            "GBps": round(step_bytes / graph2_s / 1e9, 2)}
-        result["graph_pack"] = {"packs_per_replay": n_packs, "replay_ms": round(graph_s * 1e3, 4),
-                                "GBps": round(step_bytes / graph_s / 1e9, 2),
-                                "per_call_GBps_same_packs": round(step_bytes / (launch_s * n_packs) / 1e9, 2)}
+        result["graph_pack"] = {"packs_per_replay": len(mbs), "replay_ms": round(graph_s * 1e3, 4),
+                                "GBps": round(step_bytes / graph_s / 1e9, 2)}
     imb = plan["mb_cost_scaled"].max() / plan["mb_cost_scaled"].mean()
     result["plan"] = {"max_over_mean_cost": round(float(imb), 5),
                       "eq3_max": round(float(max((t / cfg.capacity) + (m / cfg.capacity) ** 2
                                                  for t, m in zip(plan["mb_tokens"], plan["mb_max_len"]))), 5)}
     if cfg.host_pages:
-        result["tiers"] = tier_split(cfg, w, mbs, spec_of, outs, pack_stream)
+        result["tiers"] = tier_split(cfg, w, mbs, spec_of[s0], outs, pack_stream)
         result["tiers"]["h2d_copy_GBps"] = round(h2d_ceiling(), 1)
-    result["d2d_copy_ceiling_GBps"] = round(d2d_ceiling(), 1)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
-        result["cpu_baseline"] = cpu_baseline(cfg, w, mbs, args.seed, args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(cfg, w, mbs, s0, args.cpu_budget)
     else:
         result["cpu_baseline"] = None
-    w.close()
+    for wk in works.values():
+        wk.close()
     print(json.dumps(result), flush=True)
     return 0
 

@@ -432,6 +432,27 @@ fp_status pool_translate(const fp_pool* p, uint64_t gva, int32_t* tier, uint64_t
 fp_status pool_layout(const fp_pool* p, uint64_t* region_start, uint64_t* segment_start,
                       int64_t* page_bytes);
 
+/* Measurement aids (not steps of the method): plain kernels with the
+ * pack's chunk geometry (chunks of 256 threads x 3 vectors of 16 bytes, or 2
+ * for rows of 10 KiB or more, sized for the current device's compute units,
+ * with the same shrinking tail chunks) and its load and store cache policy,
+ * which move the bytes a pack moves and do nothing else, so a pack can be
+ * timed against them in the same run. Asynchronous on `stream`, on the
+ * calling thread's current device.
+ *
+ * fp_copy_bytes: copies `bytes` (a multiple of 16, at most (2^31 - 1024) * 16)
+ * from device src to device dst, both 16-byte aligned, non-overlapping;
+ * row_bytes (a multiple of 16) selects the chunk size a pack of such rows
+ * uses. Errors: EINVAL, EALIGN, EHIP. */
+fp_status fp_copy_bytes(const void* src, void* dst, int64_t bytes, int32_t row_bytes, void* stream);
+
+/* fp_gather_rows: output row r (row_bytes bytes, a multiple of 16) of dst
+ * (device, 16-byte aligned, n_rows * row_bytes bytes) is a copy of the
+ * row_bytes bytes at address rows_src[r]; rows_src is a device uint64[n_rows]
+ * of device-readable, 16-byte aligned addresses, which the call does not
+ * check (an invalid one faults the GPU). Errors: EINVAL, EALIGN, EHIP. */
+fp_status fp_gather_rows(const uint64_t* rows_src, int32_t n_rows, int32_t row_bytes, void* dst, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

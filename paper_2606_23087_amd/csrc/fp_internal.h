@@ -157,6 +157,13 @@ Divisors make_divisors(int64_t row_bytes, int64_t page_tokens, uint64_t page_byt
 void pack_chunks(PackPlan* pl, int n_cu);
 hipError_t launch_pack(const PackPlan& pl, hipStream_t stream);
 hipError_t launch_write(const WriteArgs& a, hipStream_t stream);
+// Measurement aids with the pack's geometry: a plain copy of `vecs` 16-byte
+// vectors (chunks sized as for rows of row_bytes), and a gather of n_rows
+// rows of row_bytes from the device addresses rows_src[] into consecutive
+// rows of dst.
+hipError_t launch_copy(const void* src, void* dst, int64_t vecs, int64_t row_bytes, int n_cu, hipStream_t stream);
+hipError_t launch_gather(const uint64_t* rows_src, int32_t n_rows, int64_t row_bytes, void* dst, int n_cu,
+                         hipStream_t stream);
 hipError_t launch_cost(const SampleDesc* desc, const int32_t* slots, int32_t n, int64_t k,
                        int64_t* out_cost, hipStream_t stream);
 

@@ -398,10 +398,11 @@ __global__ __launch_bounds__(kBlock) void k_cost(const SampleDesc* __restrict__ 
 
 size_t pack_lds_bytes(const PackPlan& pl) { return sizeof(uint64_t) * (size_t)std::max(pl.max_chunk_rows, 1); }
 
-void pack_chunks(PackPlan* pl, int n_cu) {
-  pl->vpt = pl->a.row_bytes >= kSmallChunkRowBytes ? 2 : kVecsPerThread;
+// Chunk geometry over `vecs` vectors: full chunks of kPackBlock * vpt
+// vectors, then a wave of resident workgroups (CUs x kPackPerCU) of
+// kTail1Vecs, then half a wave of kTail2Vecs.
+static void chunk_geometry(int64_t vecs, int n_cu, PackPlan* pl) {
   const int64_t chunk = (int64_t)kPackBlock * pl->vpt;
-  const int64_t vecs = (int64_t)pl->a.n_tokens * (pl->a.row_bytes >> 4);
   const int64_t wave = (int64_t)std::max(n_cu, 1) * kPackPerCU;
   const int64_t t2 = std::max<int64_t>(vecs - (wave / 2) * kTail2Vecs, 0);
   const int64_t t1 = (std::max<int64_t>(t2 - wave * kTail1Vecs, 0) / chunk) * chunk;
@@ -409,6 +410,13 @@ void pack_chunks(PackPlan* pl, int n_cu) {
   pl->g1 = (int32_t)(pl->g0 + (t2 - t1 + kTail1Vecs - 1) / kTail1Vecs);
   pl->t1 = (int32_t)t1;
   pl->t2 = (int32_t)t2;
+}
+
+static int vectors_per_thread(int64_t row_bytes) { return row_bytes >= kSmallChunkRowBytes ? 2 : kVecsPerThread; }
+
+void pack_chunks(PackPlan* pl, int n_cu) {
+  pl->vpt = vectors_per_thread(pl->a.row_bytes);
+  chunk_geometry((int64_t)pl->a.n_tokens * (pl->a.row_bytes >> 4), n_cu, pl);
 }
 
 template <int VPT>
@@ -425,6 +433,134 @@ hipError_t launch_pack(const PackPlan& pl, hipStream_t stream) {
   const int32_t total = (int32_t)vecs;               // the host keeps this below 2^31
   if (pl.vpt == 2) launch_pack_as<2>(pl, grid, total, stream);
   else launch_pack_as<kVecsPerThread>(pl, grid, total, stream);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Measurement aids, not steps of the method: a plain copy, and a plain gather
+// of rows from given addresses into consecutive output rows, with the pack's
+// chunk geometry (chunks of 256 threads x VPT vectors, the same shrinking
+// tail stages) and its load and store cache policy. They move the bytes a
+// pack moves and do nothing else, so the pack can be timed against them in
+// the same run.
+
+template <int VPT>
+__device__ __forceinline__ void chunk_range(int32_t g0, int32_t g1, int32_t t1, int32_t t2, int32_t total, int* v0,
+                                            int* v1) {
+  constexpr int kChunk = kPackBlock * VPT;
+  const int bx = (int)blockIdx.x;
+  if (bx < g0) {
+    *v0 = bx * kChunk;
+    *v1 = *v0 + kChunk;
+  } else if (bx < g1) {
+    *v0 = t1 + (bx - g0) * kTail1Vecs;
+    *v1 = min(*v0 + kTail1Vecs, t2);
+  } else {
+    *v0 = t2 + (bx - g1) * kTail2Vecs;
+    *v1 = min(*v0 + kTail2Vecs, total);
+  }
+}
+
+template <int VPT>
+__global__ __launch_bounds__(kPackBlock) void k_copy(int32_t g0, int32_t g1, int32_t t1, int32_t t2, int32_t total,
+                                                      const uint8_t* src, uint8_t* dst) {
+  int v0, v1;
+  chunk_range<VPT>(g0, g1, t1, t2, total, &v0, &v1);
+  u32x4 v[VPT];
+  if (v1 - v0 == kPackBlock * VPT) {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) v[u] = load16(src + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16);
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int e = v0 + u * kPackBlock + (int)threadIdx.x;
+      if (e < v1) v[u] = load16(src + (size_t)e * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int e = v0 + u * kPackBlock + (int)threadIdx.x;
+      if (e < v1) store16(dst + (size_t)e * 16, v[u]);
+    }
+  }
+}
+
+// Output row r is the row_bytes bytes at address rows_src[r].
+template <int VPT>
+__global__ __launch_bounds__(kPackBlock) void k_gather(int32_t g0, int32_t g1, int32_t t1, int32_t t2, int32_t total,
+                                                        uint64_t div_mul, int32_t div_shift, int32_t row_bytes,
+                                                        const uint64_t* rows_src, uint8_t* dst) {
+  extern __shared__ __align__(16) uint64_t s_src[];
+  int v0, v1;
+  chunk_range<VPT>(g0, g1, t1, t2, total, &v0, &v1);
+  auto div_row = [&](int e) { return (int)(((uint64_t)(uint32_t)e * div_mul) >> div_shift); };
+  const int vpr = row_bytes >> 4;
+  const int r0 = div_row(v0);
+  const int rows = v1 > v0 ? div_row(v1 - 1) - r0 + 1 : 0;
+  for (int t = threadIdx.x; t < rows; t += kPackBlock) s_src[t] = rows_src[r0 + t];
+  __syncthreads();
+  u32x4 v[VPT];
+  uint64_t from[VPT];
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int e = v0 + u * kPackBlock + (int)threadIdx.x;
+    from[u] = 0;
+    if (e < v1) {
+      const int row = div_row(e);
+      from[u] = s_src[row - r0] + (uint64_t)(e - row * vpr) * 16;
+    }
+  }
+  if (v1 - v0 == kPackBlock * VPT) {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u)
+      if (from[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
+#pragma unroll
+    for (int u = 0; u < VPT; ++u)
+      if (from[u]) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
+  }
+}
+
+// The pack's chunk geometry for `vecs` vectors of rows of row_bytes bytes.
+static void plain_geometry(int64_t vecs, int64_t row_bytes, int n_cu, PackPlan* pl) {
+  pl->vpt = vectors_per_thread(row_bytes);
+  chunk_geometry(vecs, n_cu, pl);
+}
+
+hipError_t launch_copy(const void* src, void* dst, int64_t vecs, int64_t row_bytes, int n_cu, hipStream_t stream) {
+  if (vecs <= 0) return hipSuccess;
+  PackPlan pl{};
+  plain_geometry(vecs, row_bytes, n_cu, &pl);
+  const int grid = (int)(pl.g1 + (vecs - pl.t2 + kTail2Vecs - 1) / kTail2Vecs);
+  if (pl.vpt == 2)
+    hipLaunchKernelGGL(k_copy<2>, dim3(grid), dim3(kPackBlock), 0, stream, pl.g0, pl.g1, pl.t1, pl.t2, (int32_t)vecs,
+                       (const uint8_t*)src, (uint8_t*)dst);
+  else
+    hipLaunchKernelGGL(k_copy<kVecsPerThread>, dim3(grid), dim3(kPackBlock), 0, stream, pl.g0, pl.g1, pl.t1, pl.t2,
+                       (int32_t)vecs, (const uint8_t*)src, (uint8_t*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const uint64_t* rows_src, int32_t n_rows, int64_t row_bytes, void* dst, int n_cu,
+                         hipStream_t stream) {
+  if (n_rows <= 0) return hipSuccess;
+  const int64_t vecs = (int64_t)n_rows * (row_bytes >> 4);
+  PackPlan pl{};
+  plain_geometry(vecs, row_bytes, n_cu, &pl);
+  const Divisors dv = make_divisors(row_bytes, 1, 16);
+  const int grid = (int)(pl.g1 + (vecs - pl.t2 + kTail2Vecs - 1) / kTail2Vecs);
+  const size_t lds = sizeof(uint64_t) * (size_t)std::min<int64_t>(n_rows, kChunkVecs / (row_bytes >> 4) + 2);
+  if (pl.vpt == 2)
+    hipLaunchKernelGGL(k_gather<2>, dim3(grid), dim3(kPackBlock), lds, stream, pl.g0, pl.g1, pl.t1, pl.t2,
+                       (int32_t)vecs, dv.div_mul, dv.div_shift, (int32_t)row_bytes, rows_src, (uint8_t*)dst);
+  else
+    hipLaunchKernelGGL(k_gather<kVecsPerThread>, dim3(grid), dim3(kPackBlock), lds, stream, pl.g0, pl.g1, pl.t1,
+                       pl.t2, (int32_t)vecs, dv.div_mul, dv.div_shift, (int32_t)row_bytes, rows_src, (uint8_t*)dst);
   return hipGetLastError();
 }
 

@@ -1626,6 +1626,42 @@ fp_status pool_release_captured(fp_pool* p, const uint64_t* sample_ids, int32_t 
   });
 }
 
+// Compute units of the calling thread's current device.
+static fp_status current_cus(int* n_cu) {
+  int dev = 0;
+  FP_HIP(hipGetDevice(&dev));
+  FP_HIP(hipDeviceGetAttribute(n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+  return FP_OK;
+}
+
+fp_status fp_copy_bytes(const void* src, void* dst, int64_t bytes, int32_t row_bytes, void* stream) {
+  return guarded([&]() -> fp_status {
+    if (bytes < 0 || bytes % 16 || bytes / 16 > kMaxVectors) return fail(FP_EINVAL, "bytes %lld", (long long)bytes);
+    if (row_bytes < 16 || row_bytes % 16) return fail(FP_EINVAL, "row_bytes %d", row_bytes);
+    if (bytes && (!src || !dst)) return fail(FP_EINVAL, "null buffer");
+    if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) return fail(FP_EALIGN, "src/dst must be 16-byte aligned");
+    int n_cu = 0;
+    fp_status st = current_cus(&n_cu);
+    if (st != FP_OK) return st;
+    FP_HIP(fp::launch_copy(src, dst, bytes / 16, row_bytes, n_cu, (hipStream_t)stream));
+    return FP_OK;
+  });
+}
+
+fp_status fp_gather_rows(const uint64_t* rows_src, int32_t n_rows, int32_t row_bytes, void* dst, void* stream) {
+  return guarded([&]() -> fp_status {
+    if (n_rows < 0 || row_bytes < 16 || row_bytes % 16 || (int64_t)n_rows * (row_bytes / 16) > kMaxVectors)
+      return fail(FP_EINVAL, "n_rows %d, row_bytes %d", n_rows, row_bytes);
+    if (n_rows && (!rows_src || !dst)) return fail(FP_EINVAL, "null buffer");
+    if ((uintptr_t)rows_src % 8 || (uintptr_t)dst % 16) return fail(FP_EALIGN, "rows_src/dst alignment");
+    int n_cu = 0;
+    fp_status st = current_cus(&n_cu);
+    if (st != FP_OK) return st;
+    FP_HIP(fp::launch_gather(rows_src, n_rows, row_bytes, dst, n_cu, (hipStream_t)stream));
+    return FP_OK;
+  });
+}
+
 fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages, int64_t* n_samples) {
   if (!p) return fail(FP_EINVAL, "null pool");
   fp_pool* q = const_cast<fp_pool*>(p);

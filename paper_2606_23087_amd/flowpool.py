@@ -97,6 +97,8 @@ _SIGS = {
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
     "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
     "pool_release_captured": (C.c_int32, [_P, _u64p, C.c_int32]),
+    "fp_copy_bytes": (C.c_int32, [_P, _P, C.c_int64, C.c_int32, _P]),
+    "fp_gather_rows": (C.c_int32, [_P, C.c_int32, C.c_int32, _P, _P]),
     "pool_migrate": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, _P, _i64p]),
     "alloc_candidates": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _i32p, _i32p, _i32p,
                                      C.c_int32, _i32p]),
@@ -372,6 +374,18 @@ def pack_microbatch_noalloc(pool: int, sample_ids, embed_table, vocab: int, out_
     """pack_microbatch through the entry point that allocates nothing. Returns (n_tokens, max_seqlen)."""
     return pack_microbatch(pool, sample_ids, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens,
                            out_position_ids, tier_mask, stream, _entry=_lib.pack_microbatch_noalloc)
+
+
+def fp_copy_bytes(src, dst, nbytes: int, row_bytes: int, stream=None) -> None:
+    """Measurement aid: plain copy of ``nbytes`` from device ``src`` to ``dst`` with the pack's geometry."""
+    _check(_lib.fp_copy_bytes(_buf(src, nbytes, "src", None), _buf(dst, nbytes, "dst", None), nbytes, row_bytes,
+                              _stream(stream)), "fp_copy_bytes")
+
+
+def fp_gather_rows(rows_src, n_rows: int, row_bytes: int, dst, stream=None) -> None:
+    """Measurement aid: dst row r = the row at device address rows_src[r] (a device int64 tensor)."""
+    _check(_lib.fp_gather_rows(_buf(rows_src, 8 * n_rows, "rows_src", None), n_rows, row_bytes,
+                               _buf(dst, n_rows * row_bytes, "dst", None), _stream(stream)), "fp_gather_rows")
 
 
 def pool_stats(pool: int):

@@ -40,5 +40,11 @@ def test_json_line_fields():
     roof = d["roofline"]
     assert roof["bound"] == "hbm" and roof["unit"] == "GB/s" and roof["peak"] == 8000.0
     assert abs(roof["frac"] - roof["achieved"] / roof["peak"]) < 1e-3 and "traffic" in roof
+    seeds = [x["seed"] for x in d["per_seed"]]
+    assert seeds == [0, 1, 2] and d["config"]["seeds"] == [0, 1, 2]
+    assert all(x["frac"] > 0 and x["mean_us"] > 0 for x in d["per_seed"])
+    assert d["median_over_seeds"]["frac"] == sorted(x["frac"] for x in d["per_seed"])[1]
+    ce = d["ceiling"]
+    assert ce["copy_GBps"] > 0 and ce["gather_GBps"] > 0 and ce["pack_over_gather"] > 0
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] == 1 and cb["value"] > 0 and cb["unit"] and cb["sample"]
