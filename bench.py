@@ -59,6 +59,19 @@ def cpu_model_name() -> str:
     return platform.processor() or platform.machine()
 
 
+def masked_pack_bytes(cfg, w, mb, spec_of, mask: int) -> int:
+    """Algorithmic bytes of a tier-masked pack: the rows it copies, read once
+    and written once, plus (HBM mask) the metadata a full pack moves."""
+    from paper_2606_23087_amd import flowpool as fp
+    specs = [spec_of[x] for x in mb]
+    if mask == fp.FP_TIER_MASK_ALL:
+        return pack_bytes(cfg, specs)
+    _, tier = row_sources(cfg, w, mb, spec_of, tiers=True)
+    rows = int((tier == (1 if mask == fp.FP_TIER_MASK_HOST else 0)).sum())
+    meta = pack_bytes(cfg, specs) - 2 * sum(x.length for x in specs) * cfg.row_bytes
+    return 2 * rows * cfg.row_bytes + (meta if mask & fp.FP_TIER_MASK_HBM else 0)
+
+
 def pack_bytes(cfg, specs) -> int:
     rb = cfg.row_bytes
     tokens = sum(s.length for s in specs)
@@ -85,10 +98,12 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
-def counter_traffic(workload: str):
-    """HBM bytes per pack launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"pack_{workload}_counters.md")
+def counter_traffic(workload: str, mask: str = "all"):
+    """HBM bytes per pack launch from the committed rocprofv3 counter summary
+    of the workload (and tier mask), if it was taken on the current kernel
+    source; else None."""
+    name = workload if mask == "all" else f"{workload}_{mask}"
+    path = os.path.join(ROOT, "profiles", f"pack_{name}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -253,7 +268,7 @@ def row_sources(cfg, w, mb, spec_of, tiers=False):
     return (a, np.concatenate(tier)) if tiers else a
 
 
-def ceilings(cfg, w, mbs, spec_of, outs, stream, passes: int):
+def ceilings(cfg, w, mbs, spec_of, outs, stream, passes: int, mask: int = 3):
     """Same-run ceilings for the pack of these microbatches, from the
     library's measurement kernels (the pack's chunk geometry and cache
     policy, nothing else):
@@ -262,14 +277,20 @@ def ceilings(cfg, w, mbs, spec_of, outs, stream, passes: int):
     - gather: each microbatch's rows gathered from the same source addresses
       the pack reads (table rows and page rows), into the same buffers.
     Each is timed like the pack: one event pair around all launches of
-    ``passes`` passes over the microbatches."""
+    ``passes`` passes over the microbatches. With a tier mask, only the rows
+    of that tier (text rows count as HBM)."""
     import numpy as np
     import torch
     from paper_2606_23087_amd import flowpool as fp
     rb = cfg.row_bytes
-    rows = [sum(spec_of[x].length for x in mb) for mb in mbs]
-    src_lists = [torch.from_numpy(row_sources(cfg, w, mb, spec_of).view(np.int64)).to("cuda") for mb in mbs]
-    pool_bytes = 2 << 30
+    src_lists = []
+    for mb in mbs:
+        a, t = row_sources(cfg, w, mb, spec_of, tiers=True)
+        if mask != fp.FP_TIER_MASK_ALL:
+            a = a[t == (1 if mask == fp.FP_TIER_MASK_HOST else 0)]
+        src_lists.append(torch.from_numpy(a.view(np.int64)).to("cuda"))
+    rows = [x.numel() for x in src_lists]
+    pool_bytes = max(2 << 30, max(rows) * rb)
     src = torch.empty(pool_bytes, dtype=torch.uint8, device="cuda")
     offs, at = [], 0
     for n in rows:
@@ -614,6 +635,8 @@ def main() -> int:
                     "and --allocator legs")
     ap.add_argument("--seeds", default="0,1,2", help="seeds whose workloads the timed steps cycle through")
     ap.add_argument("--buffers", type=int, default=4, help="rotating output buffers")
+    ap.add_argument("--mask", default="all", choices=["all", "hbm", "host"],
+                    help="tier mask of the timed packs (tiered pool: time one tier's part alone)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -676,6 +699,7 @@ def main() -> int:
     pack_stream = torch.cuda.Stream()
     plan_stream = torch.cuda.Stream()
     outs = [w.alloc_outputs() for _ in range(max(1, args.buffers))]
+    mask = {"all": fp.FP_TIER_MASK_ALL, "hbm": fp.FP_TIER_MASK_HBM, "host": fp.FP_TIER_MASK_HOST}[args.mask]
 
     def one_step(sd, events=None, mark=None):
         """Plan seed sd's resident samples, then pack every microbatch on the
@@ -689,7 +713,10 @@ def main() -> int:
                 mark.record(pack_stream)
             if events is not None:
                 events[j][0].record(pack_stream)
-            wk.pack(mb, out, cu, pos, stream=pack_stream)
+            if mask & fp.FP_TIER_MASK_HBM:
+                wk.pack(mb, out, cu, pos, tier_mask=mask, stream=pack_stream)
+            else:
+                wk.pack(mb, out, None, None, tier_mask=mask, stream=pack_stream)
             if events is not None:
                 events[j][1].record(pack_stream)
         return plan, mbs
@@ -698,7 +725,7 @@ def main() -> int:
     for sd in seeds:
         plan, mbs = one_step(sd)
         info[sd] = dict(plan=plan, mbs=mbs,
-                        mb_bytes=[pack_bytes(cfg, [spec_of[sd][x] for x in mb]) for mb in mbs],
+                        mb_bytes=[masked_pack_bytes(cfg, works[sd], mb, spec_of[sd], mask) for mb in mbs],
                         tokens=int(plan["mb_tokens"].sum()), deferred=int((plan["assign"] < 0).sum()))
         info[sd]["step_bytes"] = sum(info[sd]["mb_bytes"])
     for k in range(args.warmup):
@@ -777,7 +804,7 @@ def main() -> int:
     torch.cuda.synchronize()
     durs = np.array([s_.elapsed_time(e_) * 1e-3 for s_, e_ in events])   # seconds
 
-    ceiling = ceilings(cfg, w, mbs, spec_of[s0], outs, pack_stream, args.steps)
+    ceiling = ceilings(cfg, w, mbs, spec_of[s0], outs, pack_stream, args.steps, mask)
     pack_s0 = [x for x in per_seed if x["seed"] == s0][0]
     ceiling["pack_over_gather"] = round(ceiling["gather_us"] / pack_s0["mean_us"], 4)
     ceiling["pack_over_copy"] = round(ceiling["copy_us"] / pack_s0["mean_us"], 4)
@@ -825,7 +852,7 @@ def main() -> int:
         del gouts
 
     per_call = np.array(info[s0]["mb_bytes"], dtype=np.float64) / durs / 1e9
-    traffic = counter_traffic(cfg.name)
+    traffic = counter_traffic(cfg.name, args.mask)
     fracs = [x["frac"] for x in per_seed]
     result = {
         "metric": METRIC,
@@ -876,7 +903,9 @@ def main() -> int:
     result["plan"] = {"max_over_mean_cost": round(float(imb), 5),
                       "eq3_max": round(float(max((t / cfg.capacity) + (m / cfg.capacity) ** 2
                                                  for t, m in zip(plan["mb_tokens"], plan["mb_max_len"]))), 5)}
-    if cfg.host_pages:
+    if args.mask != "all":
+        result["config"]["tier_mask"] = args.mask
+    if cfg.host_pages and args.mask == "all":
         result["tiers"] = tier_split(cfg, w, mbs, spec_of[s0], outs, pack_stream)
         result["tiers"]["h2d_copy_GBps"] = round(h2d_ceiling(), 1)
     if not args.no_cpu_baseline:
