@@ -28,8 +28,10 @@
  *    was enqueued on another stream and has not finished, and a free of a
  *    sample still being read by an enqueued pack is deferred until that
  *    pack completes (Sec. 3.1: producers and consumers run decoupled).
- *    For that, a stream passed to pack_microbatch must stay valid until the
- *    samples it packed are freed or the pool is destroyed.
+ *    For that, the pool remembers the streams that packed each sample: a
+ *    stream passed to pack_microbatch (or pool_write_sample) must stay valid
+ *    until the samples it packed are freed, the pool is destroyed, or the
+ *    caller has handed it to pool_forget_stream.
  *  - Embeddings are bf16, row-major, H elements per row; the library moves
  *    them as raw 16-bit words (NaN payloads, signed zeros and denormals are
  *    preserved exactly).
@@ -401,6 +403,14 @@ fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_
                                   int32_t* out_cu_seqlens, int32_t* out_position_ids,
                                   int32_t* out_n_tokens, int32_t* out_max_seqlen,
                                   int32_t tier_mask, void* stream);
+
+/* Lets the pool forget `stream` before the caller destroys it: wherever the
+ * pool remembers the stream as a reader of a sample (a pack ran there) or as
+ * the stream of a sample's write, one event recorded now on the stream, after
+ * the work queued there, takes its place (no event if the stream is idle).
+ * Frees of those samples then wait for that event, not for the stream.
+ * Not on a capturing stream. Errors: ESTATE, EHIP. */
+fp_status pool_forget_stream(fp_pool* p, void* stream);
 
 /* Ends the hold that captured packs have on their samples (see HIP graphs
  * above): call it with a captured pack's sample id list (host uint64[n], in

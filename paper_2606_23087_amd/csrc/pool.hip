@@ -74,6 +74,9 @@ constexpr size_t kStageHostMin = 1 << 20;
 constexpr int kMaxPackRuns = fp::kMaxPackSamples + 2 * fp::kMaxPackImages;
 // Streams remembered per sample as its readers without growing host memory.
 constexpr size_t kReaders = 8;
+// Stands for "no stream" where a stream handle is remembered (no valid
+// hipStream_t has this value).
+void* const kNoStream = reinterpret_cast<void*>(~uintptr_t(0));
 
 // Device scratch of pack_microbatch_noalloc: the staged run table of a pack
 // too large for its kernel arguments goes here instead of into a staging
@@ -178,6 +181,8 @@ struct SampleRec {
                                  // k_write), -1 once seen complete
   void* write_stream = nullptr;  // stream of that write
   std::vector<void*> readers;    // streams that have packed it (capacity kReaders reserved)
+  std::vector<int32_t> reader_events;  // events standing in for reader streams the caller
+                                       // retired with pool_forget_stream
   int32_t captured = 0;          // packs of it captured into HIP graphs and not yet released
 };
 
@@ -435,10 +440,16 @@ void defer_or_release(fp_pool* p, Deferred&& d) {
   }
 }
 
-// Records an event on every stream in `readers` that still has work queued
-// (the packs that read a sample) and appends it to `events`.
-fp_status mark_readers(fp_pool* p, const std::vector<void*>& readers, std::vector<int32_t>* events) {
-  for (void* st : readers) {
+// Appends to `events` (each with a reference of its own) what follows every
+// pack that has read sample r: an event recorded now on each reader stream
+// that still has work queued, and the events that stand in for retired reader
+// streams.
+fp_status mark_readers(fp_pool* p, const SampleRec& r, std::vector<int32_t>* events) {
+  for (int32_t e : r.reader_events) {
+    p->events.ref(e);
+    events->push_back(e);
+  }
+  for (void* st : r.readers) {
     const hipError_t q = hipStreamQuery((hipStream_t)st);
     if (q == hipSuccess) continue;
     if (q != hipErrorNotReady) return fail(FP_EHIP, "stream query: %s", hipGetErrorString(q));
@@ -953,11 +964,12 @@ fp_status pool_free_sample(fp_pool* p, uint64_t sample_id) {
     Deferred d;
     // An event recorded now on every stream that packed the sample and still
     // has work queued follows those packs; idle streams need none.
-    fp_status st = mark_readers(p, r.readers, &d.events);
+    fp_status st = mark_readers(p, r, &d.events);
     if (st != FP_OK) {
       for (int32_t x : d.events) p->events.unref(x);
       return st;
     }
+    for (int32_t x : r.reader_events) p->events.unref(x);
     d.pages = std::move(r.pages);
     d.meta.emplace_back(r.meta_off, r.meta_len);
     if (r.pl_off >= 0) d.meta.emplace_back(r.pl_off, r.pl_len);
@@ -975,9 +987,11 @@ fp_status pool_reclaim(fp_pool* p, int32_t wait, int64_t* out_deferred_pages) {
     DeviceGuard guard(p->cfg.device);
     if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
     reclaim(p, wait != 0);
-    // Forget the write events that have completed (or, with wait, all of them).
+    // Forget the write events that have completed (or, with wait, all of
+    // them), and the completed events of retired reader streams.
     for (auto& kv : p->samples) {
       SampleRec& r = kv.second;
+      p->events.prune(&r.reader_events, wait != 0);
       if (r.written < 0) continue;
       if (wait) (void)hipEventSynchronize(p->events.ev[(size_t)r.written]);
       if (p->events.done(r.written)) {
@@ -1155,7 +1169,7 @@ fp_status pool_migrate(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_
       r.pl_len = pl_bytes;
       r.page_off = pl_off[j];
       r.pages = std::move(new_pages[j]);
-      fp_status ms = mark_readers(p, r.readers, &d.events);
+      fp_status ms = mark_readers(p, r, &d.events);
       if (ms != FP_OK) {
         // Without an event on every reader, wait for the whole device instead.
         (void)hipDeviceSynchronize();
@@ -1603,6 +1617,49 @@ fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_
     if (!p) return fail(FP_EINVAL, "null pool");
     return pack_impl(p, sample_ids, n, embed_table, vocab, out_emb, out_rows_cap, out_cu_seqlens, out_position_ids,
                      out_n_tokens, out_max_seqlen, tier_mask, stream, p->scratch_dev, kScratchBytes);
+  });
+}
+
+fp_status pool_forget_stream(fp_pool* p, void* stream) {
+  return guarded([&]() -> fp_status {
+    if (!p) return fail(FP_EINVAL, "null pool");
+    std::lock_guard<std::mutex> lock(p->mu);
+    DeviceGuard guard(p->cfg.device);
+    if (!guard.ok) return fail(FP_EHIP, "hipSetDevice");
+    hipStream_t hs = (hipStream_t)stream;
+    if (capturing(hs)) return fail(FP_ESTATE, "pool_forget_stream on a capturing stream");
+    // One event after the stream's queued work stands in for it wherever it
+    // is a reader (none if the stream is idle).
+    int32_t ev = -1;
+    const hipError_t q = hipStreamQuery(hs);
+    if (q != hipSuccess && q != hipErrorNotReady) return fail(FP_EHIP, "stream query: %s", hipGetErrorString(q));
+    bool used = false;
+    for (auto& kv : p->samples)
+      if (std::find(kv.second.readers.begin(), kv.second.readers.end(), stream) != kv.second.readers.end()) used = true;
+    if (used && q == hipErrorNotReady) {
+      hipError_t e = p->events.acquire(&ev);
+      if (e == hipSuccess) e = hipEventRecord(p->events.ev[(size_t)ev], hs);
+      if (e != hipSuccess) {
+        if (ev >= 0) p->events.unref(ev);
+        return fail(FP_EHIP, "stream event: %s", hipGetErrorString(e));
+      }
+    }
+    for (auto& kv : p->samples) {
+      SampleRec& r = kv.second;
+      auto it = std::find(r.readers.begin(), r.readers.end(), stream);
+      if (it != r.readers.end()) {
+        r.readers.erase(it);
+        if (ev >= 0) {
+          p->events.ref(ev);
+          r.reader_events.push_back(ev);
+        }
+      }
+      // A write still running on the stream: its event stays the sample's
+      // ordering point, but no later stream may be taken for this one.
+      if (r.write_stream == stream) r.write_stream = kNoStream;
+    }
+    if (ev >= 0) p->events.unref(ev);
+    return FP_OK;
   });
 }
 

@@ -97,6 +97,7 @@ _SIGS = {
     "pool_layout": (C.c_int32, [_P, _u64p, _u64p, _i64p]),
     "pool_reclaim": (C.c_int32, [_P, C.c_int32, _i64p]),
     "pool_release_captured": (C.c_int32, [_P, _u64p, C.c_int32]),
+    "pool_forget_stream": (C.c_int32, [_P, _P]),
     "fp_copy_bytes": (C.c_int32, [_P, _P, C.c_int64, C.c_int32, _P]),
     "fp_gather_rows": (C.c_int32, [_P, C.c_int32, C.c_int32, _P, _P]),
     "pool_migrate": (C.c_int32, [_P, _u64p, C.c_int32, C.c_int32, _P, _i64p]),
@@ -249,6 +250,11 @@ def pool_release_captured(pool: int, sample_ids) -> None:
     """End a captured pack's hold on its samples (once its graph will not be replayed again)."""
     ids, idp = _arr(sample_ids, np.uint64, _u64p)
     _check(_lib.pool_release_captured(pool, idp, len(ids)), "pool_release_captured")
+
+
+def pool_forget_stream(pool: int, stream) -> None:
+    """Before destroying ``stream``: the pool stops remembering it (an event stands in for its queued work)."""
+    _check(_lib.pool_forget_stream(pool, _stream(stream)), "pool_forget_stream")
 
 
 def pool_migrate(pool: int, sample_ids, tier: int, stream=None) -> int:

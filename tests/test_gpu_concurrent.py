@@ -7,6 +7,8 @@ embeddings into the pool while the backbone's packs read it, decoupled).
 - A pack on another stream than the sample's write waits for that write.
 - A producer thread writing and freeing on one stream and a consumer packing
   on another: every pack equals the definitional pack of its samples.
+- A stream handed to pool_forget_stream can be destroyed while the samples it
+  packed stay resident; their frees then never touch it.
 
 The delays that keep a pack or a write queued come from ordinary copies
 enqueued ahead of it on the same stream.
@@ -270,5 +272,56 @@ def test_two_producers_and_a_planning_consumer(fp):
     finally:
         for t in threads:
             t.join()
+        torch.cuda.synchronize()
+        fp.pool_destroy(pool)
+
+
+def test_forget_stream_then_destroy(fp):
+    """A stream handed to pool_forget_stream may be destroyed while samples it
+    packed stay resident: later frees wait for the event that stood in for
+    it (or for nothing, if it was idle) and never touch the dead handle."""
+    import ctypes
+    import os
+    hip = ctypes.CDLL(os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so"))
+    hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    hip.hipStreamSynchronize.argtypes = [ctypes.c_void_p]
+    say("case forget a stream, then destroy it")
+    rng = np.random.default_rng(31)
+    specs = [_spec(rng, VOCAB, int(rng.integers(5, 40)), [int(x) for x in rng.integers(1, 60, size=2)])
+             for _ in range(12)]
+    vis = [tagged_vis(i, s.n_vis, H, 31) for i, s in enumerate(specs)]
+    table = tagged_table(VOCAB, H, 31)
+    t_dev = to_dev(table)
+    pool = _pool(fp, 400)
+    try:
+        ids = [fp.pool_write_sample(pool, s.text_ids, s.img_pos, s.img_ntok, to_dev(v)) for s, v in zip(specs, vis)]
+        torch.cuda.synchronize()
+        free0 = fp.pool_stats(pool)["free_hbm_pages"]
+        rows = sum(s.length for s in specs)
+        for case in ("busy", "idle"):
+            raw = ctypes.c_void_p()
+            assert hip.hipStreamCreate(ctypes.byref(raw)) == 0
+            outs = [torch.full((rows, H), 0x5A5A, dtype=torch.int16, device="cuda") for _ in range(2)]
+            keep = _busy(torch.cuda.ExternalStream(raw.value), 10) if case == "busy" else None
+            fp.pack_microbatch(pool, ids[:6], t_dev, VOCAB, outs[0], rows, None, None, stream=raw.value)
+            fp.pack_microbatch(pool, ids[6:], t_dev, VOCAB, outs[1], rows, None, None, stream=raw.value)
+            if case == "idle":
+                assert hip.hipStreamSynchronize(raw.value) == 0
+            fp.pool_forget_stream(pool, raw.value)
+            assert hip.hipStreamSynchronize(raw.value) == 0
+            assert hip.hipStreamDestroy(raw.value) == 0
+            del keep
+            for k, g in enumerate((ids[:6], ids[6:])):
+                want = definitional_pack([specs[ids.index(x)] for x in g], [vis[ids.index(x)] for x in g], table)[0]
+                assert np.array_equal(to_host(outs[k][:len(want)]), want), (case, k)
+            if case == "busy":
+                continue                       # the samples stay; the idle case packs them again, then frees
+            for sid in ids:
+                fp.pool_free_sample(pool, sid)
+        assert fp.pool_reclaim(pool, True) == 0
+        assert fp.pool_stats(pool) == {"free_hbm_pages": free0 + sum(-(-s.n_vis // P) for s in specs),
+                                       "free_host_pages": 0, "n_samples": 0}
+    finally:
         torch.cuda.synchronize()
         fp.pool_destroy(pool)
