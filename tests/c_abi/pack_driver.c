@@ -1,6 +1,7 @@
 /* Drives libflowpool through its C ABI alone (no Python, no torch): reads a
  * workload from a file, writes every sample into a pool, plans microbatches
- * with plan_microbatches, packs each with pack_microbatch and writes the
+ * with plan_microbatches, packs each with pack_microbatch (odd-numbered
+ * microbatches with pack_microbatch_noalloc) and writes the
  * results to a file, which the test compares with the oracle.
  *
  * Input (little-endian; i32 unless noted):
@@ -158,9 +159,12 @@ int main(int argc, char** argv) {
     hip_ok(hipMalloc(&d_cu, 4 * ((size_t)k + 1)), "hipMalloc(cu)");
     hip_ok(hipMalloc(&d_pos, 4 * (size_t)cap), "hipMalloc(pos)");
     int32_t n_tok = 0, mx = 0;
-    if (pack_microbatch(pool, members, k, d_table, vocab, d_out, cap, (int32_t*)d_cu, (int32_t*)d_pos, &n_tok, &mx,
-                        FP_TIER_MASK_ALL, NULL) != FP_OK)
-      die("pack_microbatch");
+    /* odd microbatches through the entry point that allocates nothing */
+    fp_status st = (j & 1) ? pack_microbatch_noalloc(pool, members, k, d_table, vocab, d_out, cap, (int32_t*)d_cu,
+                                                     (int32_t*)d_pos, &n_tok, &mx, FP_TIER_MASK_ALL, NULL)
+                           : pack_microbatch(pool, members, k, d_table, vocab, d_out, cap, (int32_t*)d_cu,
+                                             (int32_t*)d_pos, &n_tok, &mx, FP_TIER_MASK_ALL, NULL);
+    if (st != FP_OK) die((j & 1) ? "pack_microbatch_noalloc" : "pack_microbatch");
     hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize");
     int32_t* cu = (int32_t*)xmalloc(4 * ((size_t)k + 1));
     int32_t* p = (int32_t*)xmalloc(4 * (size_t)cap);

@@ -1,8 +1,9 @@
 """The C ABI driven from plain C: `tests/c_abi/pack_driver` (built by
 build(), linked only against libflowpool.so and the HIP runtime; no Python,
 no torch in that process) writes samples into a pool, plans with
-plan_microbatches and packs every microbatch with pack_microbatch. Its
-output must equal the oracle's plan and definitional pack, bit for bit.
+plan_microbatches and packs every microbatch with pack_microbatch (every
+odd-numbered one with pack_microbatch_noalloc). Its output must equal the
+oracle's plan and definitional pack, bit for bit.
 
 The workload is the tiny configuration's samples plus hand-made edge
 samples: text only, image only, adjacent images, an empty image, an image
