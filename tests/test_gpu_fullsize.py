@@ -2,19 +2,17 @@
 benchmark times (same pool, same pack entry point, a non-default stream,
 rotating output buffers).
 
-Every microbatch is checked by properties that hold at any size:
+Every sample the plan places is also written, with the same bytes and after
+the same churn history, into the oracle pool (its visual rows and the table
+rows its text names are copied from the seeded generators to the host); then
+for every microbatch:
 - the plan (assignment, tokens, cost per microbatch) equals the oracle's;
-- every sample's page GVAs equal the oracle pool's (same churn history);
+- every sample's page GVAs equal the oracle pool's;
 - cu_seqlens and position ids equal the oracle's, in full;
-- the tag words of EVERY packed row name exactly the source the oracle's
+- the tag words of every packed row name exactly the source the oracle's
   layout gives (sample, visual index or text id);
-- sampled rows (first, last, and random ones) equal, in all H words, the
-  input row the oracle names for them.
-Two whole microbatches per workload, the first and the one with the most
-tokens, are compared element by element with the oracle pool's pack: their
-samples' visual rows (and the table rows their text names) are copied from
-the seeded generators to the host and written into the oracle pool, which
-packs them through its own page table.
+- every word of every row equals the oracle pool's pack, which resolves each
+  row through its own page table.
 """
 
 import numpy as np
@@ -63,10 +61,9 @@ def test_full_size(fp, name):
     w = GpuWorkload(cfg, seed, mode="tagged", log=say)
     try:
         assign, tok, cst, mem = oracle_plan(cfg, w.specs)
-        whole = sorted({0, int(np.argmax(tok))})          # microbatches compared element by element
-        members = {i for j in whole for i in mem[j]}
-        say(f"  {len(w.ids)} samples written; replaying in the oracle pool, with the rows of microbatches "
-            f"{whole} ({len(members)} samples)")
+        members = {i for m in mem for i in m}            # every planned sample
+        say(f"  {len(w.ids)} samples written; replaying in the oracle pool with the rows of the "
+            f"{len(members)} planned samples")
         vis_np = [to_host(vis_rows(cfg, seed, i, s.n_vis, "tagged")) if i in members and s.n_vis else None
                   for i, s in enumerate(w.specs)]
         opool, oids = oracle_pool_for(cfg, seed, w.specs, vis_np, with_bytes=True)
@@ -84,7 +81,6 @@ def test_full_size(fp, name):
         assert mbs == [[w.ids[i] for i in m] for m in mem]
         stream = torch.cuda.Stream()
         outs = [w.alloc_outputs() for _ in range(4)]
-        rng = np.random.default_rng(11)
         for j, idx in enumerate(mem):
             out, cu, pos = outs[j % 4]
             n, mx = w.pack([w.ids[i] for i in idx], out, cu, pos, stream=stream)
@@ -98,29 +94,15 @@ def test_full_size(fp, name):
             got_tags = to_host(out[:n, :4])
             bad = np.nonzero(np.any(got_tags != tags, axis=1))[0]
             assert bad.size == 0, f"microbatch {j}: {bad.size} rows with wrong source, first {bad[:5]}"
-            picks = sorted(set([0, n - 1] + rng.integers(0, n, size=24).tolist()))
-            vis_cache = {}
-            for r in picks:
-                kind, s, x = src[r]
-                if kind == "text":
-                    want = to_host(w.table[x])
-                else:
-                    g = idx[s]
-                    if g not in vis_cache:
-                        vis_cache[g] = vis_rows(cfg, seed, g, w.specs[g].n_vis, "tagged")
-                    want = to_host(vis_cache[g][x])
-                assert np.array_equal(to_host(out[r]), want), f"microbatch {j} row {r} ({kind})"
-            if j in whole:
-                rows_o, cu_o, pos_o, n_o, mx_o = opool.pack([oids[i] for i in idx], host_table)
-                assert (n_o, mx_o) == (n, mx)
-                got = to_host(out[:n])
-                bad = np.nonzero(np.any(got != rows_o, axis=1))[0]
-                assert bad.size == 0, f"microbatch {j}: {bad.size} of {n} rows differ from the oracle, first {bad[:5]}"
-                assert cu[:len(idx) + 1].cpu().numpy().tolist() == cu_o.tolist()
-                assert np.array_equal(pos[:n].cpu().numpy(), pos_o)
-                say(f"  microbatch {j}: all {n} x {cfg.hidden} words equal the oracle pool's pack")
-                del got, rows_o
-        say(f"  {len(mem)} microbatches checked")
+            rows_o, cu_o, pos_o, n_o, mx_o = opool.pack([oids[i] for i in idx], host_table)
+            assert (n_o, mx_o) == (n, mx)
+            got = to_host(out[:n])
+            bad = np.nonzero(np.any(got != rows_o, axis=1))[0]
+            assert bad.size == 0, f"microbatch {j}: {bad.size} of {n} rows differ from the oracle, first {bad[:5]}"
+            assert cu[:len(idx) + 1].cpu().numpy().tolist() == cu_o.tolist()
+            assert np.array_equal(pos[:n].cpu().numpy(), pos_o)
+            del got, rows_o
+        say(f"  {len(mem)} microbatches checked: every word equals the oracle pool's pack")
         if cfg.host_pages:
             say("  tier-mask split at full size")
             full, cu, pos = w.alloc_outputs(fill=0)
