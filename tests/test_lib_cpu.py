@@ -116,8 +116,33 @@ def test_null_pool_is_rejected_by_every_pool_call():
     assert lib.pool_free_sample(None, ctypes.c_uint64(1)) == fp.FP_EINVAL
     assert lib.pack_microbatch(None, None, 0, None, ctypes.c_int64(0), None, ctypes.c_int64(0), None, None,
                                None, None, 3, None) == fp.FP_EINVAL
+    assert lib.pack_microbatch_noalloc(None, None, 0, None, ctypes.c_int64(0), None, ctypes.c_int64(0), None, None,
+                                       None, None, 3, None) == fp.FP_EINVAL
+    assert lib.pool_release_captured(None, None, 0) == fp.FP_EINVAL
+    assert lib.pool_forget_stream(None, None) == fp.FP_EINVAL
     assert "null" in fp.fp_last_error()
     assert fp.pool_destroy(0) is None                          # NULL is accepted
+
+
+def test_measurement_aids_check_arguments_before_the_device():
+    """fp_copy_bytes and fp_gather_rows refuse bad sizes and alignments
+    before any HIP call (so this runs without a GPU)."""
+    lib = ctypes.CDLL(fp.LIB_PATH)
+    lib.fp_copy_bytes.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    lib.fp_gather_rows.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    a, b = 1 << 20, 2 << 20                                    # addresses are never dereferenced here
+    assert lib.fp_copy_bytes(a, b, 24, 16, None) == fp.FP_EINVAL           # not a multiple of 16
+    assert lib.fp_copy_bytes(a, b, -16, 16, None) == fp.FP_EINVAL
+    assert lib.fp_copy_bytes(a, b, (1 << 35), 16, None) == fp.FP_EINVAL     # more than 2^31 - 1024 vectors
+    assert lib.fp_copy_bytes(a, b, 32, 8, None) == fp.FP_EINVAL            # row_bytes not a multiple of 16
+    assert lib.fp_copy_bytes(None, b, 32, 16, None) == fp.FP_EINVAL
+    assert lib.fp_copy_bytes(a + 8, b, 32, 16, None) == fp.FP_EALIGN
+    assert lib.fp_gather_rows(a, -1, 16, b, None) == fp.FP_EINVAL
+    assert lib.fp_gather_rows(a, 4, 24, b, None) == fp.FP_EINVAL
+    assert lib.fp_gather_rows(a, 1 << 30, 1024, b, None) == fp.FP_EINVAL   # too many vectors
+    assert lib.fp_gather_rows(None, 4, 16, b, None) == fp.FP_EINVAL
+    assert lib.fp_gather_rows(a + 4, 4, 16, b, None) == fp.FP_EALIGN
+    assert lib.fp_gather_rows(a, 4, 16, b + 8, None) == fp.FP_EALIGN
 
 
 def test_bindings_refuse_ordinary_host_tensors():
