@@ -359,7 +359,10 @@ def pack_microbatch(pool: int, sample_ids, embed_table, vocab: int, out_emb, out
                     out_cu_seqlens=None, out_position_ids=None, tier_mask: int = FP_TIER_MASK_ALL,
                     stream=None, _entry=None):
     """Enqueue the pack of ``sample_ids`` into ``out_emb``. Returns (n_tokens, max_seqlen)."""
-    ids, idp = _arr(sample_ids, np.uint64, _u64p)
+    if isinstance(sample_ids, (list, tuple)):
+        ids = idp = (C.c_uint64 * len(sample_ids))(*sample_ids)   # cheaper per call than a numpy round trip
+    else:
+        ids, idp = _arr(sample_ids, np.uint64, _u64p)
     n_tok = C.c_int32()
     mx = C.c_int32()
     rb = 2 * _HIDDEN.get(pool, 0)
