@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace fp {
@@ -77,8 +78,12 @@ constexpr int64_t kMaxMetaBytes = 1ll << 33;
 // memory first, laid out at the given byte offsets. For each row bucket b,
 // brun[b] is a copy of the run holding row b << bucket_shift and bucket[b]
 // that run's index, so a row of the same run is resolved with one load, and a
-// later row steps on from there.
-struct PackArgs {
+// later row steps on from there. The table capacities are template
+// parameters: PackArgs is the general form, PackArgsSmall a compact one for
+// microbatches of a few samples, whose smaller kernel arguments take less
+// host time to launch.
+template <int kSamples, int kRuns, int kBucketCount>
+struct PackArgsT {
   const uint8_t* meta;        // device metadata arena
   const uint64_t* pte;        // device page table, index = (gva - gva_start) / page_bytes
   uint64_t gva_start;
@@ -99,19 +104,25 @@ struct PackArgs {
   uint64_t pb_mul;            // d / page_bytes == umulhi64(d, pb_mul) >> pb_shift for d < 2^52
   int32_t pt_shift;
   int32_t pb_shift;
-  alignas(16) int32_t lens[kInlineSamples];   // sample lengths (rows), in pack order
-  alignas(16) PackRun runs[kInlineRuns];
-  alignas(16) PackRun brun[kBuckets];
-  uint16_t bucket[kBuckets];
+  alignas(16) int32_t lens[kSamples];   // sample lengths (rows), in pack order
+  alignas(16) PackRun runs[kRuns];
+  alignas(16) PackRun brun[kBucketCount];
+  uint16_t bucket[kBucketCount];
+  static constexpr int kMaxSamples = kSamples, kMaxRuns = kRuns, kMaxBuckets = kBucketCount;
 };
+using PackArgs = PackArgsT<kInlineSamples, kInlineRuns, kBuckets>;
+using PackArgsSmall = PackArgsT<8, 24, 16>;
 // The pack's kernel arguments, 64 bytes of leading scalars (preloaded into
 // registers) and this struct, stay within 4 KiB.
 static_assert(sizeof(PackArgs) + 64 <= 4096, "kernel arguments stay within 4 KiB");
+static_assert(offsetof(PackArgs, lens) == offsetof(PackArgsSmall, lens), "same scalar fields");
 
 // A pack launch: the kernel's arguments and, host side, its geometry.
 struct PackPlan {
   PackArgs a;
   const uint8_t* staged;      // staged run table, or null = the arrays in `a`
+  bool small;                 // launch with PackArgsSmall (its table copied from `a`)
+  int32_t n_runs, n_buckets;  // entries of the table in `a`
   int32_t max_chunk_rows;     // rows one chunk can touch
   int32_t g0, g1;             // workgroups [0, g0): full chunks; [g0, g1): kTail1Vecs; then kTail2Vecs
   int32_t t1, t2;             // first vectors of the two tail stages (t1 = g0 * full chunk)

@@ -18,6 +18,7 @@
 #include "fp_internal.h"
 
 #include <algorithm>
+#include <cstring>
 
 namespace fp {
 
@@ -126,8 +127,8 @@ __device__ __forceinline__ PackRun run_of(const RunIndex& x, int32_t off_runs, c
 // GVAs start at 64-bit word `word` of the arena: visual index -> page GVA
 // (the sample's page list) -> page-table entry (the GVA's page number) -> row
 // in the physical page. Returns the page-table entry's flags in *flags.
-template <bool kScalar>
-__device__ __forceinline__ uint64_t walk(const PackArgs& a, int32_t word, uint32_t vidx, uint64_t* flags) {
+template <bool kScalar, class Args>
+__device__ __forceinline__ uint64_t walk(const Args& a, int32_t word, uint32_t vidx, uint64_t* flags) {
   const int lp = (int)(((uint64_t)vidx * a.pt_mul) >> a.pt_shift);
   const int in_page = (int)vidx - lp * a.page_tokens;
   const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)word + lp));
@@ -137,15 +138,16 @@ __device__ __forceinline__ uint64_t walk(const PackArgs& a, int32_t word, uint32
   return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;
 }
 
-__device__ __forceinline__ uint64_t text_row(const PackArgs& a, int32_t id) {
+template <class Args>
+__device__ __forceinline__ uint64_t text_row(const Args& a, int32_t id) {
   return reinterpret_cast<uint64_t>(a.table) + (uint64_t)(uint32_t)id * (uint64_t)a.row_bytes;
 }
 
 // Source address of packed row `row` of run r, or 0 when the tier mask
 // leaves the row out. A text row's id selects an embedding-table row; an
 // image row walks the page table.
-template <bool kScalar>
-__device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun& run, int row) {
+template <bool kScalar, class Args>
+__device__ __forceinline__ uint64_t row_source(const Args& a, const PackRun& run, int row) {
   if (run.head < 0) {
     if (!(a.tier_mask & 1)) return 0;
     return text_row(a, ld<kScalar, int32_t>(a.meta + 4 * ((int64_t)run.word + row)));
@@ -167,11 +169,11 @@ __device__ __forceinline__ uint64_t row_source(const PackArgs& a, const PackRun&
 // rows at realistic hidden sizes), each row is resolved by one wave with
 // scalar loads, so the only vector memory loads are the copies. Chunks of
 // many short rows resolve one row per lane.
-template <int VPT>
+template <int VPT, class Args>
 __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int32_t t1, int32_t t2,
                                                       uint64_t div_mul, int32_t div_shift, int32_t bucket_shift,
                                                       const uint8_t* staged, int32_t off_brun, int32_t off_bucket,
-                                                      int32_t total, PackArgs a) {
+                                                      int32_t total, Args a) {
   constexpr int kChunk = kPackBlock * VPT;       // vectors of a full chunk
   extern __shared__ __align__(16) uint64_t s_src[];
   __shared__ int32_t s_skip[kPackBlock / 64];
@@ -419,11 +421,24 @@ void pack_chunks(PackPlan* pl, int n_cu) {
   chunk_geometry((int64_t)pl->a.n_tokens * (pl->a.row_bytes >> 4), n_cu, pl);
 }
 
-template <int VPT>
-static void launch_pack_as(const PackPlan& pl, int grid, int32_t total, hipStream_t stream) {
-  hipLaunchKernelGGL(k_pack<VPT>, dim3(grid), dim3(kPackBlock), pack_lds_bytes(pl), stream, pl.g0, pl.g1, pl.t1,
-                     pl.t2, pl.div_mul, pl.div_shift, pl.a.bucket_shift, pl.staged, pl.a.off_brun, pl.a.off_bucket,
-                     total, pl.a);
+// The compact arguments of a small pack: the same scalar fields, the table
+// copied into the smaller arrays, offsets relative to them.
+static void small_args(const PackPlan& pl, PackArgsSmall* s) {
+  std::memcpy(static_cast<void*>(s), &pl.a, offsetof(PackArgs, lens));
+  std::memcpy(s->lens, pl.a.lens, sizeof(int32_t) * (size_t)pl.a.n);
+  std::memcpy(s->runs, pl.a.runs, sizeof(PackRun) * (size_t)pl.n_runs);
+  std::memcpy(s->brun, pl.a.brun, sizeof(PackRun) * (size_t)pl.n_buckets);
+  std::memcpy(s->bucket, pl.a.bucket, sizeof(uint16_t) * (size_t)pl.n_buckets);
+  s->off_runs = (int32_t)(offsetof(PackArgsSmall, runs) - offsetof(PackArgsSmall, lens));
+  s->off_brun = (int32_t)(offsetof(PackArgsSmall, brun) - offsetof(PackArgsSmall, lens));
+  s->off_bucket = (int32_t)(offsetof(PackArgsSmall, bucket) - offsetof(PackArgsSmall, lens));
+}
+
+template <int VPT, class Args>
+static void launch_pack_as(const PackPlan& pl, const Args& a, int grid, int32_t total, hipStream_t stream) {
+  hipLaunchKernelGGL((k_pack<VPT, Args>), dim3(grid), dim3(kPackBlock), pack_lds_bytes(pl), stream, pl.g0, pl.g1,
+                     pl.t1, pl.t2, pl.div_mul, pl.div_shift, a.bucket_shift, pl.staged, a.off_brun, a.off_bucket,
+                     total, a);
 }
 
 hipError_t launch_pack(const PackPlan& pl, hipStream_t stream) {
@@ -431,8 +446,15 @@ hipError_t launch_pack(const PackPlan& pl, hipStream_t stream) {
   const int64_t grid64 = pl.g1 + (vecs - pl.t2 + kTail2Vecs - 1) / kTail2Vecs;
   const int grid = grid64 > 0 ? (int)grid64 : 1;
   const int32_t total = (int32_t)vecs;               // the host keeps this below 2^31
-  if (pl.vpt == 2) launch_pack_as<2>(pl, grid, total, stream);
-  else launch_pack_as<kVecsPerThread>(pl, grid, total, stream);
+  if (pl.small) {
+    PackArgsSmall s{};
+    small_args(pl, &s);
+    if (pl.vpt == 2) launch_pack_as<2>(pl, s, grid, total, stream);
+    else launch_pack_as<kVecsPerThread>(pl, s, grid, total, stream);
+  } else {
+    if (pl.vpt == 2) launch_pack_as<2>(pl, pl.a, grid, total, stream);
+    else launch_pack_as<kVecsPerThread>(pl, pl.a, grid, total, stream);
+  }
   return hipGetLastError();
 }
 

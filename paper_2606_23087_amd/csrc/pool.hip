@@ -1389,12 +1389,12 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
 }
 
 // Bucket index of runs covering rows [0, total) (run k starts where run k-1
-// ends): at most kBuckets buckets of 2^shift rows; bucket b gets the run
+// ends): at most max_buckets buckets of 2^shift rows; bucket b gets the run
 // holding its first row and that run's number. Returns the bucket count.
-static int32_t build_buckets(const fp::PackRun* runs, int32_t n_runs, int64_t total, int32_t* shift_out,
-                             fp::PackRun* brun, uint16_t* bucket) {
+static int32_t build_buckets(const fp::PackRun* runs, int32_t n_runs, int64_t total, int32_t max_buckets,
+                             int32_t* shift_out, fp::PackRun* brun, uint16_t* bucket) {
   int32_t shift = 0;
-  while (total > 0 && ((total - 1) >> shift) >= fp::kBuckets) ++shift;
+  while (total > 0 && ((total - 1) >> shift) >= max_buckets) ++shift;
   const int32_t nb = total > 0 ? (int32_t)(((total - 1) >> shift) + 1) : 0;
   for (int32_t b = 0, k = 0; b < nb; ++b) {
     const int64_t first = (int64_t)b << shift;
@@ -1517,12 +1517,19 @@ static fp_status pack_impl(fp_pool* p, const uint64_t* sample_ids, int32_t n, co
     }
     if (n_runs) runs[n_runs - 1].end = row;
   }
+  // A microbatch of a few samples and runs launches with the compact kernel
+  // arguments (less host time per launch), whose bucket index is shorter.
+  const bool small = n <= fp::PackArgsSmall::kMaxSamples && n_runs <= fp::PackArgsSmall::kMaxRuns;
   int32_t shift = 0;
-  const int32_t n_buckets = build_buckets(runs, n_runs, total, &shift, p->pk_brun.data(), p->pk_bucket.data());
+  const int32_t n_buckets = build_buckets(runs, n_runs, total, small ? fp::PackArgsSmall::kMaxBuckets : fp::kBuckets,
+                                          &shift, p->pk_brun.data(), p->pk_bucket.data());
   const int32_t bucket_len = n_buckets + (n_buckets & 1);
   a.bucket_shift = shift;
 
   pl.max_chunk_rows = (int32_t)std::min<int64_t>(total, fp::kChunkVecs / vpr + 2);
+  pl.small = small;
+  pl.n_runs = n_runs;
+  pl.n_buckets = n_buckets;
   fp::pack_chunks(&pl, p->n_cu);
 
   const bool staged = n > fp::kInlineSamples || n_runs > fp::kInlineRuns;

@@ -331,7 +331,9 @@ def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
     that are not powers of two; 17..32 samples with an inline run table,
     samples with eleven images, empty images and adjacent images (merged
     runs), the 32-sample and 160-run limits of the inline table and
-    microbatches just past them (staged table), and 64 or more samples. pack_cus=1 sizes the chunk
+    microbatches just past them (staged table), the 8-sample and 24-run
+    limits of the compact kernel arguments and one past each, and 64 or
+    more samples. pack_cus=1 sizes the chunk
     geometry for one compute unit, so these small packs also take full
     chunks and both shrinking tail stages; with the device's count they are
     all in the last stage."""
@@ -356,9 +358,14 @@ def test_chunk_head_shapes(fp, hidden, page_tokens, pack_cus):
         r160 = int(np.searchsorted(runs, 160, side="right"))     # first r160 samples form <= 160 runs
         assert runs[r160 - 1] <= 160 < runs[r160] and r160 < 32
         assert runs[101] - runs[69] <= 160                         # samples 70..101 fit the inline table
+        # the compact kernel arguments' limits (8 samples, 24 runs) and one past each
+        rn = [_runs(s) for s in specs]
+        at24 = next([i, j] for i in range(70) for j in range(i + 1, 70) if rn[i] + rn[j] == 24)
+        at25 = next([i, j] for i in range(70) for j in range(i + 1, 70) if rn[i] + rn[j] == 25)
+        assert sum(rn[i] for i in range(70, 78)) <= 24
         groups = [list(range(17)), list(range(r160)), list(range(r160 + 1)),
                   list(range(70, 102)), list(range(70, 103)), list(range(70, 134)), list(range(70)),
-                  [11, 23, 11, 35, 140 - 1]]
+                  [11, 23, 11, 35, 140 - 1], list(range(70, 78)), list(range(70, 79)), at24, at25, [11]]
         for g in groups:
             say(f"  group of {len(g)} samples, {sum(_runs(specs[i]) for i in g)} runs")
             n, mx = w.pack([w.ids[i] for i in g], out, cu, pos)

@@ -10,7 +10,7 @@
 - The pack kernels' leading scalar arguments (13 dwords) arrive preloaded in
   scalar registers, and the first loads of the row lookup (the bucket's run and
   index entry) are issued before the wait for the other kernel arguments, so the two are in
-  flight together (for the all-rows kernels, ahead of every kernel-argument load).
+  flight together.
 """
 
 import os
@@ -66,7 +66,7 @@ def test_asm_stores_carry_their_wait_states(isa):
 
 def test_pack_kernels_keep_full_occupancy(isa):
     packs = {k: v for k, v in _kernels(isa).items() if "k_pack" in k}
-    assert len(packs) == 2                      # 2 and 3 vectors per thread
+    assert len(packs) == 4                      # 2 and 3 vectors per thread; general and compact arguments
     for name, (_, meta) in packs.items():
         vgpr = int(re.search(r"\.amdhsa_next_free_vgpr (\d+)", meta).group(1))
         scratch = int(re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", meta).group(1))
@@ -76,7 +76,7 @@ def test_pack_kernels_keep_full_occupancy(isa):
 
 def test_pack_kernels_preload_their_head_arguments(isa):
     packs = {k: v for k, v in _kernels(isa).items() if "k_pack" in k}
-    assert len(packs) == 2
+    assert len(packs) == 4
     for name, (lines, meta) in packs.items():
         assert re.search(r"\.amdhsa_user_sgpr_kernarg_preload_length 13\b", meta), name
         # Entry with preloaded arguments: 256 bytes past the kernel symbol,
@@ -87,11 +87,4 @@ def test_pack_kernels_preload_their_head_arguments(isa):
         body = [l.strip() for l in lines[entry:]]
         first_wait = next(i for i, l in enumerate(body) if l.startswith("s_waitcnt"))
         loads = [l for l in body[:first_wait] if l.startswith("s_load")]
-        table_loads = [l for l in loads if not l.split(",")[1].strip().startswith("s[0:1]")]
-        if "Lb0E" in name:
-            # the row-lookup loads leave first
-            assert loads and loads[0] in table_loads, (name, loads[:3])
-        else:
-            # compact packs (tier-masked): the row-lookup loads at least leave
-            # before the first wait, in flight with the argument loads
-            assert table_loads, (name, loads[:3])
+        assert loads and not loads[0].split(",")[1].strip().startswith("s[0:1]"), (name, loads[:3])
