@@ -662,7 +662,7 @@ def main() -> int:
     if args.allocator:
         return allocator_bench(args)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this build "
+        print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this library "
               "(run with --gpus 1)", file=sys.stderr)
         return 2
 

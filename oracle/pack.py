@@ -10,7 +10,7 @@ What a packed microbatch is, written out plainly:
   fixed-capacity microbatch; the per-sequence boundaries (cu_seqlens) are
   what a varlen attention kernel consumes.
 
-Readings taken where the paper is silent (each listed in the design notes):
+Readings taken where the paper is silent:
 an image placeholder at text position p sits before text token p and
 consumes no text token; images at equal positions keep their order; a text
 row is the embedding-table row of its id; position ids restart at 0 for each

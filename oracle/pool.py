@@ -14,7 +14,7 @@ Follows Sec. 3.2 (unified memory pool):
   segment, with metadata that pairs them; the consumer reads microbatches by
   GVA without knowing where the bytes physically are.
 
-Readings where the paper is silent (listed in the design notes): the DRAM
+Readings where the paper is silent: the DRAM
 region starts where the HBM region ends; max_size of a tier is its page count
 times the page size; a sample's visual rows (all images, in image order) fill
 its own pages densely, the last page possibly partial, and pages are never

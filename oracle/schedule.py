@@ -17,8 +17,7 @@ Sec. 3.4 builds balanced microbatches in two phases (Alg. 1):
    decreasing cost, are dealt to the N data-parallel ranks in zig-zag order
    (ranks 0..N-1, then N-1..0, and so on).
 
-Readings where the paper leaves a detail open (listed with the others in the
-design notes):
+Readings where the paper leaves a detail open:
 - the shortest length is taken over the sequences of the call;
 - best-fit ties (equal residuals) go to the microbatch opened first;
 - the close check applies to the microbatch that just took the sequence;
