@@ -279,12 +279,12 @@ fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, in
  * parallelism configurations of one module. Encoders (backbone = 0) use data
  * and tensor parallelism, DP x TP devices; the backbone (backbone != 0) also
  * pipeline parallelism, DP x TP x PP devices. The section prunes
- * configurations whose DP does not divide the global batch, whose TP/PP
- * degrees do not factorize the module's resource budget, or whose tensor
- * parallelism crosses nodes; kept here:
+ * configurations whose DP does not divide the global batch, whose TP and PP
+ * degrees fail to split the module's device budget, or whose tensor
+ * parallelism spans two nodes; kept here:
  *  - DP divides global_batch;
- *  - DP*TP*PP <= devices (the module's budget, which its degrees factorize,
- *    fits the cluster); for the backbone with layers > 0, PP also divides
+ *  - DP*TP*PP <= devices (the module's device count, the product of its
+ *    degrees, fits the cluster); for the backbone with layers > 0, PP also divides
  *    layers (pipeline stages of equal depth); layers = 0 drops that rule;
  *    PP = 1 for encoders;
  *  - TP divides per_node (TP groups on consecutive devices stay in one node).

@@ -13,9 +13,9 @@ encoders use data and tensor parallelism (DP x TP devices), the backbone also
 pipeline parallelism (DP x TP x PP devices). The paper prunes three kinds of
 configuration; each is read here as one rule:
 - the global batch is not divisible by DP: kept iff DP divides it;
-- TP/PP degrees that do not factorize the per-module resource budget: a
-  module's budget is the device count of its configuration, which the three
-  degrees factorize by construction, so the rule bounds that count by the
+- TP and PP degrees that fail to split a module's device budget: a module's
+  budget is the device count of its configuration, the product of its
+  degrees by construction, so the rule bounds that count by the
   cluster's devices (DP x TP x PP <= devices); where the caller gives the
   backbone's layer count (layers > 0), PP must also divide it, so that every
   pipeline stage holds the same number of layers (a low-efficiency pruning
