@@ -47,6 +47,18 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def seconds_since_start() -> float:
+    """Wall seconds since this process started."""
+    try:
+        import psutil
+        return max(0.0, time.time() - psutil.Process().create_time())
+    except Exception:                    # no psutil: since this module was loaded
+        return time.perf_counter() - _T_LOADED
+
+
+_T_LOADED = time.perf_counter()
+
+
 def cpu_model_name() -> str:
     """The host CPU's model string (from /proc/cpuinfo where there is one)."""
     try:
@@ -637,6 +649,10 @@ def main() -> int:
     ap.add_argument("--buffers", type=int, default=4, help="rotating output buffers")
     ap.add_argument("--mask", default="all", choices=["all", "hbm", "host"],
                     help="tier mask of the timed packs (tiered pool: time one tier's part alone)")
+    ap.add_argument("--settle", type=float, default=3.0,
+                    help="seconds after the process started before the warm-up begins (the device clears "
+                         "memory freed by an earlier process in the background for a few seconds, which "
+                         "takes HBM bandwidth from the packs)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -728,6 +744,12 @@ def main() -> int:
                         mb_bytes=[masked_pack_bytes(cfg, works[sd], mb, spec_of[sd], mask) for mb in mbs],
                         tokens=int(plan["mb_tokens"].sum()), deferred=int((plan["assign"] < 0).sum()))
         info[sd]["step_bytes"] = sum(info[sd]["mb_bytes"])
+    torch.cuda.synchronize()
+    since_start = seconds_since_start()
+    slept = max(0.0, args.settle - since_start)
+    if slept > 0:
+        log(f"settling {slept:.2f} s ({since_start:.2f} s since the process started)")
+        time.sleep(slept)
     for k in range(args.warmup):
         one_step(seeds[k % len(seeds)])
     torch.cuda.synchronize()
@@ -861,6 +883,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"since_start_s": round(since_start, 3), "slept_s": round(slept, 3)},
         "ms_per_step": round(main_t["wall"] / args.steps * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",

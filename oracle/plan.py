@@ -29,6 +29,11 @@ position advances with every sample, placed or deferred.
 
 Brute force enumerates every assignment for tiny inputs to give the optimal
 max-cost partition.
+
+Parity unpinned: the tie rules of both policies are readings (the paper
+states none); only hand-worked partitions written from them check which of
+several equally good assignments is chosen. The assignment's quality is
+pinned against brute force and Graham's bound for LPT.
 """
 
 from __future__ import annotations

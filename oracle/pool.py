@@ -27,6 +27,12 @@ freeing pushes a sample's pages back last-page-first, so an equal-sized
 write right after gets the same pages in the same order; allocation is
 all-or-nothing.
 
+Parity unpinned: the two allocation policies and the free order are readings
+(the paper names no allocator); only hand-worked sequences written from those
+readings check them. Everything the pack reads through them (GVA ->
+page-table entry -> frame) is pinned by placement independence instead: the
+pack equals the plain definition whatever frames the allocator picks.
+
 The physical memory here is a dict of numpy page frames per tier,
 materialised only when written.
 """

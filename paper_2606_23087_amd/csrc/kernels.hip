@@ -32,6 +32,15 @@ __device__ __forceinline__ u32x4 load16(const uint8_t* p) {
   return __builtin_nontemporal_load((g_u32x4_c*)p);
 }
 
+// Embedding-table rows are read at random ids, a few KiB each, so the
+// streaming hint does not fit them: with plain loads a gather of random
+// 7 KiB table rows measured about 9 % faster than with non-temporal ones,
+// while rows read in page order are about 2 % faster non-temporal. The
+// policy is an instruction bit, so the pack picks it per chunk.
+__device__ __forceinline__ u32x4 load16_table(const uint8_t* p) {
+  return *(g_u32x4_c*)p;
+}
+
 // Stores carry the nt and sc1 cache-policy bits of the gfx950 global store:
 // on the pack this measured about 1.5 % faster than nt alone. The
 // compiler has no builtin for that bit combination, hence the asm; it has
@@ -158,6 +167,33 @@ __device__ __forceinline__ uint64_t row_source(const Args& a, const PackRun& run
   return src;
 }
 
+// Moves a thread's first N vectors of a chunk: vector u comes from from[u] and
+// goes to vector v0 + u * kPackBlock + tid of the output. kWhole: every
+// vector is live, so there is no predication and the compiler keeps all
+// loads in flight and waits for them one at a time before each store;
+// otherwise only live vectors are loaded and stored. kTable: the chunk holds
+// embedding-table rows and takes plain loads, else non-temporal ones. The
+// two load forms differ only in a cache-policy bit, which the compiler drops
+// when it merges otherwise identical code of two branches into one; the
+// table form is therefore fenced by asm statements (they emit no
+// instructions) that nothing can be merged across.
+template <int N, bool kTable, bool kWhole>
+__device__ __forceinline__ void copy_vectors(const uint64_t* from, const bool* live, uint8_t* out, int v0,
+                                             int tid) {
+  if constexpr (kTable) asm volatile(";; table-row chunk");
+  u32x4 v[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u)
+    if (kWhole || live[u]) {
+      const uint8_t* p = reinterpret_cast<const uint8_t*>(from[u]);
+      v[u] = kTable ? load16_table(p) : load16(p);
+    }
+#pragma unroll
+  for (int u = 0; u < N; ++u)
+    if (kWhole || live[u]) store16(out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
+  if constexpr (kTable) asm volatile(";; table-row chunk end");
+}
+
 // One workgroup packs one chunk of 256 * VPT 16-byte vectors of the output
 // (rows are contiguous in the output, so a chunk is a contiguous byte range
 // that may start and end inside rows; the last chunks are smaller): it
@@ -176,13 +212,14 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
                                                       int32_t total, Args a) {
   constexpr int kChunk = kPackBlock * VPT;       // vectors of a full chunk
   extern __shared__ __align__(16) uint64_t s_src[];
-  __shared__ int32_t s_skip[kPackBlock / 64];
+  __shared__ int32_t s_flags[kPackBlock / 64];
   const PackHead h{g0, g1, t1, t2, div_mul, div_shift, bucket_shift, staged, off_brun, off_bucket, total};
   const RunIndex cx{h.bucket_shift, h.off_brun, h.off_bucket};
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const uint8_t* tb = h.tb ? h.tb : reinterpret_cast<const uint8_t*>(a.lens);
   int my_skip = 0;                                  // a row of this chunk is not copied
+  int my_table = 0;                                 // a row of this chunk is an embedding-table row
 
   const int bx = (int)blockIdx.x;
   int v0, v1;
@@ -217,28 +254,34 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
     for (int t = wave; t < rows; t += kPackBlock / 64) {
       const int row = r0 + t;
       const BucketHit w = t == wave ? w0 : bucket_of<true>(cx, tb, row);
-      const uint64_t src = row_source<true>(a, run_of<true>(cx, a.off_runs, tb, row, w), row);
+      const PackRun run = run_of<true>(cx, a.off_runs, tb, row, w);
+      const uint64_t src = row_source<true>(a, run, row);
       if (lane == 0) {
         s_src[t] = src;
         if (!src) my_skip = 1;
+        else if (run.head < 0) my_table = 1;
       }
     }
   } else {
     for (int t = tid; t < rows; t += kPackBlock) {
       const int row = r0 + t;
-      const uint64_t src =
-          row_source<false>(a, run_of<false>(cx, a.off_runs, tb, row, bucket_of<false>(cx, tb, row)), row);
+      const PackRun run = run_of<false>(cx, a.off_runs, tb, row, bucket_of<false>(cx, tb, row));
+      const uint64_t src = row_source<false>(a, run, row);
       s_src[t] = src;
       if (!src) my_skip = 1;
+      else if (run.head < 0) my_table = 1;
     }
   }
-  // One flag per wave, written before and read after the only barrier.
-  const bool wave_skip = __any(my_skip);
-  if (lane == 0) s_skip[tid >> 6] = wave_skip ? 1 : 0;
+  // Flags per wave, written before and read after the only barrier.
+  const int wave_flags = (__any(my_skip) ? 1 : 0) | (__any(my_table) ? 2 : 0);
+  if (lane == 0) s_flags[tid >> 6] = wave_flags;
   __syncthreads();
-  int skip = 0;
+  int flags = 0;
 #pragma unroll
-  for (int w = 0; w < kPackBlock / 64; ++w) skip |= s_skip[w];
+  for (int w = 0; w < kPackBlock / 64; ++w) flags |= s_flags[w];
+  flags = __builtin_amdgcn_readfirstlane(flags);   // the same in every lane
+  const bool skip = (flags & 1) != 0;
+  const bool table = (flags & 2) != 0;           // plain loads for the whole chunk
 
   // Vector e of the chunk belongs to row e / vpr (multiply-shift division).
   // A vector is live if it lies in the chunk and its row is copied; only
@@ -257,22 +300,25 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
       from[u] = live[u] ? base + (uint64_t)(e - row * vpr) * 16 : 0;
     }
   }
-  u32x4 v[VPT];
-  if (v1 - v0 == kChunk && !skip) {
-    // Whole chunk, every row copied: no predication, so the compiler can keep
-    // all loads in flight and wait for them one at a time before each store.
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
-#pragma unroll
-    for (int u = 0; u < VPT; ++u)
-      store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
+  // Full chunks and the two tail sizes (whole multiples of the block) with
+  // every row copied move their vectors unpredicated; the last chunk and
+  // chunks with rows the tier mask leaves out are predicated per vector.
+  static_assert(kTail1Vecs % kPackBlock == 0 && kTail2Vecs % kPackBlock == 0 && kTail2Vecs < kTail1Vecs &&
+                    kTail1Vecs <= kChunk, "tail chunks are whole multiples of the block");
+  constexpr int kT1 = kTail1Vecs / kPackBlock, kT2 = kTail2Vecs / kPackBlock;
+  const int n_vec = v1 - v0;
+  if (!skip && n_vec == kChunk) {
+    if (table) copy_vectors<VPT, true, true>(from, live, a.out, v0, tid);
+    else copy_vectors<VPT, false, true>(from, live, a.out, v0, tid);
+  } else if (!skip && n_vec == kTail1Vecs) {
+    if (table) copy_vectors<kT1, true, true>(from, live, a.out, v0, tid);
+    else copy_vectors<kT1, false, true>(from, live, a.out, v0, tid);
+  } else if (!skip && n_vec == kTail2Vecs) {
+    if (table) copy_vectors<kT2, true, true>(from, live, a.out, v0, tid);
+    else copy_vectors<kT2, false, true>(from, live, a.out, v0, tid);
   } else {
-#pragma unroll
-    for (int u = 0; u < VPT; ++u)
-      if (live[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
-#pragma unroll
-    for (int u = 0; u < VPT; ++u)
-      if (live[u]) store16(a.out + (size_t)(v0 + u * kPackBlock + tid) * 16, v[u]);
+    if (table) copy_vectors<VPT, true, false>(from, live, a.out, v0, tid);
+    else copy_vectors<VPT, false, false>(from, live, a.out, v0, tid);
   }
 
   // cu_seqlens and position ids, by the last wave after its copies.

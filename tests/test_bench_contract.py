@@ -36,6 +36,7 @@ def test_json_line_fields():
         assert isinstance(d[k], t), (k, d.get(k))
     assert "vs_baseline" in d and d["vs_baseline"] is None
     assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["value"] > 0
+    assert d["settle"]["slept_s"] >= 0 and d["settle"]["since_start_s"] + d["settle"]["slept_s"] >= 3.0 - 1e-3
     assert d["config"]["workload"].startswith("tiny")
     roof = d["roofline"]
     assert roof["bound"] == "hbm" and roof["unit"] == "GB/s" and roof["peak"] == 8000.0
