@@ -248,9 +248,10 @@ def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
 
 def row_sources(cfg, w, mb, spec_of, tiers=False):
     """Device address of the source of every row of microbatch ``mb``, in
-    pack order (text rows: their table row; image rows: their row in the
-    physical page, from the pool's page table), for the gather ceiling; with
-    ``tiers``, also each row's tier (text rows count as HBM)."""
+    pack order (text rows: their table row, with bit 0 set to mark it as one;
+    image rows: their row in the physical page, from the pool's page table),
+    for the gather ceiling; with ``tiers``, also each row's tier (text rows
+    count as HBM)."""
     import numpy as np
     from paper_2606_23087_amd import flowpool as fp
     rb, P = cfg.row_bytes, cfg.page_tokens
@@ -268,7 +269,7 @@ def row_sources(cfg, w, mb, spec_of, tiers=False):
         vis = phys[(v // np.uint64(P)).astype(np.int64)] + (v % np.uint64(P)) * np.uint64(rb) if sp.n_vis \
             else np.zeros(0, np.uint64)
         vtier = np.array(ptier, np.int8)[(np.arange(sp.n_vis) // P)] if sp.n_vis else np.zeros(0, np.int8)
-        text = table + sp.text_ids.astype(np.uint64) * np.uint64(rb)
+        text = (table + sp.text_ids.astype(np.uint64) * np.uint64(rb)) | np.uint64(1)   # bit 0: a table row
         ti = vi = 0
         for p_, nt in zip(sp.img_pos.tolist(), sp.img_ntok.tolist()):
             addr += [text[ti:p_], vis[vi:vi + nt]]
@@ -589,6 +590,56 @@ def prefetch_bench(args, cfg, w, mbs, spec_of, outs, pack_stream) -> dict:
 ALLOC_DEVICES = (64, 128, 256, 512, 1024)
 
 
+def table_policy_bench(args) -> int:
+    """Gathers of random embedding-table rows through the library's gather
+    kernel, with the table-row mark (the plain loads the pack uses for chunks
+    holding table rows) and without it (the non-temporal loads of page rows),
+    over tables of several sizes: 16000 rows of 7168 bytes per launch at
+    uniform random ids, 64 launches into 4 rotating buffers, timed like the
+    pack (one event pair around all launches of ``--steps`` passes). Plain
+    loads let the device's 256 MB memory-side cache keep table rows, which
+    pays while a good part of the table fits there."""
+    import numpy as np
+    import torch
+
+    from paper_2606_23087_amd import flowpool as fp
+
+    rb, rows, launches, passes = 7168, 16000, 64, max(1, args.steps)
+    outs = [torch.empty(rows * rb, dtype=torch.uint8, device="cuda") for _ in range(4)]
+    stream = torch.cuda.current_stream()
+    res = []
+    for table_rows in (9362, 37449, 152064, 228096, 304128, 380160, 456192, 600000):
+        table = torch.ones(table_rows * rb, dtype=torch.uint8, device="cuda")
+        ids = np.random.default_rng(args.seed).integers(0, table_rows, size=(launches, rows))
+        addr = table.data_ptr() + ids.astype(np.int64) * rb
+        row = {"table_rows": table_rows, "table_MB": round(table_rows * rb / 1e6, 1)}
+        for name, mark in (("plain_loads", 1), ("nontemporal_loads", 0)):
+            lists = torch.from_numpy(addr | mark).to("cuda")
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for rep in range(passes + 1):
+                if rep == 1:
+                    e0.record(stream)
+                for j in range(launches):
+                    fp.fp_gather_rows(lists[j], rows, rb, outs[j % 4], stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (passes * launches)
+            row[name] = {"us": round(us, 3), "GBps": round(2 * rows * rb / us / 1e3, 1)}
+            del lists
+        row["plain_over_nontemporal"] = round(row["nontemporal_loads"]["us"] / row["plain_loads"]["us"], 4)
+        log(f"table policy: {row}")
+        res.append(row)
+        del table
+    at = [x for x in res if x["table_rows"] == 152064][0]
+    print(json.dumps({
+        "metric": "gather of random 7168-byte embedding-table rows, plain vs non-temporal loads",
+        "value": at["plain_loads"]["GBps"], "unit": "GB/s", "higher_is_better": True, "n_gpus": 1,
+        "data": "synthetic", "config": {"workload": "table-policy", "rows_per_launch": rows, "launches": launches,
+                                        "passes": passes, "seed": args.seed},
+        "per_table": res}), flush=True)
+    return 0
+
+
 def allocator_bench(args) -> int:
     """Time of the allocator's flow matching (Eq. 2) on the host for clusters
     of 8-device nodes (global batch 512, a 28-layer backbone, two encoders),
@@ -669,6 +720,9 @@ def main() -> int:
                     help="tiered pool: zero-copy packs vs packs after promoting host-tier pages into HBM")
     ap.add_argument("--graph", action="store_true",
                     help="also time one step's packs captured into a HIP graph and replayed")
+    ap.add_argument("--table-policy", action="store_true",
+                    help="time gathers of random embedding-table rows with the pack's plain loads and with "
+                         "non-temporal ones, over tables of several sizes")
     ap.add_argument("--concurrent", action="store_true",
                     help="time the packs alone and under a concurrent producer on another stream")
     args = ap.parse_args()
@@ -681,6 +735,9 @@ def main() -> int:
         print("bench.py measures one GPU only: the pack path is not sharded across GPUs in this library "
               "(run with --gpus 1)", file=sys.stderr)
         return 2
+
+    if args.table_policy:
+        return table_policy_bench(args)
 
     import numpy as np
     import torch

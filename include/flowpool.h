@@ -364,6 +364,9 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
  *  out_position_ids  device int32[out_rows_cap] (or NULL): r within sample.
  *  embed_table       device bf16 [vocab, H], 16-byte aligned; may be NULL when
  *                    no sample has text. vocab must be >= the pool's vocab.
+ *                    A table of at most 2.5 GiB is read with plain loads, which
+ *                    let the device's memory-side cache keep its rows; a larger
+ *                    one with non-temporal loads (this changes timing only).
  *  out_n_tokens, out_max_seqlen  host int32 (or NULL): total and longest l.
  *  tier_mask         FP_TIER_MASK_HBM copies text rows and rows on HBM pages
  *                    and writes cu_seqlens/position ids; FP_TIER_MASK_HOST
@@ -458,9 +461,12 @@ fp_status fp_copy_bytes(const void* src, void* dst, int64_t bytes, int32_t row_b
 
 /* fp_gather_rows: output row r (row_bytes bytes, a multiple of 16) of dst
  * (device, 16-byte aligned, n_rows * row_bytes bytes) is a copy of the
- * row_bytes bytes at address rows_src[r]; rows_src is a device uint64[n_rows]
- * of device-readable, 16-byte aligned addresses, which the call does not
- * check (an invalid one faults the GPU). Errors: EINVAL, EALIGN, EHIP. */
+ * row_bytes bytes at address rows_src[r] with its low 4 bits cleared;
+ * rows_src is a device uint64[n_rows] of device-readable, 16-byte aligned
+ * addresses, which the call does not check (an invalid one faults the GPU).
+ * Bit 0 of an entry marks an embedding-table row: a chunk of the output that
+ * holds one reads with the loads pack_microbatch uses for table rows.
+ * Errors: EINVAL, EALIGN, EHIP. */
 fp_status fp_gather_rows(const uint64_t* rows_src, int32_t n_rows, int32_t row_bytes, void* dst, void* stream);
 
 #ifdef __cplusplus

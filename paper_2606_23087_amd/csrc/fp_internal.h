@@ -69,6 +69,14 @@ struct alignas(16) PackRun {
 };
 static_assert(sizeof(PackRun) == 16, "PackRun layout");
 constexpr int32_t kTextRun = INT32_MIN;
+// A bit of PackArgs::tier_mask beside the two tier bits: chunks holding
+// embedding-table rows read with plain loads, which let the device's 256 MB
+// memory-side cache keep table rows between reads. Set for tables of at most
+// kPlainTableMaxBytes: over uniform random rows, plain loads gather 9 % faster
+// than non-temporal ones from a 1.09 GB table, break even near 3 GB, and
+// are 1.5 % slower from a 4.3 GB one.
+constexpr int32_t kTablePlainLoads = 4;
+constexpr int64_t kPlainTableMaxBytes = 5ll << 29;   // 2.5 GiB
 constexpr int64_t kMaxMetaBytes = 1ll << 33;
 
 // What the pack kernel reads, passed by value. The run table (sample
@@ -99,7 +107,7 @@ struct PackArgsT {
   int32_t n_tokens;           // total rows
   int32_t row_bytes;
   int32_t page_tokens;
-  int32_t tier_mask;
+  int32_t tier_mask;          // FP_TIER_MASK_* bits, plus kTablePlainLoads
   uint64_t pt_mul;            // v / page_tokens == (v * pt_mul) >> pt_shift for v < 2^31
   uint64_t pb_mul;            // d / page_bytes == umulhi64(d, pb_mul) >> pb_shift for d < 2^52
   int32_t pt_shift;

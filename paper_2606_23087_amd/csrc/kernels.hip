@@ -32,11 +32,11 @@ __device__ __forceinline__ u32x4 load16(const uint8_t* p) {
   return __builtin_nontemporal_load((g_u32x4_c*)p);
 }
 
-// Embedding-table rows are read at random ids, a few KiB each, so the
-// streaming hint does not fit them: with plain loads a gather of random
-// 7 KiB table rows measured about 9 % faster than with non-temporal ones,
-// while rows read in page order are about 2 % faster non-temporal. The
-// policy is an instruction bit, so the pack picks it per chunk.
+// Embedding-table rows are read at random ids, a few KiB each, and may be
+// read again by later packs: plain loads let the memory-side cache keep
+// them (see kTablePlainLoads), while rows read in page order are about 2 %
+// faster non-temporal. The policy is an instruction bit, so the pack picks
+// it per chunk.
 __device__ __forceinline__ u32x4 load16_table(const uint8_t* p) {
   return *(g_u32x4_c*)p;
 }
@@ -281,7 +281,8 @@ __global__ __launch_bounds__(kPackBlock) void k_pack(int32_t g0, int32_t g1, int
   for (int w = 0; w < kPackBlock / 64; ++w) flags |= s_flags[w];
   flags = __builtin_amdgcn_readfirstlane(flags);   // the same in every lane
   const bool skip = (flags & 1) != 0;
-  const bool table = (flags & 2) != 0;           // plain loads for the whole chunk
+  // Plain loads for the whole chunk (for tables small enough to cache).
+  const bool table = (flags & 2) != 0 && (a.tier_mask & kTablePlainLoads) != 0;
 
   // Vector e of the chunk belongs to row e / vpr (multiply-shift division).
   // A vector is live if it lies in the chunk and its row is copied; only
@@ -529,69 +530,71 @@ __device__ __forceinline__ void chunk_range(int32_t g0, int32_t g1, int32_t t1, 
   }
 }
 
+// The pack's copy of one chunk's vectors (see k_pack): full chunks and the
+// two tail sizes unpredicated, the last chunk predicated per vector.
+template <int VPT, bool kTable>
+__device__ __forceinline__ void copy_chunk(const uint64_t* from, const bool* live, uint8_t* dst, int v0, int v1) {
+  constexpr int kT1 = kTail1Vecs / kPackBlock, kT2 = kTail2Vecs / kPackBlock;
+  const int tid = (int)threadIdx.x;
+  if (v1 - v0 == kPackBlock * VPT) copy_vectors<VPT, kTable, true>(from, live, dst, v0, tid);
+  else if (v1 - v0 == kTail1Vecs) copy_vectors<kT1, kTable, true>(from, live, dst, v0, tid);
+  else if (v1 - v0 == kTail2Vecs) copy_vectors<kT2, kTable, true>(from, live, dst, v0, tid);
+  else copy_vectors<VPT, kTable, false>(from, live, dst, v0, tid);
+}
+
 template <int VPT>
 __global__ __launch_bounds__(kPackBlock) void k_copy(int32_t g0, int32_t g1, int32_t t1, int32_t t2, int32_t total,
                                                       const uint8_t* src, uint8_t* dst) {
   int v0, v1;
   chunk_range<VPT>(g0, g1, t1, t2, total, &v0, &v1);
-  u32x4 v[VPT];
-  if (v1 - v0 == kPackBlock * VPT) {
+  uint64_t from[VPT];
+  bool live[VPT];
 #pragma unroll
-    for (int u = 0; u < VPT; ++u) v[u] = load16(src + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16);
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
-  } else {
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int e = v0 + u * kPackBlock + (int)threadIdx.x;
-      if (e < v1) v[u] = load16(src + (size_t)e * 16);
-    }
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int e = v0 + u * kPackBlock + (int)threadIdx.x;
-      if (e < v1) store16(dst + (size_t)e * 16, v[u]);
-    }
+  for (int u = 0; u < VPT; ++u) {
+    const int e = v0 + u * kPackBlock + (int)threadIdx.x;
+    live[u] = e < v1;
+    from[u] = live[u] ? reinterpret_cast<uint64_t>(src) + (uint64_t)e * 16 : 0;
   }
+  copy_chunk<VPT, false>(from, live, dst, v0, v1);
 }
 
-// Output row r is the row_bytes bytes at address rows_src[r].
+// Output row r is the row_bytes bytes at address rows_src[r] & ~15; bit 0 of
+// an entry marks an embedding-table row, and a chunk holding one takes the
+// pack's plain loads.
 template <int VPT>
 __global__ __launch_bounds__(kPackBlock) void k_gather(int32_t g0, int32_t g1, int32_t t1, int32_t t2, int32_t total,
                                                         uint64_t div_mul, int32_t div_shift, int32_t row_bytes,
                                                         const uint64_t* rows_src, uint8_t* dst) {
   extern __shared__ __align__(16) uint64_t s_src[];
+  __shared__ int32_t s_table;
   int v0, v1;
   chunk_range<VPT>(g0, g1, t1, t2, total, &v0, &v1);
   auto div_row = [&](int e) { return (int)(((uint64_t)(uint32_t)e * div_mul) >> div_shift); };
   const int vpr = row_bytes >> 4;
   const int r0 = div_row(v0);
   const int rows = v1 > v0 ? div_row(v1 - 1) - r0 + 1 : 0;
-  for (int t = threadIdx.x; t < rows; t += kPackBlock) s_src[t] = rows_src[r0 + t];
+  if (threadIdx.x == 0) s_table = 0;
   __syncthreads();
-  u32x4 v[VPT];
+  for (int t = threadIdx.x; t < rows; t += kPackBlock) {
+    const uint64_t x = rows_src[r0 + t];
+    s_src[t] = x & ~(uint64_t)15;
+    if (x & 1) s_table = 1;
+  }
+  __syncthreads();
   uint64_t from[VPT];
+  bool live[VPT];
 #pragma unroll
   for (int u = 0; u < VPT; ++u) {
     const int e = v0 + u * kPackBlock + (int)threadIdx.x;
+    live[u] = e < v1;
     from[u] = 0;
-    if (e < v1) {
+    if (live[u]) {
       const int row = div_row(e);
       from[u] = s_src[row - r0] + (uint64_t)(e - row * vpr) * 16;
     }
   }
-  if (v1 - v0 == kPackBlock * VPT) {
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
-  } else {
-#pragma unroll
-    for (int u = 0; u < VPT; ++u)
-      if (from[u]) v[u] = load16(reinterpret_cast<const uint8_t*>(from[u]));
-#pragma unroll
-    for (int u = 0; u < VPT; ++u)
-      if (from[u]) store16(dst + (size_t)(v0 + u * kPackBlock + threadIdx.x) * 16, v[u]);
-  }
+  if (__builtin_amdgcn_readfirstlane(s_table)) copy_chunk<VPT, true>(from, live, dst, v0, v1);
+  else copy_chunk<VPT, false>(from, live, dst, v0, v1);
 }
 
 // The pack's chunk geometry for `vecs` vectors of rows of row_bytes bytes.

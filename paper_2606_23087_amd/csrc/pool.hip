@@ -1472,7 +1472,8 @@ static fp_status pack_impl(fp_pool* p, const uint64_t* sample_ids, int32_t n, co
   a.n_tokens = (int32_t)total;
   a.row_bytes = (int32_t)p->rb;
   a.page_tokens = p->cfg.page_tokens;
-  a.tier_mask = tier_mask;
+  const bool plain_table = vocab >= 0 && vocab <= fp::kPlainTableMaxBytes / p->rb;
+  a.tier_mask = tier_mask | (plain_table ? fp::kTablePlainLoads : 0);
   a.pt_mul = p->dv.pt_mul;
   a.pt_shift = p->dv.pt_shift;
   a.pb_mul = p->dv.pb_mul;

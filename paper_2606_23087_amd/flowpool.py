@@ -392,7 +392,8 @@ def fp_copy_bytes(src, dst, nbytes: int, row_bytes: int, stream=None) -> None:
 
 
 def fp_gather_rows(rows_src, n_rows: int, row_bytes: int, dst, stream=None) -> None:
-    """Measurement aid: dst row r = the row at device address rows_src[r] (a device int64 tensor)."""
+    """Measurement aid: dst row r = the row at device address rows_src[r] & ~15 (a device int64
+    tensor; bit 0 set marks an embedding-table row, read as the pack reads those)."""
     _check(_lib.fp_gather_rows(_buf(rows_src, 8 * n_rows, "rows_src", None), n_rows, row_bytes,
                                _buf(dst, n_rows * row_bytes, "dst", None), _stream(stream)), "fp_gather_rows")
 

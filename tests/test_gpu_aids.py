@@ -2,7 +2,7 @@
 give the benchmark its same-run ceilings, do what they claim: byte-exact
 copies and gathers at sizes that end in every chunk stage (full chunks, both
 shrinking tail sizes, a ragged last chunk), for rows that take 12 KiB and
-8 KiB chunks."""
+8 KiB chunks, with and without table-row marks on the gathered rows."""
 
 import numpy as np
 import pytest
@@ -34,13 +34,14 @@ def test_copy_bytes(fp, nbytes, row_bytes):
     assert torch.equal(dst[:nbytes], src[16:16 + nbytes]) and not bool(dst[nbytes:].any())
 
 
-@pytest.mark.parametrize("n_rows,hidden", [(1, 8), (333, 3584), (16000, 3584), (2500, 8192), (7, 5120)])
+@pytest.mark.parametrize("n_rows,hidden", [(1, 8), (333, 3584), (16000, 3584), (16001, 3584), (2500, 8192), (7, 5120)])
 def test_gather_rows(fp, n_rows, hidden):
     say(f"case gather aid: {n_rows} rows, H={hidden}")
     rng = np.random.default_rng(n_rows)
     table = torch.from_numpy(rng.integers(-2 ** 15, 2 ** 15, size=(4096, hidden), dtype=np.int16)).to("cuda")
     pick = rng.integers(0, 4096, size=n_rows)
     addr = table.data_ptr() + pick.astype(np.int64) * 2 * hidden
+    addr |= rng.integers(0, 2, size=n_rows) * (n_rows % 2)      # table-row marks (bit 0) on odd cases
     out = torch.zeros((n_rows + 2, hidden), dtype=torch.int16, device="cuda")
     fp.fp_gather_rows(torch.from_numpy(addr).to("cuda"), n_rows, 2 * hidden, out)
     torch.cuda.synchronize()
