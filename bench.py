@@ -751,9 +751,11 @@ def main() -> int:
     seeds = [int(x) for x in str(args.seeds).split(",")] if not (args.prefetch or args.concurrent) else [args.seed]
     log(f"workload {cfg.name}: H={cfg.hidden} P={cfg.page_tokens} C={cfg.capacity} M={cfg.n_mb}, seeds {seeds}")
     works = {}
+    table = None          # the seeds' workloads read one embedding table, as the steps of one job do
     for sd in seeds:
         t_setup = time.perf_counter()
-        works[sd] = GpuWorkload(cfg, sd, mode="normal", log=log)
+        works[sd] = GpuWorkload(cfg, sd, mode="normal", log=log, table=table)
+        table = works[sd].table
         log(f"seed {sd}: pool built, {len(works[sd].ids)} samples in {time.perf_counter() - t_setup:.1f} s, "
             f"{fp.pool_stats(works[sd].pool)}")
     s0 = seeds[0]
@@ -950,7 +952,8 @@ def main() -> int:
         "config": {"workload": f"{cfg.name}-h{cfg.hidden}", "hidden": cfg.hidden, "page_tokens": cfg.page_tokens,
                    "pool_pages": cfg.hbm_pages + cfg.host_pages, "alloc": cfg.alloc, "capacity": cfg.capacity,
                    "n_mb": cfg.n_mb, "cost_k": cfg.cost_k, "samples": len(w.ids),
-                   "seeds": seeds, "steps_cycle_seeds": True, "parallelism": "none (1 GPU)"},
+                   "seeds": seeds, "steps_cycle_seeds": True, "table": f"one embedding table (seed {s0}'s) for all seeds",
+                   "parallelism": "none (1 GPU)"},
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "tokens_per_s": round(main_t["tokens"] / main_t["wall"], 1),
         "step_tokens": info[s0]["tokens"],
