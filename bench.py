@@ -246,6 +246,39 @@ def tier_split(cfg, w, mbs, spec_of, outs, stream, reps: int = 3):
             "one_full_pack_ms": round(t_all * 1e3, 3)}
 
 
+def aux_tiered(args) -> dict:
+    """The tiered workload (seed 0) beside the headline: the HBM-tier part
+    (text rows and rows on HBM pages) and the host-tier part (rows on pinned
+    host pages, read over PCIe) of each microbatch as separate masked packs,
+    each timed over ``max(3, steps // 2)`` passes after one warm pass, with
+    the gather ceiling of the HBM part and a pinned host-to-device copy rate."""
+    import torch
+
+    from paper_2606_23087_amd.harness import GpuWorkload
+    from paper_2606_23087_amd.workloads import CONFIGS
+
+    cfg = CONFIGS["tiered"]
+    w = GpuWorkload(cfg, 0, mode="normal")
+    try:
+        stream = torch.cuda.Stream()
+        plan = w.plan(stream=stream)
+        mbs = w.microbatches(plan)
+        spec_of = {sid: sp for sid, sp in zip(w.ids, w.specs)}
+        outs = [w.alloc_outputs() for _ in range(4)]
+        tiers = tier_split(cfg, w, mbs, spec_of, outs, stream, reps=1)          # warm pass
+        tiers = tier_split(cfg, w, mbs, spec_of, outs, stream, reps=max(3, args.steps // 2))
+        tiers["hbm_tier"]["frac"] = round(tiers["hbm_tier"]["GBps"] / HBM_PEAK_GBPS, 4)
+        tiers["host_tier"]["frac_of_pcie"] = round(tiers["host_tier"]["GBps"] / PCIE_PEAK_GBPS, 4)
+        tiers["h2d_copy_GBps"] = round(h2d_ceiling(), 1)
+        tiers["config"] = {"workload": f"{cfg.name}-h{cfg.hidden}", "seed": 0, "microbatches": len(mbs),
+                           "passes": max(3, args.steps // 2)}
+        log(f"aux tiered: HBM part {tiers['hbm_tier']['GBps']} GB/s ({tiers['hbm_tier']['frac']}), host part "
+            f"{tiers['host_tier']['GBps']} GB/s over PCIe")
+        return tiers
+    finally:
+        w.close()
+
+
 def row_sources(cfg, w, mb, spec_of, tiers=False):
     """Device address of the source of every row of microbatch ``mb``, in
     pack order (text rows: their table row, with bit 0 set to mark it as one;
@@ -725,6 +758,9 @@ def main() -> int:
                          "non-temporal ones, over tables of several sizes")
     ap.add_argument("--concurrent", action="store_true",
                     help="time the packs alone and under a concurrent producer on another stream")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="skip the auxiliary legs the headline run adds to its line (the tiered workload's "
+                         "two tier parts, and the packs under a concurrent producer)")
     args = ap.parse_args()
 
     if args.scheduler:
@@ -996,6 +1032,24 @@ def main() -> int:
         result["cpu_baseline"] = cpu_baseline(cfg, w, mbs, s0, args.cpu_budget)
     else:
         result["cpu_baseline"] = None
+    if cfg.name == "qwen" and args.mask == "all" and not args.no_aux:
+        # Auxiliary legs, after everything above is measured: the packs of
+        # this workload under a concurrent producer, then the tiered
+        # workload's two tier parts. An error in one is recorded in the line.
+        # The pools stay resident until the end: the device clears freed
+        # memory in the background, which would take bandwidth from the legs.
+        aux = {}
+        try:
+            log("aux: packs under a concurrent producer")
+            aux["concurrent"] = concurrent_bench(args, cfg, w, mbs, spec_of[s0], outs, pack_stream)
+        except Exception as e:                     # noqa: BLE001 - recorded, the headline stands
+            aux["concurrent"] = {"error": repr(e)}
+        try:
+            log("aux: tiered workload, tier parts")
+            aux["tiered"] = aux_tiered(args)
+        except Exception as e:                     # noqa: BLE001
+            aux["tiered"] = {"error": repr(e)}
+        result["aux"] = aux
     for wk in works.values():
         wk.close()
     print(json.dumps(result), flush=True)

@@ -49,3 +49,26 @@ def test_json_line_fields():
     assert ce["copy_GBps"] > 0 and ce["gather_GBps"] > 0 and ce["pack_over_gather"] > 0
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] == 1 and cb["value"] > 0 and cb["unit"] and cb["sample"]
+
+
+@pytest.mark.gpu
+def test_headline_line_carries_the_auxiliary_legs():
+    """The headline workload's line also carries the tiered workload's two
+    tier parts and the packs under a concurrent producer."""
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    print("case bench contract: qwen workload with auxiliary legs, 2 steps", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "2", "--warmup", "1",
+                        "--no-cpu-baseline"], capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    d = json.loads([ln for ln in r.stdout.splitlines() if ln.strip()][-1])
+    assert d["config"]["workload"] == "qwen-h3584"
+    conc, tiers = d["aux"]["concurrent"], d["aux"]["tiered"]
+    assert "error" not in conc and "error" not in tiers, d["aux"]
+    assert conc["pack_alone_GBps"] > 0 and conc["pack_with_producer_GBps"] > 0 and conc["producer_writes"] > 0
+    assert conc["producer_error"] is None
+    assert tiers["config"]["workload"] == "tiered-h4096"
+    assert 0 < tiers["hbm_tier"]["frac"] < 1 and tiers["hbm_tier"]["gather_ceiling_GBps"] > 0
+    assert 0 < tiers["host_tier"]["GBps"] < tiers["host_tier"]["peak"] * 1.2
+    assert 0 < tiers["host_tier_row_fraction"] < 1
