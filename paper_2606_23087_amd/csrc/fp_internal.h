@@ -65,7 +65,8 @@ struct alignas(16) PackRun {
   int32_t vdelta;     // image run: visual index of row r is r + vdelta
   int32_t word;       // text run: the id of row r is 32-bit word word + r of the
                       // arena; image run: the sample's page GVAs start at
-                      // 64-bit word `word`
+                      // 64-bit word `word`, or, when its pages have
+                      // consecutive GVAs, -1 - (page number of its first page)
 };
 static_assert(sizeof(PackRun) == 16, "PackRun layout");
 constexpr int32_t kTextRun = INT32_MIN;

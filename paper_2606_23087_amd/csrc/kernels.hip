@@ -132,16 +132,24 @@ __device__ __forceinline__ PackRun run_of(const RunIndex& x, int32_t off_runs, c
   return r;
 }
 
-// Row of physical memory holding visual row `vidx` of the sample whose page
-// GVAs start at 64-bit word `word` of the arena: visual index -> page GVA
-// (the sample's page list) -> page-table entry (the GVA's page number) -> row
-// in the physical page. Returns the page-table entry's flags in *flags.
+// Row of physical memory holding visual row `vidx` of an image run: visual
+// index -> page GVA -> page-table entry (the GVA's page number) -> row in the
+// physical page. `word` >= 0: the sample's page GVAs start at 64-bit word
+// `word` of the arena (the page list). `word` < 0: the sample's pages have
+// consecutive GVAs, page lp's GVA is page 0's plus lp pages, and -word - 1 is
+// page 0's page number, so the page number needs no load. Returns the
+// page-table entry's flags in *flags.
 template <bool kScalar, class Args>
 __device__ __forceinline__ uint64_t walk(const Args& a, int32_t word, uint32_t vidx, uint64_t* flags) {
   const int lp = (int)(((uint64_t)vidx * a.pt_mul) >> a.pt_shift);
   const int in_page = (int)vidx - lp * a.page_tokens;
-  const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)word + lp));
-  const uint64_t vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
+  uint64_t vpn;
+  if (word < 0) {
+    vpn = (uint64_t)(-(int64_t)word - 1) + (uint64_t)lp;
+  } else {
+    const uint64_t gva = ld<kScalar, uint64_t>(a.meta + 8 * ((int64_t)word + lp));
+    vpn = __umul64hi(gva - a.gva_start, a.pb_mul) >> a.pb_shift;
+  }
   const uint64_t pte = ld<kScalar, uint64_t>(a.pte + vpn);
   *flags = pte;
   return (pte & PTE_ADDR_MASK) + (uint64_t)in_page * (uint64_t)a.row_bytes;

@@ -1388,6 +1388,25 @@ fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, i
   });
 }
 
+// The word of a sample's image runs: its page list's arena word index, or,
+// when its pages have consecutive GVAs (a contiguous allocation), -1 - the
+// page number of its first page, from which the kernel computes every page's
+// number without reading the list. Only rows packed in 12 KiB chunks take
+// the shortcut: same-machine A/B, qwen (H 3584) 0.45 % faster per launch,
+// video (H 5120, 8 KiB chunks) 0.3 % slower with it.
+static int32_t image_word(const fp_pool* p, const SampleRec& r) {
+  const size_t n = r.pages.size();
+  if (n > 0 && p->rb < fp::kSmallChunkRowBytes) {
+    const uint64_t pb = (uint64_t)p->pb;
+    const uint64_t first = r.pages[0];
+    bool consecutive = true;
+    for (size_t k = 1; k < n && consecutive; ++k) consecutive = r.pages[k] == first + k * pb;
+    const int64_t vpn0 = (int64_t)((first - p->gva_start) / pb);
+    if (consecutive && vpn0 + (int64_t)n < INT32_MAX) return (int32_t)(-1 - vpn0);
+  }
+  return (int32_t)(r.page_off / 8);
+}
+
 // Bucket index of runs covering rows [0, total) (run k starts where run k-1
 // ends): at most max_buckets buckets of 2^shift rows; bucket b gets the run
 // holding its first row and that run's number. Returns the bucket count.
@@ -1508,7 +1527,7 @@ static fp_status pack_impl(fp_pool* p, const uint64_t* sample_ids, int32_t n, co
         if (nt <= 0) continue;
         if (!in_image) {
           if (n_runs) runs[n_runs - 1].end = row;
-          runs[n_runs++] = fp::PackRun{0, s0, vis - row, (int32_t)(r.page_off / 8)};
+          runs[n_runs++] = fp::PackRun{0, s0, vis - row, image_word(p, r)};
           in_image = true;
         }
         row += nt;
