@@ -673,6 +673,47 @@ def table_policy_bench(args) -> int:
     return 0
 
 
+def copy_sizes_bench(args) -> int:
+    """The library's plain copy kernel (the pack's chunk geometry and cache
+    policy, rows of 7168 bytes) at launch sizes from one qwen microbatch (230
+    MB moved) to sixteen, so the copy's steady rate and the fixed cost of a
+    launch's ramp and drain can be read apart: about as many bytes per size,
+    sources walked forward through 8 GiB, destinations alternating between
+    two buffers, one event pair around all launches of a size (after one
+    untimed pass)."""
+    import torch
+
+    from paper_2606_23087_amd import flowpool as fp
+
+    time.sleep(max(0.0, args.settle - seconds_since_start()))
+    rb = 7168
+    src = torch.empty(8 << 30, dtype=torch.uint8, device="cuda")
+    dst = [torch.empty(4 << 30, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    stream = torch.cuda.current_stream()
+    res = []
+    for mult in (1, 2, 4, 8, 16):
+        n = (115 * 1000 * 1000 * mult) // rb * rb          # bytes read (and written) per launch
+        launches = max(4, 64 // mult)
+        for rep in range(2):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for j in range(launches):
+                off = (j * n) % ((8 << 30) - n)
+                fp.fp_copy_bytes(src.data_ptr() + off - off % 256, dst[j % 2], n, rb, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / launches
+        res.append({"moved_MB": round(2 * n / 1e6, 1), "launches": launches, "us_per_launch": round(us, 3),
+                    "GBps": round(2 * n / us / 1e3, 1), "frac": round(2 * n / us / 1e3 / HBM_PEAK_GBPS, 4)})
+        log(f"copy sizes: {res[-1]}")
+    print(json.dumps({
+        "metric": "plain copy kernel with the pack's geometry, by launch size", "value": max(r["GBps"] for r in res),
+        "unit": "GB/s", "higher_is_better": True, "n_gpus": 1, "data": "synthetic",
+        "config": {"workload": "copy-sizes", "row_bytes": rb}, "per_size": res}), flush=True)
+    return 0
+
+
 def allocator_bench(args) -> int:
     """Time of the allocator's flow matching (Eq. 2) on the host for clusters
     of 8-device nodes (global batch 512, a 28-layer backbone, two encoders),
@@ -758,6 +799,8 @@ def main() -> int:
                          "non-temporal ones, over tables of several sizes")
     ap.add_argument("--concurrent", action="store_true",
                     help="time the packs alone and under a concurrent producer on another stream")
+    ap.add_argument("--copy-sizes", action="store_true",
+                    help="time the library's plain copy kernel at launch sizes from 230 MB to 3.7 GB moved")
     ap.add_argument("--no-aux", action="store_true",
                     help="skip the auxiliary legs the headline run adds to its line (the tiered workload's "
                          "two tier parts, and the packs under a concurrent producer)")
@@ -774,6 +817,8 @@ def main() -> int:
 
     if args.table_policy:
         return table_policy_bench(args)
+    if args.copy_sizes:
+        return copy_sizes_bench(args)
 
     import numpy as np
     import torch
