@@ -30,10 +30,14 @@ position advances with every sample, placed or deferred.
 Brute force enumerates every assignment for tiny inputs to give the optimal
 max-cost partition.
 
-Parity unpinned: the tie rules of both policies are readings (the paper
-states none); only hand-worked partitions written from them check which of
-several equally good assignments is chosen. The assignment's quality is
-pinned against brute force and Graham's bound for LPT.
+The tie rules of both policies are readings (the paper states none). They
+are pinned by hand-worked partitions written from them (with equal lengths,
+exact fits and deferrals) and by a check of the output alone: replayed in
+the samples' turn order, each placed sample went where the rule sends it
+(least cost with room, lowest index among equals; or the first microbatch
+with room along the snake) and each deferred one fit nowhere. The
+assignment's quality is pinned against brute force and Graham's bound for
+LPT.
 """
 
 from __future__ import annotations

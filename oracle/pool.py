@@ -27,11 +27,16 @@ freeing pushes a sample's pages back last-page-first, so an equal-sized
 write right after gets the same pages in the same order; allocation is
 all-or-nothing.
 
-Parity unpinned: the two allocation policies and the free order are readings
-(the paper names no allocator); only hand-worked sequences written from those
-readings check them. Everything the pack reads through them (GVA ->
-page-table entry -> frame) is pinned by placement independence instead: the
-pack equals the plain definition whatever frames the allocator picks.
+The two allocation policies and the free order are readings (the paper
+names no allocator). They are pinned by hand-worked sequences written from
+them and by properties that state each reading without its algorithm: under
+"contig" every write takes the lowest-index run of free pages found among
+the pages no live sample's page list holds, and fails exactly when there is
+none; under "scatter" a model that ranks the free pages of a tier by when
+they were given back (no stacks) picks the same page for every write and
+migration. Everything the pack reads through them (GVA -> page-table entry
+-> frame) is pinned by placement independence as well: the pack equals the
+plain definition whatever frames the allocator picks.
 
 The physical memory here is a dict of numpy page frames per tier,
 materialised only when written.

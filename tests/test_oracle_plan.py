@@ -147,3 +147,60 @@ def test_zigzag_properties(seed):
             if a < 0:                             # nor after (token counts only grow)
                 assert all(t + lengths[i] > capacity for t in tok)
     assert zigzag_partition(lengths, k, 300, 1) == greedy_partition(lengths, k, 300, 1)
+
+
+def _turns(lengths, k):
+    """Samples in the order both policies take them: decreasing cost, ties by lower index."""
+    costs = [cost_scaled(int(l), k) for l in lengths]
+    return sorted(range(len(lengths)), key=lambda i: (-costs[i], i)), costs
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_greedy_certificate(seed):
+    """Reading R11, checked on the output alone: replaying the assignment in
+    the samples' turn order, each placed sample went to a microbatch of
+    least accumulated cost among those with room at its turn, the lowest
+    index among equals, and each deferred sample fit in none. Random inputs
+    with many equal lengths, so the tie rules decide often."""
+    rng = np.random.default_rng(500 + seed)
+    n, n_mb = int(rng.integers(1, 30)), int(rng.integers(1, 6))
+    lengths = [int(x) for x in rng.choice([1, 2, 3, 5, 8, 13], size=n)]
+    capacity, k = int(rng.integers(8, 40)), int(rng.choice([1, 10, 4096]))
+    assign, tok, cst = greedy_partition(lengths, k, capacity, n_mb)
+    order, costs = _turns(lengths, k)
+    t, c = [0] * n_mb, [0] * n_mb
+    for i in order:
+        room = [j for j in range(n_mb) if t[j] + lengths[i] <= capacity]
+        if not room:
+            assert assign[i] == -1
+            continue
+        least = min(c[j] for j in room)
+        assert assign[i] == min(j for j in room if c[j] == least)
+        t[assign[i]] += lengths[i]
+        c[assign[i]] += costs[i]
+    assert t == tok and c == cst
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_zigzag_certificate(seed):
+    """Reading R11's zig-zag form, checked on the output alone: the sample
+    at turn p went to the first microbatch with room along the snake from
+    position p (0, 1, ..., M-1, M-1, ..., 0, 0, 1, ...), and a deferred one
+    found room in none."""
+    rng = np.random.default_rng(600 + seed)
+    n, n_mb = int(rng.integers(1, 30)), int(rng.integers(1, 6))
+    lengths = [int(x) for x in rng.choice([1, 2, 3, 5, 8, 13], size=n)]
+    capacity, k = int(rng.integers(8, 40)), int(rng.choice([1, 10, 4096]))
+    assign, tok, cst = zigzag_partition(lengths, k, capacity, n_mb)
+    order, costs = _turns(lengths, k)
+    walk = [x for x in range(n_mb)] + [x for x in reversed(range(n_mb))]     # one period of the snake
+    t = [0] * n_mb
+    for p, i in enumerate(order):
+        along = [walk[(p + q) % (2 * n_mb)] for q in range(2 * n_mb)]
+        room = [j for j in along if t[j] + lengths[i] <= capacity]
+        if not room:
+            assert assign[i] == -1
+            continue
+        assert assign[i] == room[0]
+        t[assign[i]] += lengths[i]
+    assert t == tok

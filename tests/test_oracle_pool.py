@@ -240,3 +240,112 @@ def test_migration_keeps_bytes_and_conserves_pages():
         pool.migrate(sid, 0)
         assert all(pool.translate(g)[0] == 0 for g in pool.sample_pages(sid))
     assert np.array_equal(pool.pack(ids, table)[0], want)
+
+
+def _held(pool, live):
+    """(tier, page index) of every page held by the live samples, from their page lists."""
+    return {pool._page_of(g) for sid in live for g in pool.sample_pages(sid)}
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_contig_first_fit_certificate(seed):
+    """Reading R6, contig: every write takes the lowest-index run of free
+    pages of its length in the HBM tier, else in the host tier, and fails
+    exactly when neither tier has such a run. Checked from the outside on
+    random writes and frees: the free pages are those no live sample's page
+    list holds, and the run is searched for among them, not in the pool's
+    own state."""
+    rng = np.random.default_rng(300 + seed)
+    n_pages = (40, 24)
+    pool = OraclePool(hidden=8, page_tokens=3, hbm_pages=n_pages[0], host_pages=n_pages[1], alloc="contig")
+    live = []
+
+    def lowest_run(held, n):
+        for t in (0, 1):
+            run = 0
+            for i in range(n_pages[t]):
+                run = 0 if (t, i) in held else run + 1
+                if run == n:
+                    return [(t, j) for j in range(i - n + 1, i + 1)]
+        return None
+
+    for step in range(500):
+        if live and rng.integers(0, 3) == 0:
+            pool.free(live.pop(int(rng.integers(0, len(live)))))
+            continue
+        n_vis = int(rng.integers(1, 3 * 20))
+        n = -(-n_vis // 3)
+        want = lowest_run(_held(pool, live), n)
+        try:
+            sid = pool.write([1], [0], [n_vis])
+        except PoolError as e:
+            assert e.code == "ENOMEM" and want is None
+            continue
+        live.append(sid)
+        assert [pool._page_of(g) for g in pool.sample_pages(sid)] == want
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_scatter_lifo_against_a_timestamp_model(seed):
+    """Reading R6, scatter: a page goes to the wished tier, or the other one
+    when the wished tier has no free page; within a tier the page taken is
+    the one freed most recently (a free gives its last page back first, so
+    the first page comes back on top), and a never-used page after all freed
+    ones, lowest index first. The model keeps no stacks: each free page of a
+    tier carries a rank (a never-used page i: -i; a freed page: a counter
+    that grows with every page given back) and a write takes the highest
+    rank. Random writes with random tier wishes, frees and migrations."""
+    rng = np.random.default_rng(400 + seed)
+    n_pages = (30, 30)
+    P = 2
+    pool = OraclePool(hidden=8, page_tokens=P, hbm_pages=n_pages[0], host_pages=n_pages[1], alloc="scatter")
+    rank = [{i: -i for i in range(n_pages[t])} for t in (0, 1)]     # free pages of each tier -> rank
+    clock = [0]
+
+    def give_back(pages):                       # pages in a sample's order; the last one is given back first
+        for t, i in reversed(pages):
+            clock[0] += 1
+            rank[t][i] = clock[0]
+
+    def take(t):
+        i = max(rank[t], key=rank[t].get)
+        del rank[t][i]
+        return (t, i)
+
+    live = {}
+    for step in range(600):
+        op = rng.integers(0, 5)
+        if live and op == 0:
+            sid = list(live)[int(rng.integers(0, len(live)))]
+            pool.free(sid)
+            give_back(live.pop(sid))
+        elif live and op == 1:
+            sid = list(live)[int(rng.integers(0, len(live)))]
+            tier = int(rng.integers(0, 2))
+            moving = [k for k, p in enumerate(live[sid]) if p[0] != tier]
+            try:
+                pool.migrate(sid, tier)
+            except PoolError as e:
+                assert e.code == "ENOMEM" and len(moving) > len(rank[tier])
+                continue
+            old = [live[sid][k] for k in moving]
+            for k in moving:
+                live[sid][k] = take(tier)
+            give_back(old)
+            assert [pool._page_of(g) for g in pool.sample_pages(sid)] == live[sid]
+        else:
+            n_vis = int(rng.integers(1, 2 * 12))
+            n = -(-n_vis // P)
+            wish = rng.integers(0, 2, size=n).astype(np.uint8)
+            free = [len(rank[0]), len(rank[1])]
+            try:
+                sid = pool.write([1], [0], [n_vis], tier_wish=wish)
+            except PoolError as e:
+                assert e.code == "ENOMEM" and n > free[0] + free[1]
+                continue
+            want = []
+            for w in wish.tolist():
+                t = w if rank[w] else 1 - w
+                want.append(take(t))
+            live[sid] = want
+            assert [pool._page_of(g) for g in pool.sample_pages(sid)] == want
