@@ -14,7 +14,7 @@ import numpy as np
 import pytest
 
 from oracle.pool import MASK_HBM, MASK_HOST, OraclePool, PoolError
-from paper_2606_23087_amd.workloads import CONFIGS, churn_ops, gen_samples, scaled
+from paper_2606_23087_amd.workloads import CONFIGS, SampleSpec, churn_ops, gen_samples, scaled
 from tagging import tagged_table, tagged_vis
 from conftest import read_golden
 
@@ -191,6 +191,39 @@ def test_tier_mask_split_equals_full():
     b = pool.pack(ids, table, tier_mask=MASK_HOST, out=out)
     assert b[1] is None
     assert np.array_equal(out, full[0]) and np.array_equal(a[1], full[1]) and np.array_equal(a[2], full[2])
+
+
+def test_tier_masks_on_samples_wholly_on_one_tier():
+    """Reading R17 on a case checked by eye: sample A has every page on the
+    host tier, sample B every page in HBM (the tier wishes are honoured while
+    both tiers have room). The HBM mask writes the text rows of both and B's
+    image rows and leaves A's image rows as they were; the host mask writes
+    A's image rows only and produces no cu_seqlens or position ids."""
+    H, P = 8, 2
+    pool = OraclePool(H, P, 8, 8, "scatter", 20)
+    table = tagged_table(20, H)
+    spec_a = SampleSpec(np.array([3, 4, 5], np.int32), np.array([1], np.int32), np.array([3], np.int32))
+    spec_b = SampleSpec(np.array([6, 7], np.int32), np.array([2], np.int32), np.array([4], np.int32))
+    a = pool.write(spec_a.text_ids, spec_a.img_pos, spec_a.img_ntok, tagged_vis(0, 3, H), tier_wish=[1, 1])
+    b = pool.write(spec_b.text_ids, spec_b.img_pos, spec_b.img_ntok, tagged_vis(1, 4, H), tier_wish=[0, 0])
+    assert [pool.translate(g)[0] for g in pool.sample_pages(a)] == [1, 1]
+    assert [pool.translate(g)[0] for g in pool.sample_pages(b)] == [0, 0]
+    # Packed rows: A = t3, v0..v2, t4, t5; B = t6, t7, v0..v3.
+    a_vis = [1, 2, 3]
+    full = pool.pack([a, b], table)
+    sentinel = 0x5A5A
+    out = np.full_like(full[0], sentinel)
+    hb = pool.pack([a, b], table, tier_mask=MASK_HBM, out=out)
+    untouched = np.all(out == sentinel, axis=1)
+    assert np.flatnonzero(untouched).tolist() == a_vis
+    assert np.array_equal(out[~untouched], full[0][~untouched])
+    assert hb[1].tolist() == [0, 6, 12] and hb[2].tolist() == [0, 1, 2, 3, 4, 5, 0, 1, 2, 3, 4, 5]
+    out = np.full_like(full[0], sentinel)
+    ho = pool.pack([a, b], table, tier_mask=MASK_HOST, out=out)
+    written = ~np.all(out == sentinel, axis=1)
+    assert np.flatnonzero(written).tolist() == a_vis
+    assert np.array_equal(out[written], full[0][written])
+    assert ho[1] is None and ho[2] is None
 
 
 def test_churn_sequence_is_feasible():

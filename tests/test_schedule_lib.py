@@ -66,3 +66,14 @@ def test_errors():
         fp.plan_dynamic_packing([5], 10, 1, 0)
     with pytest.raises(fp.FlowPoolError, match="EINVAL"):
         fp.plan_dynamic_packing([5], (1 << 20) + 1, 1, 1)
+
+
+def test_kmeans_tie_goes_to_the_lower_bucket():
+    """An exact k-means tie (reading R21: ties to the lower bucket). At L 33,
+    lengths 19, 26 and 32 each fill a microbatch of their own, with scaled
+    costs 988, 1534 and 2080; two buckets start at 988 and 2080, and 1534 lies
+    exactly between them, so it joins bucket 0, whose centroid then moves to
+    1261."""
+    got = _compare(np.array([19, 26, 32], np.int32), 33, 2, 2)
+    assert got["mb_cost_scaled"].tolist() == [988, 1534, 2080]
+    assert got["mb_bucket"].tolist() == [0, 0, 1]
