@@ -41,6 +41,9 @@ MUTANTS = [
     ("pack", "max_len = max(max_len, length)", "max_len = length", "max_seqlen of the last sample"),
     ("pack", "for s, spec in enumerate(samples):\n        sample_parts = []",
      "for s, spec in enumerate(samples[::-1]):\n        sample_parts = []", "samples packed in reverse order"),
+    ("pack", 'out.append(("vis", s, i))', 'out.append(("vis", s, i + 1))', "symbolic image row one off"),
+    ("pack", 'out.append(("text", s, int(spec.text_ids[i])))', 'out.append(("text", s, i))',
+     "symbolic text row names its position, not its id"),
     # Pool: GVA addressing, page table, allocators, walk, tiers (Sec. 3.2).
     ("pool", "base = self.gva_start + ((gva - self.gva_start) // self.pb) * self.pb",
      "base = self.gva_start + ((gva - self.gva_start) // self.pb + 1) * self.pb", "translation to the next page"),
@@ -73,6 +76,20 @@ MUTANTS = [
     ("pool", "        for gva in reversed(old):", "        for gva in old:", "migration returns its pages first page first"),
     ("pool", "t = int(wish[j]) if wish is not None else TIER_HBM", "t = 1 - int(wish[j]) if wish is not None else TIER_HBM",
      "tier wishes inverted"),
+    ("pool", "return t, (gva - self.seg_start[t]) // self.pb", "return t, (gva - self.seg_start[t]) // self.rb",
+     "page index from a row size"),
+    ("pool", "moving = [k for k, gva in enumerate(s.pages) if self._page_of(gva)[0] != tier]",
+     "moving = [k for k, gva in enumerate(s.pages) if self._page_of(gva)[0] == tier]", "migration moves the wrong pages"),
+    ("pool", "self.frames[nt][nf] = self.frames[ot][of].copy()", "self.frames[nt][nf] = self.frames[ot][of] * 0",
+     "migration drops the bytes"),
+    ("pool", "max_len = max((s.length for s in recs), default=0)", "max_len = sum((s.length for s in recs))",
+     "max_seqlen as the total"),
+    ("pool", "if out_rows_cap is not None and total > out_rows_cap:", "if out_rows_cap is not None and total >= out_rows_cap:",
+     "a microbatch that exactly fills the output refused"),
+    ("pool", "if p < 0 or p > T or (j and p < img_pos[j - 1]):", "if p < 0 or p >= T or (j and p < img_pos[j - 1]):",
+     "an image after the last text token refused"),
+    ("pool", "page[off // self.rb] = vis_rows[v]", "page[(off // self.rb) ^ 1] = vis_rows[v]",
+     "producer rows swapped in pairs inside a page"),
     # Planner: per-sample cost, Eq. 3, greedy and zig-zag partitions.
     ("plan", "return k * length + length * length", "return k * length + length", "cost without the square"),
     ("plan", "return sum(lengths) / capacity + (max(lengths) ** 2) / (capacity ** 2)",
@@ -94,6 +111,14 @@ MUTANTS = [
     ("plan", "return q if q < n_mb else 2 * n_mb - 1 - q", "return q if q < n_mb else 2 * n_mb - q",
      "snake turns one position late"),
     ("plan", "j = snake(p + q, n_mb)", "j = snake(p + q + 1, n_mb)", "snake starts one position late"),
+    ("plan", "out[j].append(i)", "out[j].insert(0, i)", "microbatch members in reverse input order"),
+    ("plan", "return (max(mb_cost) / mean) if mean > 0 else 1.0", "return (min(mb_cost) / mean) if mean > 0 else 1.0",
+     "imbalance from the cheapest microbatch"),
+    ("plan", "for q in range(2 * n_mb):", "for q in range(n_mb):", "zig-zag tries half the snake"),
+    ("plan", "if tok[j] > capacity:", "if tok[j] >= capacity:", "brute force with a strict capacity"),
+    ("plan", "        if all(j < n_mb for j in combo):", "        if any(j < n_mb for j in combo):",
+     "brute-force optimum over assignments that defer"),
+    ("plan", "key = (packed, -mx)", "key = (packed, mx)", "brute force prefers the costlier maximum"),
     # Alg. 1: best-fit packing, Eq. 3 cost, k-means buckets, zig-zag dealing.
     ("schedule", "if best < 0 or residual[j] < residual[best]:", "if best < 0 or residual[j] > residual[best]:",
      "worst fit instead of best fit"),
@@ -116,6 +141,13 @@ MUTANTS = [
     ("schedule", "for b in range(n_b - 1, -1, -1):", "for b in range(n_b):", "buckets dealt cheapest first"),
     ("schedule", "key=lambda j: (-costs[j], j))\n        for j, r in zip",
      "key=lambda j: (costs[j], j))\n        for j, r in zip", "a bucket dealt cheapest first"),
+    ("schedule", "centroid = [Fraction(costs[order[(2 * k + 1) * m // (2 * k_n)]]) for k in range(k_n)]",
+     "centroid = [Fraction(costs[order[k * m // k_n]]) for k in range(k_n)]", "k-means started at other positions"),
+    ("schedule", "            next_slot[r] += 1", "            next_slot[r] += 0", "slots not advanced"),
+    ("schedule", "return Fraction(cost_scaled(mb_lengths, capacity), capacity * capacity)",
+     "return Fraction(cost_scaled(mb_lengths, capacity), capacity)", "exact Eq. 3 over L"),
+    ("schedule", "if bins[b] + ls[i] <= capacity and bins[b] not in seen:",
+     "if bins[b] + ls[i] < capacity and bins[b] not in seen:", "optimal bin count with a strict capacity"),
     # Allocator: candidate pruning and the flow matching of Eq. 1-2.
     ("allocate", "g, f = min(t_enc, t_bb), abs(t_enc - t_bb)", "g, f = max(t_enc, t_bb), abs(t_enc - t_bb)",
      "throughput of the faster side instead of the slower"),
@@ -127,6 +159,11 @@ MUTANTS = [
     ("allocate", "if dp * tp * pp <= devices:", "if dp * tp * pp < devices:", "device bound made strict"),
     ("allocate", "pps = divisors(layers)", "pps = divisors(devices)", "PP degree not tied to the layers"),
     ("allocate", "for tp in divisors(per_node):", "for tp in divisors(devices):", "TP degree across nodes"),
+    ("allocate", "return [d for d in range(1, n + 1) if n % d == 0]", "return [d for d in range(1, n) if n % d == 0]",
+     "divisors without the number itself"),
+    ("allocate", "t_bb = bb[choice[-1]][0]", "t_bb = bb[choice[0]][0]", "backbone throughput read from an encoder's choice"),
+    ("allocate", "cost = sum(modules[i][c][1] for i, c in enumerate(choice))",
+     "cost = max(modules[i][c][1] for i, c in enumerate(choice))", "resources not summed over the modules"),
 ]
 
 

@@ -60,7 +60,12 @@ def test_worked_examples():
             a = _kv_lists(f[1:eq])
             opt, _ = brute_force(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
             assert opt == int(f[eq + 1])
-    assert seen == {"cost", "eq3", "greedy", "zigzag", "opt"}
+        elif f[0] == "lex":
+            eq = f.index("=")
+            a = _kv_lists(f[1:eq])
+            _, lex = brute_force(a["lengths"], a["K"][0], a["C"][0], a["M"][0])
+            assert lex == (int(f[eq + 1]), -int(f[eq + 2]))
+    assert seen == {"cost", "eq3", "greedy", "zigzag", "opt", "lex"}
 
 
 def _check_plan(lengths, capacity, n_mb, assign, tok, cst, k):

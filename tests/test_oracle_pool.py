@@ -165,6 +165,7 @@ def test_error_paths():
     with pytest.raises(PoolError) as e:
         pool.pack([sid], tagged_table(10, 8), out_rows_cap=17)
     assert e.value.code == "ECAPACITY"
+    assert pool.pack([sid], tagged_table(10, 8), out_rows_cap=18)[3] == 18     # exactly full is fine
     pool.free(sid)
     for call in (lambda: pool.free(sid), lambda: pool.pack([sid], None)):
         with pytest.raises(PoolError) as e:
