@@ -90,6 +90,22 @@ MUTANTS = [
      "an image after the last text token refused"),
     ("pool", "page[off // self.rb] = vis_rows[v]", "page[(off // self.rb) ^ 1] = vis_rows[v]",
      "producer rows swapped in pairs inside a page"),
+    ("pool", "self.region_start = [gva_start, gva_start + world_size * self.max_size[0]]",
+     "self.region_start = [gva_start, gva_start + self.max_size[0]]", "DRAM region after one rank's HBM segment"),
+    ("pool", "self.seg_start = [self.region_start[t] + rank * self.max_size[t] for t in (0, 1)]",
+     "self.seg_start = [self.region_start[t] + rank * self.max_size[0] for t in (0, 1)]",
+     "rank segments sized by the HBM tier"),
+    ("pool", "self.pb = page_tokens * self.rb", "self.pb = page_tokens * self.hidden", "page size in elements"),
+    ("pool", "n_pages = -(-n_vis // self.P)", "n_pages = n_vis // self.P", "partial last page not allocated"),
+    ("pool", "if len(moving) > len(self.stack[tier]):", "if len(moving) >= len(self.stack[tier]):",
+     "a migration that exactly fits refused"),
+    ("pool", "self.stack = [list(range(self.n_pages[0] - 1, -1, -1)),",
+     "self.stack = [list(range(self.n_pages[0])),", "HBM stack pops the highest page first"),
+    ("pool", "if self.vocab is not None and T and (text_ids.min() < 0 or text_ids.max() >= self.vocab):",
+     "if self.vocab is not None and T and (text_ids.min() < 0 or text_ids.max() > self.vocab):",
+     "a text id equal to the vocabulary size accepted"),
+    ("pool", "self.page_table[self.seg_start[t] + i * self.pb] = (t, order[i])",
+     "self.page_table[self.seg_start[t] + i * self.pb] = (t, i)", "frame order ignored"),
     # Planner: per-sample cost, Eq. 3, greedy and zig-zag partitions.
     ("plan", "return k * length + length * length", "return k * length + length", "cost without the square"),
     ("plan", "return sum(lengths) / capacity + (max(lengths) ** 2) / (capacity ** 2)",
@@ -219,7 +235,7 @@ def _first_failure(replaced, monkeypatch):
                         fn(**kwargs)
                     except pytest.skip.Exception:
                         pass
-                    except Exception as e:      # noqa: BLE001 - any failure of a pin counts
+                    except (Exception, pytest.fail.Exception) as e:   # noqa: BLE001 - any failure of a pin counts
                         return f"{pin.__name__}.{tname}({kwargs}): {type(e).__name__}"
     return None
 

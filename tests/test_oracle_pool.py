@@ -81,9 +81,14 @@ def test_gva_segments_and_translation():
     frame and offset that hold the row."""
     H, P = 8, 4
     for ws, rank in [(1, 0), (4, 2), (3, 2)]:
+        order = [list(range(9, -1, -1)), [3, 1, 4, 0, 5, 2]]
         pool = OraclePool(hidden=H, page_tokens=P, hbm_pages=10, host_pages=6, alloc="scatter",
-                          world_size=ws, rank=rank, frame_order=[list(range(9, -1, -1)), [3, 1, 4, 0, 5, 2]])
+                          world_size=ws, rank=rank, frame_order=order)
         mx = [10 * P * 2 * H, 6 * P * 2 * H]
+        # Page i of tier t is bound to frame order[t][i] (the permuted page table).
+        for t in (0, 1):
+            for i, f in enumerate(order[t]):
+                assert pool.translate(pool.seg_start[t] + i * pool.pb + 3) == (t, f, 3)
         assert pool.region_start[1] == pool.region_start[0] + ws * mx[0]
         rng = np.random.default_rng(ws)
         for i in range(5):
