@@ -43,7 +43,7 @@ def _spec(rng):
     return SampleSpec(rng.integers(0, VOCAB, size=t).astype(np.int32), pos, ntok)
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(224))
 def test_random_interleavings(fp, seed):
     say(f"case chaos seed={seed}")
     rng = np.random.default_rng(7700 + seed)

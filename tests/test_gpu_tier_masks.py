@@ -84,7 +84,7 @@ def _check_masks(fp, pool, ids, opool, oids, t_dev, table, vocab, hidden, total,
     assert np.array_equal(to_host(full[:m]), opool.pack(oids, table)[0])
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(440))
 def test_random_tier_masks(fp, seed):
     rng = np.random.default_rng(7100 + seed)
     hidden = int(rng.choice([8, 24, 64, 200, 1024, 4096, 5120]))
