@@ -160,8 +160,9 @@ void fp_config_init(fp_pool_config* cfg);
  * failed). */
 fp_status pool_create(const fp_pool_config* cfg, fp_pool** out);
 
-/* Destroy a pool and free all its memory. The caller must have synchronised
- * every stream that still uses it. NULL is accepted. */
+/* Destroy a pool and free all its memory (the library's; the paper describes
+ * no teardown). The caller must have synchronised every stream that still
+ * uses it. NULL is accepted. */
 fp_status pool_destroy(fp_pool* p);
 
 /* Producer write (Sec. 3.2: each producer writes vision embeddings and text
@@ -204,7 +205,8 @@ fp_status pool_write_sample(fp_pool* p, const int32_t* text_ids, int32_t n_text,
  * Errors: ENOENT, ESTATE (a captured pack still holds the sample), EHIP. */
 fp_status pool_free_sample(fp_pool* p, uint64_t sample_id);
 
-/* Returns the resources of deferred frees whose packs have completed (with
+/* The library's side of pool_free_sample (the paper defines no release):
+ * returns the resources of deferred frees whose packs have completed (with
  * wait != 0, first waits for all of them), and forgets the events of writes
  * that have completed (all of them with wait != 0). *out_deferred_pages
  * (host, may be NULL) receives the pages still deferred. pool_write_sample reclaims by
@@ -267,7 +269,8 @@ fp_status plan_microbatches(fp_pool* p, const uint64_t* sample_ids, int32_t n,
                             int64_t* out_mb_cost_scaled, int32_t* out_mb_max_len,
                             int64_t* out_sample_cost_scaled, void* stream);
 
-/* The partition of plan_microbatches on given lengths and costs, host only
+/* The partition step of plan_microbatches (Sec. 3.4: samples balanced across
+ * microbatches by cost) on given lengths and costs, host only
  * (no pool, no GPU). lengths: host int32[n] >= 1; costs_scaled: host
  * int64[n]; outputs as in plan_microbatches. Errors: EINVAL. */
 fp_status plan_partition(const int32_t* lengths, const int64_t* costs_scaled, int32_t n,
@@ -344,7 +347,7 @@ fp_status plan_dynamic_packing(const int32_t* lengths, int32_t n, int32_t capaci
                                int64_t* out_mb_cost_scaled, int32_t* out_mb_bucket,
                                int32_t* out_mb_rank, int32_t* out_mb_slot);
 
-/* plan_dynamic_packing over resident samples: sequence i is sample_ids[i]
+/* plan_dynamic_packing (Alg. 1, Sec. 3.4) over resident samples: sequence i is sample_ids[i]
  * with its pool length (text + image rows). Errors: EINVAL (also a sample
  * longer than capacity), ENOENT. */
 fp_status plan_pool_packing(fp_pool* p, const uint64_t* sample_ids, int32_t n, int32_t capacity,
@@ -407,7 +410,8 @@ fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_
                                   int32_t* out_n_tokens, int32_t* out_max_seqlen,
                                   int32_t tier_mask, void* stream);
 
-/* Lets the pool forget `stream` before the caller destroys it: wherever the
+/* The library's (not an operation of the paper): lets the pool forget
+ * `stream` before the caller destroys it: wherever the
  * pool remembers the stream as a reader of a sample (a pack ran there) or as
  * the stream of a sample's write, one event recorded now on the stream, after
  * the work queued there, takes its place (no event if the stream is idle).
@@ -415,7 +419,8 @@ fp_status pack_microbatch_noalloc(fp_pool* p, const uint64_t* sample_ids, int32_
  * Not on a capturing stream. Errors: ESTATE, EHIP. */
 fp_status pool_forget_stream(fp_pool* p, void* stream);
 
-/* Ends the hold that captured packs have on their samples (see HIP graphs
+/* The library's (not an operation of the paper): ends the hold that
+ * captured packs have on their samples (see HIP graphs
  * above): call it with a captured pack's sample id list (host uint64[n], in
  * any order; an id listed twice releases two captures of it) once no graph
  * holding that pack will be replayed again. Afterwards the samples may be
@@ -427,7 +432,8 @@ fp_status pool_release_captured(fp_pool* p, const uint64_t* sample_ids, int32_t 
 fp_status pool_stats(const fp_pool* p, int64_t* free_hbm_pages, int64_t* free_host_pages,
                      int64_t* n_samples);
 
-/* Page GVAs of a sample in visual-row order. gvas: host uint64[cap]; *n (host)
+/* Page GVAs of a sample in visual-row order (Sec. 3.2: a sample's visual
+ * embeddings are referenced by GVAs). gvas: host uint64[cap]; *n (host)
  * receives the page count even when cap is too small (then EINVAL). */
 fp_status pool_sample_pages(const fp_pool* p, uint64_t sample_id, uint64_t* gvas,
                             int32_t cap, int32_t* n);
@@ -436,11 +442,13 @@ fp_status pool_sample_pages(const fp_pool* p, uint64_t sample_id, uint64_t* gvas
 fp_status pool_sample_info(const fp_pool* p, uint64_t sample_id, int32_t* length,
                            int32_t* n_text, int32_t* n_vis);
 
-/* Translate a GVA through the page table: *tier (FP_TIER_*) and *phys, the
+/* Translate a GVA through the page table (Sec. 3.2: translation is local to
+ * the rank): *tier (FP_TIER_*) and *phys, the
  * device-visible address of that byte. Errors: EINVAL (unmapped GVA). */
 fp_status pool_translate(const fp_pool* p, uint64_t gva, int32_t* tier, uint64_t* phys);
 
-/* GVA layout: region starts and this rank's segment starts for the two tiers
+/* GVA layout (Sec. 3.2: per tier a region of world_size segments): region
+ * starts and this rank's segment starts for the two tiers
  * (host uint64[2] each, may be NULL) and the page size in bytes. */
 fp_status pool_layout(const fp_pool* p, uint64_t* region_start, uint64_t* segment_start,
                       int64_t* page_bytes);
