@@ -9,6 +9,7 @@ surrogates of small clusters; ECAPACITY when nothing fits.
 import numpy as np
 import pytest
 
+from conftest import golden_solves
 from oracle.allocate import candidates, solve
 from paper_2606_23087_amd.workloads import allocator_tables
 
@@ -30,6 +31,14 @@ def _check(mods, budget):
         return
     got = fp.plan_allocation(mods, budget)
     assert (got["choice"], got["G"], got["F"], got["devices"]) == tuple(want)
+
+
+def test_worked_examples_match():
+    """The hand-worked cases (tests/golden/allocator_flow_example.txt),
+    ties included, give the library the same answers as the oracle."""
+    for mods, budget, want in golden_solves():
+        assert (solve(mods, budget) is None) == (want is None)
+        _check(mods, budget)
 
 
 @pytest.mark.parametrize("seed", range(25))

@@ -1,0 +1,238 @@
+"""The library's host-side solvers are held to the oracle closely enough to
+catch plausible mistakes (CPU only).
+
+The dynamic packing scheduler (csrc/schedule.cpp: Alg. 1) and the allocator
+(csrc/allocate.cpp: candidate pruning and the flow matching of Eq. 1-2) are
+plain C++. Each mutant below edits one expression of one of them; the edited
+source is compiled with g++ into a small test library beside an unchanged
+copy of the other, and run on the inputs the library tests use
+(tests/test_schedule_lib.py, tests/test_allocate_lib.py) against the oracle:
+every mutant must give a different result somewhere. The real sources,
+compiled the same way, must agree with the oracle everywhere, so that a
+mutant's difference comes from its edit.
+"""
+
+import ctypes as C
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from conftest import golden_solves
+from oracle.allocate import candidates, solve
+from oracle.schedule import dynamic_packing
+from paper_2606_23087_amd.workloads import allocator_tables
+
+CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2606_23087_amd", "csrc")
+
+SHIM = r"""
+#include <cstddef>
+#include "schedule.h"
+#include "allocate.h"
+using std::size_t;
+extern "C" {
+int m_sched(const int32_t* lengths, int32_t n, int32_t L, int32_t N, int32_t K, int32_t* mb_of_seq,
+            int32_t* per_mb, int64_t* cost, int32_t cap) {
+  fp::PackingPlan p;
+  fp::dynamic_packing(lengths, n, L, N, K, &p);
+  const int32_t m = (int32_t)p.tokens.size();
+  if (m > cap) return -1;
+  for (int32_t i = 0; i < n; ++i) mb_of_seq[i] = p.mb_of_seq[(size_t)i];
+  for (int32_t j = 0; j < m; ++j) {
+    per_mb[5 * j] = p.tokens[(size_t)j];
+    per_mb[5 * j + 1] = p.max_len[(size_t)j];
+    per_mb[5 * j + 2] = p.bucket[(size_t)j];
+    per_mb[5 * j + 3] = p.rank[(size_t)j];
+    per_mb[5 * j + 4] = p.slot[(size_t)j];
+    cost[j] = p.cost[(size_t)j];
+  }
+  return m;
+}
+int m_cands(int32_t backbone, int32_t devices, int32_t per_node, int32_t gb, int32_t layers, int32_t* out,
+            int32_t cap) {
+  const std::vector<fp::Config> v = fp::prune_candidates(backbone != 0, devices, per_node, gb, layers);
+  if ((int32_t)v.size() > cap) return -1;
+  for (size_t i = 0; i < v.size(); ++i) {
+    out[3 * i] = v[i].dp;
+    out[3 * i + 1] = v[i].tp;
+    out[3 * i + 2] = v[i].pp;
+  }
+  return (int32_t)v.size();
+}
+int m_flow(int32_t n_mod, const int32_t* n_cfg, const int64_t* tau, const int64_t* cost, int64_t budget,
+           int32_t* choice, int64_t* gfd) {
+  std::vector<std::vector<int64_t>> t((size_t)n_mod), c((size_t)n_mod);
+  for (int32_t i = 0, at = 0; i < n_mod; ++i)
+    for (int32_t k = 0; k < n_cfg[i]; ++k, ++at) {
+      t[(size_t)i].push_back(tau[at]);
+      c[(size_t)i].push_back(cost[at]);
+    }
+  fp::FlowChoice f;
+  if (!fp::flow_match(t, c, budget, &f)) return 0;
+  for (int32_t i = 0; i < n_mod; ++i) choice[i] = f.choice[(size_t)i];
+  gfd[0] = f.G;
+  gfd[1] = f.F;
+  gfd[2] = f.devices;
+  return 1;
+}
+}
+"""
+
+# (source file, text of the real source, its mutated form, the slip)
+MUTANTS = [
+    ("schedule.cpp", "while (i < (size_t)size_) i = (t_[2 * i] >= l) ? 2 * i : 2 * i + 1;",
+     "while (i < (size_t)size_) i = (t_[2 * i] > l) ? 2 * i : 2 * i + 1;", "best-fit descent refuses an exact fit"),
+    ("schedule.cpp", "if (t_[1] < l) return -1;", "if (t_[1] <= l) return -1;", "no fit when the largest residual equals l"),
+    ("schedule.cpp", "j = *at[r].begin();", "j = *at[r].rbegin();", "best-fit ties go to the newest microbatch"),
+    ("schedule.cpp", "if (residual[(size_t)j] >= l_min) enter(j);", "if (residual[(size_t)j] > l_min) enter(j);",
+     "a microbatch closed while the shortest sequence still fits"),
+    ("schedule.cpp", "out->max_len[(size_t)j] = std::max(out->max_len[(size_t)j], l);",
+     "out->max_len[(size_t)j] = l;", "longest length of a microbatch is its last"),
+    ("schedule.cpp", "out->cost[j] = (int64_t)capacity * out->tokens[j] + (int64_t)out->max_len[j] * out->max_len[j];",
+     "out->cost[j] = (int64_t)out->tokens[j] + (int64_t)out->max_len[j] * out->max_len[j];",
+     "Eq. 3 without the factor L"),
+    ("schedule.cpp", "return da * b.count < db * a.count;", "return da * b.count <= db * a.count;",
+     "k-means ties to the higher bucket"),
+    ("schedule.cpp", "x[(size_t)order[(size_t)((2 * k + 1) * m / (2 * k_n))]]", "x[(size_t)order[(size_t)(k * m / k_n)]]",
+     "k-means started at other positions"),
+    ("schedule.cpp", "if (acc[(size_t)k].count) c[(size_t)k] = acc[(size_t)k];", "c[(size_t)k] = acc[(size_t)k];",
+     "an empty cluster loses its centroid"),
+    ("schedule.cpp", "for (int32_t b = n_b - 1; b >= 0; --b) {", "for (int32_t b = 0; b < n_b; ++b) {",
+     "buckets dealt cheapest first"),
+    ("schedule.cpp", "return out->cost[(size_t)u] > out->cost[(size_t)v];", "return out->cost[(size_t)u] < out->cost[(size_t)v];",
+     "a bucket dealt cheapest first"),
+    ("schedule.cpp", "      forward = !forward;", "      forward = true;", "round-robin instead of zig-zag"),
+    ("allocate.cpp", "if ((int64_t)dp * tp * pp > devices) break;", "if ((int64_t)dp * tp * pp >= devices) break;",
+     "device bound made strict"),
+    ("allocate.cpp", "if (layers > 0 && layers % pp) continue;", "if (layers > 0 && pp > layers) continue;",
+     "PP degree not tied to the layer count"),
+    ("allocate.cpp", "for (int32_t tp = 1; tp <= per_node; ++tp) {", "for (int32_t tp = 1; tp < per_node; ++tp) {",
+     "TP of a whole node left out"),
+    ("allocate.cpp", "if (c.cost <= budget) combos.push_back(std::move(c));", "if (c.cost < budget) combos.push_back(std::move(c));",
+     "encoders that exactly fill the budget refused"),
+    ("allocate.cpp", "cand.G = std::min(c.sum, tb[b]);", "cand.G = std::max(c.sum, tb[b]);",
+     "throughput of the faster side"),
+    ("allocate.cpp", "if (x.F != y.F) return x.F < y.F;", "if (x.F != y.F) return x.F > y.F;", "mismatch maximised"),
+    ("allocate.cpp", "if (x.devices != y.devices) return x.devices < y.devices;",
+     "if (x.devices != y.devices) return x.devices > y.devices;", "more devices preferred on ties"),
+    ("allocate.cpp", "if (g < 0) g = tree.last_fit(left);", "", "no fallback to the largest encoder sum below the backbone's"),
+    ("allocate.cpp", "const int64_t lo = (int64_t)(std::lower_bound(gsum.begin(), gsum.end(), tb[b]) - gsum.begin());",
+     "const int64_t lo = (int64_t)(std::upper_bound(gsum.begin(), gsum.end(), tb[b]) - gsum.begin());",
+     "an encoder sum equal to the backbone's skipped"),
+]
+
+
+def _gxx():
+    g = shutil.which("g++")
+    if not g:
+        pytest.skip("g++ not found")
+    return g
+
+
+def _build(dirname, sources):
+    """Compile the shim with the given (name -> text) sources into dirname."""
+    for name, text in sources.items():
+        with open(os.path.join(dirname, name), "w") as f:
+            f.write(text)
+    with open(os.path.join(dirname, "shim.cpp"), "w") as f:
+        f.write(SHIM)
+    lib = os.path.join(dirname, "libmut.so")
+    cmd = [_gxx(), "-std=c++17", "-O1", "-shared", "-fPIC", "-I", CSRC, "-o", lib,
+           os.path.join(dirname, "shim.cpp")] + [os.path.join(dirname, n) for n in sources]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return C.CDLL(lib)
+
+
+def _real(name):
+    with open(os.path.join(CSRC, name)) as f:
+        return f.read()
+
+
+def _sched_inputs():
+    out = [([19, 26, 32], 33, 2, 2)]                       # an exact k-means tie
+    for L in (64, 512, 2048, 8192, 32768):
+        for seed in (0, 1, 2):
+            rng = np.random.default_rng([seed, L])
+            n = int(rng.integers(50, 400))
+            N, K = int(rng.integers(1, 9)), int(rng.integers(1, 6))
+            text = np.clip(np.round(rng.lognormal(np.log(400), 0.8, size=n)), 16, 4096)
+            imgs = rng.integers(0, 5, size=n) * rng.integers(64, 1281, size=n)
+            out.append(([int(x) for x in np.clip(text + imgs, 1, L)], L, N, K))
+    L = 100
+    out += [([37], L, 2, 3), ([25] * 17, L, 2, 3), ([51, 99, 60, 100, 77], L, 2, 3), ([10, 90, 45, 55, 3], L, 2, 50),
+            ([30] * 7, L, 16, 3), ([6, 5, 4, 3, 2, 2, 7, 1], 10, 2, 2), ([6, 6, 3, 2, 4], 10, 2, 2),
+            ([3] * 7, 10, 3, 2)]
+    return out
+
+
+def _alloc_inputs():
+    clusters = [(8, 4, 8, 4), (24, 8, 48, 12), (64, 8, 256, 28), (3, 2, 5, 7), (8, 4, 4, 0), (64, 8, 512, 0),
+                (6, 4, 6, 0)]
+    tables = [(mods, budget) for mods, budget, _ in golden_solves()]
+    for seed in range(25):
+        rng = np.random.default_rng([seed, 77])
+        n_mod = int(rng.integers(2, 5))
+        mods = [[(int(rng.integers(0, 60)), int(rng.integers(1, 8))) for _ in range(int(rng.integers(1, 6)))]
+                for _ in range(n_mod)]
+        tables += [(mods, b) for b in (0, 3, 8, 15, 40)]
+    for devices in (16, 32):
+        mods = allocator_tables(devices, devices, per_node=8, global_batch=64, layers=12, n_encoders=2,
+                                candidates_fn=candidates)
+        tables += [(mods, devices // 2), (mods, devices)]
+    return clusters, tables
+
+
+def _first_difference(lib):
+    """Runs the library-test inputs through `lib` and the oracle; returns the
+    first input whose results differ, or None."""
+    for lengths, L, N, K in _sched_inputs():
+        n = len(lengths)
+        arr = (C.c_int32 * n)(*lengths)
+        mb = (C.c_int32 * n)()
+        per = (C.c_int32 * (5 * n + 5))()
+        cost = (C.c_int64 * (n + 1))()
+        m = lib.m_sched(arr, n, L, N, K, mb, per, cost, n + 1)
+        want = dynamic_packing(lengths, L, N, K)
+        got = dict(n_mb=m, mb_of_seq=list(mb), mb_tokens=[per[5 * j] for j in range(m)],
+                   mb_max_len=[per[5 * j + 1] for j in range(m)], mb_cost_scaled=[cost[j] for j in range(m)],
+                   mb_bucket=[per[5 * j + 2] for j in range(m)], mb_rank=[per[5 * j + 3] for j in range(m)],
+                   mb_slot=[per[5 * j + 4] for j in range(m)])
+        if any(got[k] != want[k] for k in got):
+            return f"schedule L={L} N={N} K={K} n={n}"
+    clusters, tables = _alloc_inputs()
+    for cl in clusters:
+        for bb in (0, 1):
+            out = (C.c_int32 * (3 * 4096))()
+            k = lib.m_cands(bb, *cl, out, 4096)
+            if [tuple(out[3 * i:3 * i + 3]) for i in range(k)] != [tuple(c) for c in candidates(bool(bb), *cl)]:
+                return f"candidates {cl} backbone={bb}"
+    for mods, budget in tables:
+        n_cfg = [len(m) for m in mods]
+        tau = [t for m in mods for t, _ in m]
+        cst = [c for m in mods for _, c in m]
+        choice = (C.c_int32 * len(mods))()
+        gfd = (C.c_int64 * 3)()
+        ok = lib.m_flow(len(mods), (C.c_int32 * len(mods))(*n_cfg), (C.c_int64 * len(tau))(*tau),
+                        (C.c_int64 * len(cst))(*cst), C.c_int64(budget), choice, gfd)
+        want = solve(mods, budget)
+        got = (list(choice), gfd[0], gfd[1], gfd[2]) if ok else None
+        if (got is None) != (want is None) or (got is not None and got != tuple(want)):
+            return f"flow matching budget={budget} modules={n_cfg}"
+    return None
+
+
+def test_real_sources_match_the_oracle(tmp_path):
+    lib = _build(str(tmp_path), {n: _real(n) for n in ("schedule.cpp", "allocate.cpp")})
+    assert _first_difference(lib) is None
+
+
+@pytest.mark.parametrize("name,old,new,slip", MUTANTS, ids=[m[3] for m in MUTANTS])
+def test_library_checks_catch_mutant(tmp_path, name, old, new, slip):
+    sources = {n: _real(n) for n in ("schedule.cpp", "allocate.cpp")}
+    assert sources[name].count(old) == 1, f"the text to mutate is not found once in csrc/{name}"
+    sources[name] = sources[name].replace(old, new)
+    assert _first_difference(_build(str(tmp_path), sources)) is not None, \
+        f"the library checks miss the mutant '{slip}' of csrc/{name}"

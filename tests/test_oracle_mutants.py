@@ -169,6 +169,7 @@ MUTANTS = [
      "throughput of the faster side instead of the slower"),
     ("allocate", "key = (-g, f, cost, choice)", "key = (-g, -f, cost, choice)", "mismatch maximised"),
     ("allocate", "key = (-g, f, cost, choice)", "key = (f, -g, cost, choice)", "criteria in the wrong order"),
+    ("allocate", "key = (-g, f, cost, choice)", "key = (-g, f, -cost, choice)", "more devices preferred on ties"),
     ("allocate", "if cost > budget:", "if cost >= budget:", "budget made strict"),
     ("allocate", "t_enc = sum(enc[i][c][0] for i, c in enumerate(choice[:-1]))",
      "t_enc = max(enc[i][c][0] for i, c in enumerate(choice[:-1]))", "encoder throughputs not summed"),
