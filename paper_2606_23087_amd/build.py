@@ -49,6 +49,9 @@ def build_driver(verbose: bool = False) -> str:
     linked against the in-tree library and the HIP runtime."""
     rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
     tmp = DRIVER + ".tmp"
+    # The HIP runtime header, included by plain C through gcc rather than
+    # hipcc, needs its platform macro defined by the compiler line; the
+    # driver itself has one code path.
     cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__",
            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(rocm, "include"),
            DRIVER_SRC, "-o", tmp, "-L", HERE, "-lflowpool", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
