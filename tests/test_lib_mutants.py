@@ -1,12 +1,15 @@
 """The library's host-side solvers are held to the oracle closely enough to
 catch plausible mistakes (CPU only).
 
-The dynamic packing scheduler (csrc/schedule.cpp: Alg. 1) and the allocator
-(csrc/allocate.cpp: candidate pruning and the flow matching of Eq. 1-2) are
+The dynamic packing scheduler (csrc/schedule.cpp: Alg. 1), the allocator
+(csrc/allocate.cpp: candidate pruning and the flow matching of Eq. 1-2) and
+the planner's partition step (the function `greedy` of csrc/pool.hip, taken
+out of that file as text: the greedy and zig-zag policies of Sec. 3.4) are
 plain C++. Each mutant below edits one expression of one of them; the edited
-source is compiled with g++ into a small test library beside an unchanged
-copy of the other, and run on the inputs the library tests use
-(tests/test_schedule_lib.py, tests/test_allocate_lib.py) against the oracle:
+source is compiled with g++ into a small test library beside unchanged
+copies of the others, and run on the inputs the library tests use
+(tests/test_schedule_lib.py, tests/test_allocate_lib.py,
+tests/test_lib_cpu.py) against the oracle:
 every mutant must give a different result somewhere. The real sources,
 compiled the same way, must agree with the oracle everywhere, so that a
 mutant's difference comes from its edit.
@@ -22,16 +25,22 @@ import pytest
 
 from conftest import golden_solves
 from oracle.allocate import candidates, solve
+from oracle.plan import cost_scaled, greedy_partition, zigzag_partition
 from oracle.schedule import dynamic_packing
 from paper_2606_23087_amd.workloads import allocator_tables
 
-CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2606_23087_amd", "csrc")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2606_23087_amd", "csrc")
+INCLUDE = os.path.join(ROOT, "include")
 
 SHIM = r"""
 #include <cstddef>
 #include "schedule.h"
 #include "allocate.h"
+#include "flowpool.h"
 using std::size_t;
+fp_status fp_greedy(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity, int32_t n_mb,
+                    int32_t policy, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost, int32_t* mb_max);
 extern "C" {
 int m_sched(const int32_t* lengths, int32_t n, int32_t L, int32_t N, int32_t K, int32_t* mb_of_seq,
             int32_t* per_mb, int64_t* cost, int32_t cap) {
@@ -60,6 +69,10 @@ int m_cands(int32_t backbone, int32_t devices, int32_t per_node, int32_t gb, int
     out[3 * i + 2] = v[i].pp;
   }
   return (int32_t)v.size();
+}
+int m_part(const int32_t* lengths, const int64_t* costs, int32_t n, int32_t capacity, int32_t n_mb,
+           int32_t policy, int32_t* assign, int32_t* mb_tokens, int64_t* mb_cost, int32_t* mb_max) {
+  return fp_greedy(lengths, costs, n, capacity, n_mb, policy, assign, mb_tokens, mb_cost, mb_max);
 }
 int m_flow(int32_t n_mod, const int32_t* n_cfg, const int64_t* tau, const int64_t* cost, int64_t budget,
            int32_t* choice, int64_t* gfd) {
@@ -104,6 +117,22 @@ MUTANTS = [
     ("schedule.cpp", "return out->cost[(size_t)u] > out->cost[(size_t)v];", "return out->cost[(size_t)u] < out->cost[(size_t)v];",
      "a bucket dealt cheapest first"),
     ("schedule.cpp", "      forward = !forward;", "      forward = true;", "round-robin instead of zig-zag"),
+    ("greedy.cpp", "return costs[a] > costs[b] || (costs[a] == costs[b] && a < b);",
+     "return costs[a] > costs[b] || (costs[a] == costs[b] && a > b);", "equal-cost samples taken last index first"),
+    ("greedy.cpp", "return costs[a] > costs[b] || (costs[a] == costs[b] && a < b);",
+     "return costs[a] < costs[b] || (costs[a] == costs[b] && a < b);", "samples taken cheapest first"),
+    ("greedy.cpp", "        if (tok[(size_t)j] + lengths[i] <= capacity &&\n",
+     "        if (tok[(size_t)j] + lengths[i] < capacity &&\n", "greedy capacity made strict"),
+    ("greedy.cpp", "(best < 0 || cst[(size_t)j] < cst[(size_t)best]))", "(best < 0 || cst[(size_t)j] <= cst[(size_t)best]))",
+     "cost ties go to the higher microbatch"),
+    ("greedy.cpp", "const int j = (int)(r < n_mb ? r : period - 1 - r);", "const int j = (int)(r < n_mb ? r : period - r);",
+     "snake turns one position late"),
+    ("greedy.cpp", "const int64_t r = ((int64_t)pos + q) % period;", "const int64_t r = ((int64_t)pos + q + 1) % period;",
+     "snake starts one position late"),
+    ("greedy.cpp", "for (int64_t q = 0; q < period && best < 0; ++q) {", "for (int64_t q = 0; q < n_mb && best < 0; ++q) {",
+     "zig-zag tries half the snake"),
+    ("greedy.cpp", "mx[(size_t)best] = std::max(mx[(size_t)best], lengths[i]);", "mx[(size_t)best] = lengths[i];",
+     "longest length of a microbatch is its last"),
     ("allocate.cpp", "if ((int64_t)dp * tp * pp > devices) break;", "if ((int64_t)dp * tp * pp >= devices) break;",
      "device bound made strict"),
     ("allocate.cpp", "if (layers > 0 && layers % pp) continue;", "if (layers > 0 && pp > layers) continue;",
@@ -139,7 +168,7 @@ def _build(dirname, sources):
     with open(os.path.join(dirname, "shim.cpp"), "w") as f:
         f.write(SHIM)
     lib = os.path.join(dirname, "libmut.so")
-    cmd = [_gxx(), "-std=c++17", "-O1", "-shared", "-fPIC", "-I", CSRC, "-o", lib,
+    cmd = [_gxx(), "-std=c++17", "-O1", "-shared", "-fPIC", "-I", CSRC, "-I", INCLUDE, "-o", lib,
            os.path.join(dirname, "shim.cpp")] + [os.path.join(dirname, n) for n in sources]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
@@ -147,8 +176,19 @@ def _build(dirname, sources):
 
 
 def _real(name):
+    if name == "greedy.cpp":
+        # The partition step, taken out of pool.hip as text and renamed.
+        with open(os.path.join(CSRC, "pool.hip")) as f:
+            src = f.read()
+        start = src.index("fp_status greedy(")
+        end = src.index("\n}\n", start) + 3
+        return ("#include <algorithm>\n#include <numeric>\n#include <vector>\n#include \"flowpool.h\"\n"
+                + src[start:end].replace("fp_status greedy(", "fp_status fp_greedy(", 1))
     with open(os.path.join(CSRC, name)) as f:
         return f.read()
+
+
+SOURCES = ("schedule.cpp", "allocate.cpp", "greedy.cpp")
 
 
 def _sched_inputs():
@@ -202,6 +242,28 @@ def _first_difference(lib):
                    mb_slot=[per[5 * j + 4] for j in range(m)])
         if any(got[k] != want[k] for k in got):
             return f"schedule L={L} N={N} K={K} n={n}"
+    for seed in range(30):
+        rng = np.random.default_rng(seed)
+        n = int(rng.integers(0, 300))
+        M = int(rng.integers(1, 70))
+        K = int(rng.integers(1, 9000))
+        lengths = rng.integers(1, 5000, size=n)
+        if seed % 3 == 0 and n:
+            lengths = rng.choice([100, 200, 300], size=n)       # many ties
+        lengths = [int(x) for x in lengths]
+        Cap = int(rng.integers(5000, 40000))
+        costs = [cost_scaled(x, K) for x in lengths]
+        for policy, ref in ((0, greedy_partition), (1, zigzag_partition)):
+            assign = (C.c_int32 * max(n, 1))()
+            tok = (C.c_int32 * M)()
+            cst = (C.c_int64 * M)()
+            mx = (C.c_int32 * M)()
+            lib.m_part((C.c_int32 * max(n, 1))(*lengths), (C.c_int64 * max(n, 1))(*costs), n, Cap, M, policy,
+                       assign, tok, cst, mx)
+            a, t, c = ref(lengths, K, Cap, M)
+            want_mx = [max([lengths[i] for i in range(n) if a[i] == j], default=0) for j in range(M)]
+            if (list(assign)[:n], list(tok), list(cst), list(mx)) != (a, t, c, want_mx):
+                return f"partition seed={seed} policy={policy}"
     clusters, tables = _alloc_inputs()
     for cl in clusters:
         for bb in (0, 1):
@@ -225,13 +287,13 @@ def _first_difference(lib):
 
 
 def test_real_sources_match_the_oracle(tmp_path):
-    lib = _build(str(tmp_path), {n: _real(n) for n in ("schedule.cpp", "allocate.cpp")})
+    lib = _build(str(tmp_path), {n: _real(n) for n in SOURCES})
     assert _first_difference(lib) is None
 
 
 @pytest.mark.parametrize("name,old,new,slip", MUTANTS, ids=[m[3] for m in MUTANTS])
 def test_library_checks_catch_mutant(tmp_path, name, old, new, slip):
-    sources = {n: _real(n) for n in ("schedule.cpp", "allocate.cpp")}
+    sources = {n: _real(n) for n in SOURCES}
     assert sources[name].count(old) == 1, f"the text to mutate is not found once in csrc/{name}"
     sources[name] = sources[name].replace(old, new)
     assert _first_difference(_build(str(tmp_path), sources)) is not None, \
